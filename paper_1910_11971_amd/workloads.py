@@ -1,0 +1,144 @@
+"""Seeded synthetic workloads shaped like the paper's CNN layers.
+
+This module only draws random inputs; it holds none of the CCI method's
+arithmetic and is the one piece shared by the HIP path's tests/benchmark and
+the CPU oracle's checks.  Every draw uses numpy's PCG64 generator seeded per
+workload, standard normal samples in float64, scaled, then rounded to fp32
+(numpy cast, round-to-nearest-even) and, for bf16 inputs, rounded once more to
+bfloat16 by torch's conversion.  Draw order: activations X first, then the
+dense fp32 master weights W.
+
+The layer shapes stand in for the paper's ImageNet / CIFAR CNN layers
+(Sec. 6): no dataset is read.
+  fc256      single FC layer, fp32, X [64,256] ~ N(0,1), W [256,256] ~ N(0,1/256),
+             G=8, K=4 (50% sparse)
+  conv3x3    3x3 conv, batch 32, 56x56, 64->64, pad 1, stride 1, X bf16 ~ N(0,1),
+             W ~ N(0, 2/576), G=8, K=2 (75%), bf16 out (ResNet layer1 3x3)
+  conv1x1    1x1 bottleneck conv, batch 64, 14x14, 1024->256, X bf16 ~ ReLU(N(0,1)),
+             W ~ N(0, 2/1024), G=16, K=4 or 2 (75% / 87.5%)
+  fc4096     FC sweep, X bf16 [4096,4096] ~ N(0,1), W [4096,4096] ~ N(0,1/4096),
+             G=16, K in {1,2,4,8,16} (K=16 is the dense control)
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, replace
+
+import numpy as np
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    # activations: FC uses (N, C); conv uses NHWC (B, H, W, Cin) and a kernel
+    B: int
+    H: int
+    W: int
+    Cin: int
+    O: int
+    KH: int = 1
+    KW: int = 1
+    stride: int = 1
+    pad: int = 0
+    G: int = 8
+    K: int = 2
+    x_dtype: str = "bf16"      # "f32" | "bf16"
+    y_dtype: str = "bf16"      # "f32" | "bf16"
+    x_dist: str = "normal"     # "normal" | "relu_normal"
+    w_std: float = 1.0
+    seed: int = 0
+    conv: bool = False
+
+    # GEMM view ------------------------------------------------------------
+    @property
+    def Ho(self) -> int:
+        return (self.H + 2 * self.pad - self.KH) // self.stride + 1 if self.conv else self.H
+
+    @property
+    def Wo(self) -> int:
+        return (self.W + 2 * self.pad - self.KW) // self.stride + 1 if self.conv else self.W
+
+    @property
+    def N(self) -> int:
+        """GEMM rows: samples (FC) or output pixels (conv)."""
+        return self.B * self.Ho * self.Wo
+
+    @property
+    def C(self) -> int:
+        """GEMM reduction length: inputs (FC) or KH*KW*Cin (conv)."""
+        return self.KH * self.KW * self.Cin
+
+    @property
+    def nnz(self) -> int:
+        return self.O * self.C * self.K // self.G
+
+    @property
+    def x_shape(self):
+        return (self.B, self.H, self.W, self.Cin) if self.conv else (self.B * self.H * self.W, self.Cin)
+
+    def with_(self, **kw) -> "Workload":
+        return replace(self, **kw)
+
+
+def fc(name, N, C, O, **kw) -> Workload:
+    return Workload(name=name, B=N, H=1, W=1, Cin=C, O=O, conv=False, **kw)
+
+
+def conv(name, B, H, W, Cin, O, k, stride, pad, **kw) -> Workload:
+    return Workload(name=name, B=B, H=H, W=W, Cin=Cin, O=O, KH=k, KW=k,
+                    stride=stride, pad=pad, conv=True, **kw)
+
+
+WORKLOADS = {
+    "fc256": fc("fc256", 64, 256, 256, G=8, K=4, x_dtype="f32", y_dtype="f32",
+                w_std=(1 / 256) ** 0.5),
+    "conv3x3": conv("conv3x3", 32, 56, 56, 64, 64, 3, 1, 1, G=8, K=2,
+                    w_std=(2 / 576) ** 0.5),
+    "conv1x1_k4": conv("conv1x1_k4", 64, 14, 14, 1024, 256, 1, 1, 0, G=16, K=4,
+                       x_dist="relu_normal", w_std=(2 / 1024) ** 0.5),
+    "conv1x1_k2": conv("conv1x1_k2", 64, 14, 14, 1024, 256, 1, 1, 0, G=16, K=2,
+                       x_dist="relu_normal", w_std=(2 / 1024) ** 0.5),
+}
+for _k in (1, 2, 4, 8, 16):
+    WORKLOADS[f"fc4096_k{_k}"] = fc(f"fc4096_k{_k}", 4096, 4096, 4096, G=16, K=_k,
+                                    w_std=(1 / 4096) ** 0.5)
+
+
+def draw(wl: Workload):
+    """Return (X, W): X a torch CPU tensor in wl.x_dtype with wl.x_shape,
+    W the dense fp32 master weights as numpy [O, C] (conv: [O, KH*KW*Cin] in
+    (kh, kw, cin) order)."""
+    import torch
+
+    rng = np.random.Generator(np.random.PCG64(wl.seed))
+    x = rng.standard_normal(wl.x_shape)
+    if wl.x_dist == "relu_normal":
+        x = np.maximum(x, 0.0)
+    x32 = x.astype(np.float32)
+    X = torch.from_numpy(x32)
+    if wl.x_dtype == "bf16":
+        X = X.to(torch.bfloat16)
+    w = rng.standard_normal((wl.O, wl.C)) * wl.w_std
+    W = np.ascontiguousarray(w.astype(np.float32))
+    return X, W
+
+
+def draw_epilogue(wl: Workload, *, scale=True, bias=True, residual=False, seed_offset=1000):
+    """Optional fused-epilogue operands: per-output fp32 scale and bias and a
+    residual shaped like Y (in wl.y_dtype).  Drawn from their own stream."""
+    import torch
+
+    rng = np.random.Generator(np.random.PCG64(wl.seed + seed_offset))
+    out = {}
+    if scale:
+        out["scale"] = torch.from_numpy((0.5 + rng.random(wl.O)).astype(np.float32))
+    if bias:
+        out["bias"] = torch.from_numpy((0.1 * rng.standard_normal(wl.O)).astype(np.float32))
+    if residual:
+        r = torch.from_numpy(rng.standard_normal((wl.N, wl.O)).astype(np.float32))
+        out["residual"] = r.to(torch.bfloat16) if wl.y_dtype == "bf16" else r
+    return out
+
+
+def small(wl: Workload, **kw) -> Workload:
+    """A reduced copy of a workload (same G, K, dtypes, distributions)."""
+    return wl.with_(**kw)

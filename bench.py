@@ -1,0 +1,259 @@
+#!/usr/bin/env python3
+"""Benchmark of the CCI-sparse forward path on one MI355X.
+
+One step = the whole hot path over one batch of synthetic input:
+  cci_pack (per-group top-K of the dense fp32 master weights -> packed bf16
+  values + uint8 indices) followed by cci_conv_im2col (implicit-im2col
+  CCI-sparse convolution with fp32 accumulation, bf16 out).
+
+Default workload: 3x3 conv, batch 32, 56x56, 64->64, pad 1, stride 1, G=8,
+K=2 (75% sparse), X ~ N(0,1) bf16, W ~ N(0, 2/576).
+
+Metric: effective TFLOP/s = 2 * N * nnz / step time (N = output pixels,
+nnz = kept weights).  Inputs are resident in HBM before timing starts; X and
+Y rotate over enough copies (> 2x the 256 MB last-level cache) that no step
+reads its activations from cache.
+
+Prints one JSON line.  Extra objects: `roofline` of the dominant kernel
+(timed with HIP events on its own stream), `cpu_baseline` (the CPU oracle on a
+bounded sample, host cores), `dense_bf16` (torch/hipBLASLt GEMM on the
+explicit im2col matrix and MIOpen conv2d of the same shape, for the speedup).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, HERE)
+
+PEAK = {"hbm_GBps": 8000.0, "mfma_bf16_TFLOPs": 2516.6, "valu_fp32_TFLOPs": 157.3}
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--workload", default="conv3x3")
+    p.add_argument("--algo", default="auto", choices=["auto", "sparse_mac", "dense_tile_mfma"])
+    p.add_argument("--rotate-mb", type=float, default=600.0,
+                   help="total size of rotated X/Y copies (0: no rotation)")
+    p.add_argument("--cpu-seconds", type=float, default=12.0, help="target wall time of the CPU oracle sample")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-dense", action="store_true")
+    return p.parse_args()
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(HERE, "paper_1910_11971_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(workload: str, kernel: str, src_hash: str):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
+    taken on the current kernel sources."""
+    path = os.path.join(HERE, "profiles", f"traffic_{kernel}_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.load(f)
+    if d.get("source_hash") != src_hash:
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the CCI path has no multi-GPU part in this build "
+              "(rows or output groups would shard with no exchange; see DESIGN.md). Use --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_1910_11971_amd import cci, workloads
+
+    wl = workloads.WORKLOADS[args.workload]
+    if not wl.conv:
+        raise SystemExit("bench.py times the convolution workloads (conv3x3, conv1x1_k4, conv1x1_k2)")
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    X_cpu, W_np = workloads.draw(wl)
+    xdt = torch.bfloat16 if wl.x_dtype == "bf16" else torch.float32
+    ydt = torch.bfloat16 if wl.y_dtype == "bf16" else torch.float32
+    vdt = xdt
+    stride, pad = (wl.stride, wl.stride), (wl.pad, wl.pad)
+
+    # ---- resident inputs, rotated copies --------------------------------------
+    x_bytes = X_cpu.numel() * X_cpu.element_size()
+    y_bytes = wl.N * wl.O * (2 if ydt == torch.bfloat16 else 4)
+    ncopy = 1 if args.rotate_mb <= 0 else max(1, int(np.ceil(args.rotate_mb * 1e6 / (x_bytes + y_bytes))))
+    X0 = X_cpu.to(dev)
+    Xs = [X0] + [X0.clone() for _ in range(ncopy - 1)]
+    Ys = [torch.empty((wl.B, wl.Ho, wl.Wo, wl.O), dtype=ydt, device=dev) for _ in range(ncopy)]
+    W = torch.from_numpy(W_np).to(dev)
+    vals = torch.empty((wl.O // wl.G, wl.K, wl.C), dtype=vdt, device=dev)
+    idx = torch.empty((wl.O // wl.G, wl.K, wl.C), dtype=torch.uint8, device=dev)
+
+    stream = torch.cuda.Stream(device=dev)  # default priority
+    algo = args.algo if args.algo != "auto" else cci.auto_algo(xdt, vdt, wl.N, wl.C, wl.Cin, wl.O, wl.G, wl.K)
+
+    def step(i, ev=None):
+        v, ix = cci.pack(W, wl.G, wl.K, vdt)
+        if ev is not None:
+            ev.record(stream)
+        cci.conv_im2col(Xs[i % ncopy], v, ix, wl.G, wl.KH, wl.KW, stride, pad, out_dtype=ydt, algo=algo,
+                        out=Ys[i % ncopy])
+
+    with torch.cuda.stream(stream):
+        for i in range(args.warmup):
+            step(i)
+        torch.cuda.synchronize()
+        # timed region: K whole steps; events between pack and conv give the
+        # dominant kernel's own duration on this stream
+        e_start = torch.cuda.Event(enable_timing=True)
+        e_end = torch.cuda.Event(enable_timing=True)
+        mids = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+        ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        e_start.record(stream)
+        for i in range(args.steps):
+            step(i, mids[i])
+            ends[i].record(stream)
+        e_end.record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+    ms_total = e_start.elapsed_time(e_end)
+    ms_step = ms_total / args.steps
+    conv_ms = [mids[i].elapsed_time(ends[i]) for i in range(args.steps)]
+    pack_ms = [(e_start if i == 0 else ends[i - 1]).elapsed_time(mids[i]) for i in range(args.steps)]
+    conv_avg = float(np.mean(conv_ms))
+    pack_avg = float(np.mean(pack_ms))
+
+    flop = 2.0 * wl.N * wl.nnz
+    value = flop / (ms_step * 1e-3) / 1e12
+
+    # ---- roofline of the dominant kernel (the convolution) ---------------------
+    val_b = 2 if vdt == torch.bfloat16 else 4
+    alg_bytes = x_bytes + wl.nnz * (val_b + 1) + y_bytes
+    dense_flop = 2.0 * wl.N * wl.C * wl.O
+    src_hash = kernel_source_hash()
+    kname = "cci_dense_tile" if algo == "dense_tile_mfma" else "cci_sparse_mac"
+    if algo == "dense_tile_mfma":
+        t_hbm = alg_bytes / (PEAK["hbm_GBps"] * 1e9)
+        t_mfma = dense_flop / (PEAK["mfma_bf16_TFLOPs"] * 1e12)
+        if t_hbm >= t_mfma:
+            ach = alg_bytes / (conv_avg * 1e-3) / 1e9
+            roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK["hbm_GBps"], "unit": "GB/s",
+                    "frac": round(ach / PEAK["hbm_GBps"], 4)}
+        else:
+            ach = flop / (conv_avg * 1e-3) / 1e12
+            roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK["mfma_bf16_TFLOPs"],
+                    "unit": "TFLOP/s", "frac": round(ach / PEAK["mfma_bf16_TFLOPs"], 4)}
+    else:
+        ach = flop / (conv_avg * 1e-3) / 1e12
+        roof = {"bound": "alu", "achieved": round(ach, 2), "peak": PEAK["valu_fp32_TFLOPs"], "unit": "TFLOP/s",
+                "frac": round(ach / PEAK["valu_fp32_TFLOPs"], 4)}
+    roof["traffic"] = load_traffic(args.workload, kname, src_hash)
+    roof["kernel"] = kname
+    roof["kernel_avg_us"] = round(conv_avg * 1e3, 3)
+    roof["algorithmic_bytes"] = int(alg_bytes)
+    roof["algorithmic_flop"] = flop
+
+    # ---- dense bf16 comparator --------------------------------------------------
+    dense = None
+    if not args.no_dense and xdt == torch.bfloat16:
+        with torch.cuda.stream(stream):
+            Wd = W.to(torch.bfloat16)                                  # [O, C] dense
+            if wl.KH == 1 and wl.stride == 1 and wl.pad == 0:
+                A = Xs[0].reshape(wl.N, wl.Cin)
+            else:
+                A = torch.nn.functional.unfold(Xs[0].permute(0, 3, 1, 2).float(), (wl.KH, wl.KW),
+                                               padding=wl.pad, stride=wl.stride)   # [B, Cin*k*k, L]
+                A = A.reshape(wl.B, wl.Cin, wl.KH, wl.KW, -1).permute(0, 4, 2, 3, 1).reshape(wl.N, wl.C)
+                A = A.to(torch.bfloat16).contiguous()
+            Bt = Wd.t().contiguous()
+            Xn = Xs[0].permute(0, 3, 1, 2)                             # channels_last view
+            Wc = W.reshape(wl.O, wl.KH, wl.KW, wl.Cin).permute(0, 3, 1, 2).to(torch.bfloat16).contiguous(
+                memory_format=torch.channels_last)
+
+            def timeit(fn, n):
+                for _ in range(5):
+                    fn()
+                torch.cuda.synchronize()
+                a = torch.cuda.Event(enable_timing=True)
+                b = torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                for _ in range(n):
+                    fn()
+                b.record(stream)
+                torch.cuda.synchronize()
+                return a.elapsed_time(b) / n
+
+            gemm_ms = timeit(lambda: torch.matmul(A, Bt), 50)
+            conv_ms_d = timeit(lambda: torch.nn.functional.conv2d(Xn, Wc, stride=wl.stride, padding=wl.pad), 50)
+        dense = {"gemm_explicit_im2col_ms": round(gemm_ms, 5), "miopen_conv2d_ms": round(conv_ms_d, 5),
+                 "speedup_vs_gemm": round(gemm_ms / conv_avg, 3), "speedup_vs_conv2d": round(conv_ms_d / conv_avg, 3),
+                 "note": "dense times are warm (inputs not rotated); CCI kernel time is rotated/cold"}
+        del A
+
+    # ---- CPU oracle baseline (rank 0, N=1 only) ---------------------------------
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        Xf = X_cpu.float().numpy()
+        t = time.perf_counter()
+        v32, ix = oracle.pack(W_np, wl.G, wl.K)
+        vb = oracle.bf16_bits_to_f32(oracle.bf16_rne(v32)) if vdt == torch.bfloat16 else v32
+        Wm = oracle.unpack(vb, ix, wl.G).reshape(wl.O, wl.KH, wl.KW, wl.Cin)
+        t_pack = time.perf_counter() - t
+        rng = np.random.default_rng(0)
+        n = 256
+        while True:
+            pix = np.sort(rng.choice(wl.N, size=min(n, wl.N), replace=False))
+            t = time.perf_counter()
+            oracle.conv2d_nhwc(Xf, Wm, stride, pad, pixels=pix)
+            dt = time.perf_counter() - t
+            if dt >= args.cpu_seconds or n >= wl.N:
+                break
+            n = min(wl.N, max(2 * n, int(n * args.cpu_seconds / max(dt, 1e-3) * 1.05)))
+        per_pix = dt / len(pix)
+        t_step = t_pack + per_pix * wl.N
+        cpu = {"value": round(flop / t_step / 1e12, 6), "unit": "TFLOP/s", "cores": oracle.num_threads(),
+               "kind": "oracle",
+               "sample": f"oracle pack of all {wl.O}x{wl.C} weights ({t_pack:.3f}s) + direct conv of "
+                         f"{len(pix)} of {wl.N} output pixels ({dt:.2f}s, double precision), "
+                         f"scaled to the full step"}
+
+    out = {
+        "metric": "CCI-sparse GEMM effective TFLOP/s (2*N*nnz) + speedup vs dense bf16 GEMM",
+        "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 6), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{wl.name}: conv {wl.KH}x{wl.KW} s{wl.stride} p{wl.pad}, batch {wl.B}, "
+                               f"{wl.H}x{wl.W}, {wl.Cin}->{wl.O}, G={wl.G}, K={wl.K}, bf16 in/out, fp32 acc",
+                   "N": wl.N, "C": wl.C, "O": wl.O, "G": wl.G, "K": wl.K, "nnz": wl.nnz, "algo": algo,
+                   "rotated_copies": ncopy},
+        "kernels_us": {"cci_pack": round(pack_avg * 1e3, 3), kname: round(conv_avg * 1e3, 3)},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "dense_bf16": dense,
+        "wall_s": round(wall, 3),
+        "source_hash": src_hash,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

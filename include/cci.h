@@ -1,0 +1,161 @@
+/*
+ * cci.h -- C ABI of the MI355X (gfx950) CCI-sparse forward path.
+ *
+ * Cross-channel intragroup (CCI) sparsity (Yu et al., arXiv:1910.11971):
+ * the weights W [O][C] of a layer are split into groups of G contiguous output
+ * channels at one input column; each group keeps exactly K nonzeros (the
+ * paper's s), stored packed as K values plus K intra-group row indices
+ * (Sec. 3.1, Fig. 1).  The forward product Y = X W^T is computed from the
+ * packed form (Sec. 3.2, Alg. 1); convolution is lowered to that product
+ * (Sec. 3.2).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Memory.  Every tensor argument is a device pointer to caller-owned,
+ *    contiguous, row-major memory on the current HIP device.  The library
+ *    never allocates, frees or synchronises, and keeps no state between calls
+ *    apart from a thread-local error string.
+ *  - Streams.  `stream` is a hipStream_t passed as void* (NULL = the default
+ *    stream).  Calls only enqueue work; results are ready once the stream is.
+ *  - Errors.  Arguments are validated before anything is enqueued; on a
+ *    validation failure the call returns a non-OK status and outputs are left
+ *    untouched.  A launch failure reported by the HIP runtime returns
+ *    CCI_EHIP.  cci_last_error() gives a message for the last failure on the
+ *    calling thread.  No C++ exception crosses this interface.
+ *  - Alignment.  Device pointers must be 16-byte aligned (CCI_EALIGN).
+ *  - Aliasing.  Outputs must not overlap any input.
+ *  - Limits.  1 <= K <= G <= 256; O % G == 0; C >= 1; N >= 0 (N == 0 is a
+ *    no-op).  The index is stored as one byte per kept weight.
+ *  - Arithmetic.  Products and sums are taken in fp32 (bf16 inputs widen
+ *    exactly); a bf16 output is rounded once, to nearest even, after the
+ *    fused epilogue.
+ */
+#ifndef CCI_H
+#define CCI_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  CCI_OK = 0,
+  CCI_EINVAL = 1,       /* bad sizes, null pointer, K/G/O out of range      */
+  CCI_EUNSUPPORTED = 2, /* valid request this build does not implement      */
+  CCI_EALIGN = 3,       /* a device pointer is not 16-byte aligned          */
+  CCI_EHIP = 4          /* the HIP runtime reported an error                */
+} cci_status;
+
+typedef enum { CCI_F32 = 0, CCI_BF16 = 1 } cci_dtype;
+
+/* Which kernel family computes a product.
+ *  CCI_ALGO_AUTO            the library's choice (cost model on the shape).
+ *  CCI_ALGO_SPARSE_MAC      Alg. 1 dataflow on the vector ALUs: only the K
+ *                           kept weights of each group are multiplied; the G
+ *                           outputs of a group stay in registers.  Any dtype
+ *                           combination and any C; G in {2,4,8,16,32}.
+ *  CCI_ALGO_DENSE_TILE_MFMA packed groups are expanded to dense bf16 tiles in
+ *                           LDS and multiplied on the matrix cores.  Needs
+ *                           bf16 X and vals, C % 32 == 0 (conv: Cin % 32 ==
+ *                           0) and 64 % G == 0.                              */
+typedef enum {
+  CCI_ALGO_AUTO = 0,
+  CCI_ALGO_SPARSE_MAC = 1,
+  CCI_ALGO_DENSE_TILE_MFMA = 2
+} cci_algo;
+
+/* Optional fused epilogue, applied per output element before rounding:
+ *   y = acc * scale[o] + bias[o] + residual[n][o];  y = max(y, 0) if relu.
+ * Any pointer may be NULL (scale = 1, bias = 0, residual = 0).  scale and
+ * bias are fp32 [O]; residual has Y's shape and dtype.  (Not from the paper:
+ * this is the folded batch-norm / residual / ReLU of a CNN layer.) */
+typedef struct {
+  const float *scale;
+  const float *bias;
+  const void *residual;
+  int32_t relu;
+} cci_epilogue;
+
+/* Byte sizes of the packed arrays for an [O][C] weight matrix with groups of
+ * G and K kept per group (Sec. 3.1: G rows compress to K rows of C entries).
+ * vals: [O/G][K][C] of val_t; idx: [O/G][K][C] uint8.  Pure host arithmetic. */
+cci_status cci_packed_sizes(int64_t O, int64_t C, int32_t G, int32_t K,
+                            cci_dtype val_t, size_t *val_bytes,
+                            size_t *idx_bytes);
+
+/* Magnitude projection onto CCI sparsity (Sec. 5.1: low-|w| weights are
+ * pruned; Sec. 3.1: exactly K per group).  For every group g and column c,
+ * among w_r = W[gG+r][c] keep the K largest |w| (equal |w|: lower r first;
+ * compared as fp32 bit patterns with the sign cleared, so NaN ranks above
+ * Inf) and write them in ascending r:
+ *   idx[g][k][c] = r,  vals[g][k][c] = w_r  (fp32 copy, or bf16 rounded to
+ *   nearest even when val_t == CCI_BF16).
+ * W: device fp32 [O][C] (conv: [O][KH][KW][Cin], C = KH*KW*Cin).
+ * vals, idx: device outputs of cci_packed_sizes() bytes.  Any G <= 256. */
+cci_status cci_pack(const float *W, int64_t O, int64_t C, int32_t G,
+                    int32_t K, void *vals, cci_dtype val_t, uint8_t *idx,
+                    void *stream);
+
+/* CCI-sparse product (Sec. 3.2, Alg. 1, generalised to K slots):
+ *   Y[n][o] = epilogue( sum_c sum_k [gG + idx[g][k][c] == o]
+ *                                     vals[g][k][c] * X[n][c] ),  g = o / G.
+ * X: device [N][C] of x_t.  vals/idx as produced by cci_pack.  Y: device
+ * [N][O] of y_t.  Supported (x_t, val_t, y_t): (F32, F32, F32) and
+ * (BF16, BF16, BF16 or F32); anything else is CCI_EUNSUPPORTED.
+ * algo selects the kernel family (see cci_algo); an explicit choice whose
+ * requirements the shape does not meet returns CCI_EUNSUPPORTED. */
+cci_status cci_spmm(const void *X, cci_dtype x_t, int64_t N, int64_t C,
+                    const void *vals, cci_dtype val_t, const uint8_t *idx,
+                    int64_t O, int32_t G, int32_t K, const cci_epilogue *ep,
+                    void *Y, cci_dtype y_t, cci_algo algo, void *stream);
+
+/* Convolution lowered to the CCI product (Sec. 3.2) without materialising
+ * the im2col matrix.  X: device NHWC [B][H][W][Cin].  The packed weights
+ * describe W [O][KH][KW][Cin] as an [O][C] matrix with C = KH*KW*Cin in
+ * (kh, kw, cin) order.  Output pixel p = (b*Ho + oh)*Wo + ow with
+ * Ho = (H + 2*pad_h - KH)/stride_h + 1 (Wo likewise); Y: device NHWC
+ * [B][Ho][Wo][O], i.e. [N][O] with N = B*Ho*Wo.  Input taps outside the
+ * image read as 0.  Dtypes, epilogue and algo as for cci_spmm. */
+cci_status cci_conv_im2col(const void *X, cci_dtype x_t, int64_t B, int64_t H,
+                           int64_t W, int64_t Cin, int32_t KH, int32_t KW,
+                           int32_t stride_h, int32_t stride_w, int32_t pad_h,
+                           int32_t pad_w, const void *vals, cci_dtype val_t,
+                           const uint8_t *idx, int64_t O, int32_t G, int32_t K,
+                           const cci_epilogue *ep, void *Y, cci_dtype y_t,
+                           cci_algo algo, void *stream);
+
+/* Which family CCI_ALGO_AUTO picks for a product of N x C x O (conv: pass
+ * N = B*Ho*Wo, C = KH*KW*Cin and cin = Cin; FC: cin = C).  Host-only. */
+cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C,
+                       int64_t cin, int64_t O, int32_t G, int32_t K);
+
+/* CNN glue for the ResNet-shaped forward (not from the paper).
+ * Max pooling, NHWC, window k, stride s, padding p (padding never wins).
+ * X, Y: device [B][H][W][C] -> [B][Ho][Wo][C] of dtype t (F32 or BF16). */
+cci_status cci_maxpool2d_nhwc(const void *X, cci_dtype t, int64_t B, int64_t H,
+                              int64_t W, int64_t C, int32_t k, int32_t s,
+                              int32_t p, void *Y, void *stream);
+
+/* Global average pooling, NHWC [B][H][W][C] of x_t -> [B][C] of y_t, summed
+ * in fp32 then divided by H*W. */
+cci_status cci_global_avgpool_nhwc(const void *X, cci_dtype x_t, int64_t B,
+                                   int64_t H, int64_t W, int64_t C, void *Y,
+                                   cci_dtype y_t, void *stream);
+
+/* Static description of a status code. */
+const char *cci_status_str(cci_status s);
+
+/* Message for the last non-OK status returned on the calling thread
+ * ("" if none).  Valid until the next library call on that thread. */
+const char *cci_last_error(void);
+
+/* Library version as MAJOR*10000 + MINOR*100 + PATCH. */
+int32_t cci_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CCI_H */

@@ -1,0 +1,203 @@
+"""Python binding of the C ABI in include/cci.h (argument marshalling only).
+
+Every function takes and returns torch tensors on a HIP device; the work is
+enqueued on the current torch stream of that device and runs in the HIP
+kernels of ``libcci.so``.  There is no fallback: if the library is missing,
+importing this module raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libcci.so")
+HEADER_PATH = os.path.join(os.path.dirname(_HERE), "include", "cci.h")
+
+OK, EINVAL, EUNSUPPORTED, EALIGN, EHIP = 0, 1, 2, 3, 4
+F32, BF16 = 0, 1
+ALGO_AUTO, ALGO_SPARSE_MAC, ALGO_DENSE_TILE_MFMA = 0, 1, 2
+ALGOS = {"auto": ALGO_AUTO, "sparse_mac": ALGO_SPARSE_MAC, "dense_tile_mfma": ALGO_DENSE_TILE_MFMA}
+
+
+class CCIError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"status {status}: {msg}")
+        self.status = status
+
+
+class Epilogue(ctypes.Structure):
+    _fields_ = [("scale", ctypes.c_void_p), ("bias", ctypes.c_void_p),
+                ("residual", ctypes.c_void_p), ("relu", ctypes.c_int32)]
+
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_1910_11971_amd.build`")
+
+# torch is imported first so that its HIP runtime (same soname) is the one
+# libcci.so binds to: one runtime per process.
+_lib = ctypes.CDLL(LIB_PATH)
+_vp, _i64, _i32, _sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+_lib.cci_packed_sizes.argtypes = [_i64, _i64, _i32, _i32, ctypes.c_int, ctypes.POINTER(_sz), ctypes.POINTER(_sz)]
+_lib.cci_pack.argtypes = [_vp, _i64, _i64, _i32, _i32, _vp, ctypes.c_int, _vp, _vp]
+_lib.cci_spmm.argtypes = [_vp, ctypes.c_int, _i64, _i64, _vp, ctypes.c_int, _vp, _i64, _i32, _i32,
+                          ctypes.POINTER(Epilogue), _vp, ctypes.c_int, ctypes.c_int, _vp]
+_lib.cci_conv_im2col.argtypes = [_vp, ctypes.c_int, _i64, _i64, _i64, _i64, _i32, _i32, _i32, _i32,
+                                 _i32, _i32, _vp, ctypes.c_int, _vp, _i64, _i32, _i32,
+                                 ctypes.POINTER(Epilogue), _vp, ctypes.c_int, ctypes.c_int, _vp]
+_lib.cci_auto_algo.argtypes = [ctypes.c_int, ctypes.c_int, _i64, _i64, _i64, _i64, _i32, _i32]
+_lib.cci_auto_algo.restype = ctypes.c_int
+_lib.cci_maxpool2d_nhwc.argtypes = [_vp, ctypes.c_int, _i64, _i64, _i64, _i64, _i32, _i32, _i32, _vp, _vp]
+_lib.cci_global_avgpool_nhwc.argtypes = [_vp, ctypes.c_int, _i64, _i64, _i64, _i64, _vp, ctypes.c_int, _vp]
+_lib.cci_status_str.argtypes = [ctypes.c_int]
+_lib.cci_status_str.restype = ctypes.c_char_p
+_lib.cci_last_error.restype = ctypes.c_char_p
+_lib.cci_version.restype = ctypes.c_int32
+for _fn in ("cci_packed_sizes", "cci_pack", "cci_spmm", "cci_conv_im2col", "cci_maxpool2d_nhwc",
+            "cci_global_avgpool_nhwc"):
+    getattr(_lib, _fn).restype = ctypes.c_int
+
+
+def raw():
+    """The loaded ctypes library (for ABI-level tests)."""
+    return _lib
+
+
+def header_functions() -> list[str]:
+    """Names of the functions include/cci.h declares."""
+    with open(HEADER_PATH) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(cci_[a-z0-9_]+)\s*\(", text)))
+
+
+def _check(status: int):
+    if status != OK:
+        raise CCIError(status, _lib.cci_last_error().decode() or _lib.cci_status_str(status).decode())
+
+
+def _code(dt: torch.dtype) -> int:
+    if dt == torch.float32:
+        return F32
+    if dt == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {dt}")
+
+
+def _ptr(t: torch.Tensor | None):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _dev(t: torch.Tensor) -> torch.Tensor:
+    if not t.is_cuda:
+        raise ValueError("tensor must be on a HIP device")
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    return t
+
+
+def _stream(t: torch.Tensor):
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _algo(algo) -> int:
+    return ALGOS[algo] if isinstance(algo, str) else int(algo)
+
+
+def version() -> int:
+    return int(_lib.cci_version())
+
+
+def packed_sizes(O: int, C: int, G: int, K: int, val_dtype=torch.bfloat16):
+    vb, ib = _sz(), _sz()
+    _check(_lib.cci_packed_sizes(O, C, G, K, _code(val_dtype), ctypes.byref(vb), ctypes.byref(ib)))
+    return vb.value, ib.value
+
+
+def pack(W: torch.Tensor, G: int, K: int, val_dtype=torch.bfloat16):
+    """cci_pack: W fp32 [O, C] (conv: [O, KH, KW, Cin]) -> (vals [O/G, K, C], idx uint8)."""
+    _dev(W)
+    if W.dtype != torch.float32:
+        raise TypeError("W must be float32")
+    O = W.shape[0]
+    C = W.numel() // max(O, 1)
+    if O % G:
+        raise ValueError("O must be a multiple of G")
+    vals = torch.empty((O // G, K, C), dtype=val_dtype, device=W.device)
+    idx = torch.empty((O // G, K, C), dtype=torch.uint8, device=W.device)
+    _check(_lib.cci_pack(_ptr(W), O, C, G, K, _ptr(vals), _code(val_dtype), _ptr(idx), _stream(W)))
+    return vals, idx
+
+
+def _epilogue(scale, bias, residual, relu):
+    for t in (scale, bias, residual):
+        if t is not None:
+            _dev(t)
+    return Epilogue(_ptr(scale), _ptr(bias), _ptr(residual), int(bool(relu)))
+
+
+def spmm(X: torch.Tensor, vals: torch.Tensor, idx: torch.Tensor, G: int, *, scale=None, bias=None,
+         residual=None, relu=False, out_dtype=None, algo="auto", out=None) -> torch.Tensor:
+    """cci_spmm: Y [N, O] = epilogue(X [N, C] . W_hat^T) from packed (vals, idx)."""
+    _dev(X), _dev(vals), _dev(idx)
+    N, C = X.shape
+    ng, K, C2 = vals.shape
+    if C2 != C or tuple(idx.shape) != tuple(vals.shape):
+        raise ValueError("shape mismatch between X and packed weights")
+    O = ng * G
+    out_dtype = out_dtype or X.dtype
+    Y = out if out is not None else torch.empty((N, O), dtype=out_dtype, device=X.device)
+    ep = _epilogue(scale, bias, residual, relu)
+    _check(_lib.cci_spmm(_ptr(X), _code(X.dtype), N, C, _ptr(vals), _code(vals.dtype), _ptr(idx), O, G, K,
+                         ctypes.byref(ep), _ptr(Y), _code(Y.dtype), _algo(algo), _stream(X)))
+    return Y
+
+
+def conv_out_hw(H, W, KH, KW, stride, pad):
+    return (H + 2 * pad[0] - KH) // stride[0] + 1, (W + 2 * pad[1] - KW) // stride[1] + 1
+
+
+def conv_im2col(X: torch.Tensor, vals: torch.Tensor, idx: torch.Tensor, G: int, KH: int, KW: int,
+                stride=(1, 1), pad=(0, 0), *, scale=None, bias=None, residual=None, relu=False,
+                out_dtype=None, algo="auto", out=None) -> torch.Tensor:
+    """cci_conv_im2col: NHWC X [B, H, W, Cin] -> NHWC Y [B, Ho, Wo, O]."""
+    _dev(X), _dev(vals), _dev(idx)
+    B, H, W, Cin = X.shape
+    ng, K, C = vals.shape
+    if C != KH * KW * Cin:
+        raise ValueError("packed weights do not match KH*KW*Cin")
+    O = ng * G
+    Ho, Wo = conv_out_hw(H, W, KH, KW, stride, pad)
+    out_dtype = out_dtype or X.dtype
+    Y = out if out is not None else torch.empty((B, Ho, Wo, O), dtype=out_dtype, device=X.device)
+    ep = _epilogue(scale, bias, residual, relu)
+    _check(_lib.cci_conv_im2col(_ptr(X), _code(X.dtype), B, H, W, Cin, KH, KW, stride[0], stride[1],
+                                pad[0], pad[1], _ptr(vals), _code(vals.dtype), _ptr(idx), O, G, K,
+                                ctypes.byref(ep), _ptr(Y), _code(Y.dtype), _algo(algo), _stream(X)))
+    return Y
+
+
+def auto_algo(x_dtype, val_dtype, N, C, cin, O, G, K) -> str:
+    code = _lib.cci_auto_algo(_code(x_dtype), _code(val_dtype), N, C, cin, O, G, K)
+    return {v: k for k, v in ALGOS.items()}[code]
+
+
+def maxpool2d_nhwc(X: torch.Tensor, k: int, s: int, p: int) -> torch.Tensor:
+    _dev(X)
+    B, H, W, C = X.shape
+    Ho, Wo = (H + 2 * p - k) // s + 1, (W + 2 * p - k) // s + 1
+    Y = torch.empty((B, Ho, Wo, C), dtype=X.dtype, device=X.device)
+    _check(_lib.cci_maxpool2d_nhwc(_ptr(X), _code(X.dtype), B, H, W, C, k, s, p, _ptr(Y), _stream(X)))
+    return Y
+
+
+def global_avgpool_nhwc(X: torch.Tensor, out_dtype=None) -> torch.Tensor:
+    _dev(X)
+    B, H, W, C = X.shape
+    Y = torch.empty((B, C), dtype=out_dtype or X.dtype, device=X.device)
+    _check(_lib.cci_global_avgpool_nhwc(_ptr(X), _code(X.dtype), B, H, W, C, _ptr(Y), _code(Y.dtype),
+                                        _stream(X)))
+    return Y

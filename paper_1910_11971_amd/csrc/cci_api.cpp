@@ -1,0 +1,254 @@
+// C ABI of the CCI library: argument validation, kernel-family choice and
+// error reporting.  Nothing here allocates, synchronises or keeps state other
+// than the calling thread's last error message.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "../../include/cci.h"
+#include "cci_launch.hpp"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+cci_status fail(cci_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+cci_status ok() {
+  g_last_error[0] = '\0';
+  return CCI_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool dtype_ok(cci_dtype t) { return t == CCI_F32 || t == CCI_BF16; }
+
+cci::DType to_dt(cci_dtype t) { return t == CCI_F32 ? cci::DType::F32 : cci::DType::BF16; }
+
+size_t dsize(cci_dtype t) { return t == CCI_F32 ? 4 : 2; }
+
+cci_status check_groups(int64_t O, int64_t C, int32_t G, int32_t K) {
+  if (G < 1 || G > 256) return fail(CCI_EINVAL, "G=%d outside [1, 256]", G);
+  if (K < 1 || K > G) return fail(CCI_EINVAL, "K=%d outside [1, G=%d]", K, G);
+  if (O < 1 || O % G != 0) return fail(CCI_EINVAL, "O=%lld is not a positive multiple of G=%d", (long long)O, G);
+  if (C < 1) return fail(CCI_EINVAL, "C=%lld < 1", (long long)C);
+  // packed arrays and grids are indexed with 64-bit offsets; keep element
+  // counts well inside what the launch grids can cover
+  if (O > (int64_t(1) << 31) || C > (int64_t(1) << 31) || O * C > (int64_t(1) << 40))
+    return fail(CCI_EINVAL, "O*C too large");
+  return CCI_OK;
+}
+
+cci_status check_types(cci_dtype x_t, cci_dtype val_t, cci_dtype y_t) {
+  if (!dtype_ok(x_t) || !dtype_ok(val_t) || !dtype_ok(y_t))
+    return fail(CCI_EINVAL, "unknown dtype code");
+  const bool f32 = x_t == CCI_F32 && val_t == CCI_F32 && y_t == CCI_F32;
+  const bool bf = x_t == CCI_BF16 && val_t == CCI_BF16;
+  if (!f32 && !bf)
+    return fail(CCI_EUNSUPPORTED, "dtype combination (x=%d, vals=%d, y=%d) not supported", x_t,
+                val_t, y_t);
+  return CCI_OK;
+}
+
+cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* ep,
+                       void* stream) {
+  a.scale = ep ? ep->scale : nullptr;
+  a.bias = ep ? ep->bias : nullptr;
+  a.residual = ep ? ep->residual : nullptr;
+  a.relu = ep ? ep->relu : 0;
+  if ((a.scale && !aligned16(a.scale)) || (a.bias && !aligned16(a.bias)) ||
+      (a.residual && !aligned16(a.residual)))
+    return fail(CCI_EALIGN, "epilogue pointer not 16-byte aligned");
+  if (algo != CCI_ALGO_AUTO && algo != CCI_ALGO_SPARSE_MAC && algo != CCI_ALGO_DENSE_TILE_MFMA)
+    return fail(CCI_EINVAL, "unknown algo %d", (int)algo);
+  if (a.N == 0) return ok();
+
+  const bool mac_ok = cci::sparse_mac_supports(a);
+  const bool tile_ok = cci::dense_tile_supports(a);
+  cci_algo chosen = algo;
+  if (algo == CCI_ALGO_AUTO) {
+    const int64_t cin = a.conv ? a.geom.Cin : a.C;
+    chosen = cci_auto_algo(a.x_t == cci::DType::F32 ? CCI_F32 : CCI_BF16,
+                           a.val_t == cci::DType::F32 ? CCI_F32 : CCI_BF16, a.N, a.C, cin, a.O,
+                           a.G, a.K);
+  }
+  if (chosen == CCI_ALGO_SPARSE_MAC && !mac_ok)
+    return fail(CCI_EUNSUPPORTED, "sparse-MAC kernels need G in {2,4,8,16,32} (G=%d)", a.G);
+  if (chosen == CCI_ALGO_DENSE_TILE_MFMA && !tile_ok)
+    return fail(CCI_EUNSUPPORTED,
+                "dense-tile MFMA kernels need bf16 X/vals, 64 %% G == 0 and C (conv: Cin) %% 32 == 0");
+  hipError_t e = chosen == CCI_ALGO_SPARSE_MAC ? cci::launch_sparse_mac(a, static_cast<hipStream_t>(stream))
+                                               : cci::launch_dense_tile(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(CCI_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t cci_version(void) { return 100; }
+
+const char* cci_status_str(cci_status s) {
+  switch (s) {
+    case CCI_OK: return "CCI_OK";
+    case CCI_EINVAL: return "CCI_EINVAL: invalid argument";
+    case CCI_EUNSUPPORTED: return "CCI_EUNSUPPORTED: not supported by this build";
+    case CCI_EALIGN: return "CCI_EALIGN: pointer not 16-byte aligned";
+    case CCI_EHIP: return "CCI_EHIP: HIP runtime error";
+  }
+  return "unknown cci_status";
+}
+
+const char* cci_last_error(void) { return g_last_error; }
+
+cci_status cci_packed_sizes(int64_t O, int64_t C, int32_t G, int32_t K, cci_dtype val_t,
+                            size_t* val_bytes, size_t* idx_bytes) {
+  if (cci_status s = check_groups(O, C, G, K)) return s;
+  if (!dtype_ok(val_t)) return fail(CCI_EINVAL, "unknown dtype code");
+  if (!val_bytes || !idx_bytes) return fail(CCI_EINVAL, "null output pointer");
+  const size_t n = static_cast<size_t>(O / G) * static_cast<size_t>(K) * static_cast<size_t>(C);
+  *val_bytes = n * dsize(val_t);
+  *idx_bytes = n;
+  return ok();
+}
+
+cci_status cci_pack(const float* W, int64_t O, int64_t C, int32_t G, int32_t K, void* vals,
+                    cci_dtype val_t, uint8_t* idx, void* stream) {
+  if (cci_status s = check_groups(O, C, G, K)) return s;
+  if (!dtype_ok(val_t)) return fail(CCI_EINVAL, "unknown dtype code");
+  if (!W || !vals || !idx) return fail(CCI_EINVAL, "null pointer");
+  if (!aligned16(W) || !aligned16(vals) || !aligned16(idx))
+    return fail(CCI_EALIGN, "pointer not 16-byte aligned");
+  hipError_t e = cci::launch_pack(W, O, C, G, K, vals, to_dt(val_t), idx,
+                                  static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(CCI_EHIP, "pack launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C, int64_t cin,
+                       int64_t O, int32_t G, int32_t K) {
+  (void)N;
+  (void)O;
+  (void)C;
+  // The matrix cores multiply the expanded tile at 2516.6 dense bf16 TFLOP/s;
+  // the vector ALUs multiply only kept weights at 78.6 fp32 TFLOP/s (no
+  // packed fp32).  Expanded work is G/K times the kept work, so the tile
+  // path wins whenever K/G > 78.6/2516.6 (about 1/32).
+  const bool tile_shape = x_t == CCI_BF16 && val_t == CCI_BF16 && G >= 1 && 64 % G == 0 &&
+                          cin % 32 == 0;
+  if (tile_shape && 32 * static_cast<int64_t>(K) > G) return CCI_ALGO_DENSE_TILE_MFMA;
+  return CCI_ALGO_SPARSE_MAC;
+}
+
+cci_status cci_spmm(const void* X, cci_dtype x_t, int64_t N, int64_t C, const void* vals,
+                    cci_dtype val_t, const uint8_t* idx, int64_t O, int32_t G, int32_t K,
+                    const cci_epilogue* ep, void* Y, cci_dtype y_t, cci_algo algo, void* stream) {
+  if (cci_status s = check_groups(O, C, G, K)) return s;
+  if (N < 0) return fail(CCI_EINVAL, "N=%lld < 0", (long long)N);
+  if (cci_status s = check_types(x_t, val_t, y_t)) return s;
+  if (N > 0 && (!X || !vals || !idx || !Y)) return fail(CCI_EINVAL, "null pointer");
+  if (N > (int64_t(1) << 40) / (C > O ? C : O)) return fail(CCI_EINVAL, "N too large");
+  if (N > 0 && (!aligned16(X) || !aligned16(vals) || !aligned16(idx) || !aligned16(Y)))
+    return fail(CCI_EALIGN, "pointer not 16-byte aligned");
+  cci::ProductArgs a{};
+  a.X = X;
+  a.x_t = to_dt(x_t);
+  a.N = N;
+  a.C = C;
+  a.conv = false;
+  a.vals = vals;
+  a.val_t = to_dt(val_t);
+  a.idx = idx;
+  a.O = O;
+  a.G = G;
+  a.K = K;
+  a.Y = Y;
+  a.y_t = to_dt(y_t);
+  return run_product(a, algo, ep, stream);
+}
+
+cci_status cci_conv_im2col(const void* X, cci_dtype x_t, int64_t B, int64_t H, int64_t W,
+                           int64_t Cin, int32_t KH, int32_t KW, int32_t stride_h, int32_t stride_w,
+                           int32_t pad_h, int32_t pad_w, const void* vals, cci_dtype val_t,
+                           const uint8_t* idx, int64_t O, int32_t G, int32_t K,
+                           const cci_epilogue* ep, void* Y, cci_dtype y_t, cci_algo algo,
+                           void* stream) {
+  if (B < 0 || H < 1 || W < 1 || Cin < 1 || KH < 1 || KW < 1 || stride_h < 1 || stride_w < 1 ||
+      pad_h < 0 || pad_w < 0)
+    return fail(CCI_EINVAL, "bad convolution geometry");
+  if (H > (1 << 20) || W > (1 << 20) || Cin > (1 << 24) || KH > 64 || KW > 64 ||
+      pad_h > 64 || pad_w > 64 || stride_h > 64 || stride_w > 64)
+    return fail(CCI_EINVAL, "convolution geometry out of range");
+  if (H + 2 * pad_h < KH || W + 2 * pad_w < KW) return fail(CCI_EINVAL, "kernel larger than padded input");
+  const int64_t C = static_cast<int64_t>(KH) * KW * Cin;
+  if (cci_status s = check_groups(O, C, G, K)) return s;
+  if (cci_status s = check_types(x_t, val_t, y_t)) return s;
+  const int64_t Ho = (H + 2 * pad_h - KH) / stride_h + 1;
+  const int64_t Wo = (W + 2 * pad_w - KW) / stride_w + 1;
+  const int64_t N = B * Ho * Wo;
+  if (B * H * W * Cin >= (int64_t(1) << 31)) return fail(CCI_EINVAL, "input tensor too large");
+  if (N > (int64_t(1) << 40) / (C > O ? C : O)) return fail(CCI_EINVAL, "output too large");
+  if (N > 0 && (!X || !vals || !idx || !Y)) return fail(CCI_EINVAL, "null pointer");
+  if (N > 0 && (!aligned16(X) || !aligned16(vals) || !aligned16(idx) || !aligned16(Y)))
+    return fail(CCI_EALIGN, "pointer not 16-byte aligned");
+  cci::ProductArgs a{};
+  a.X = X;
+  a.x_t = to_dt(x_t);
+  a.N = N;
+  a.C = C;
+  a.conv = true;
+  a.B = B;
+  a.geom = cci::ConvGeom{static_cast<int32_t>(H), static_cast<int32_t>(W),
+                         static_cast<int32_t>(Cin), KH, KW, stride_h, stride_w, pad_h, pad_w,
+                         static_cast<int32_t>(Ho), static_cast<int32_t>(Wo)};
+  a.vals = vals;
+  a.val_t = to_dt(val_t);
+  a.idx = idx;
+  a.O = O;
+  a.G = G;
+  a.K = K;
+  a.Y = Y;
+  a.y_t = to_dt(y_t);
+  return run_product(a, algo, ep, stream);
+}
+
+cci_status cci_maxpool2d_nhwc(const void* X, cci_dtype t, int64_t B, int64_t H, int64_t W,
+                              int64_t C, int32_t k, int32_t s, int32_t p, void* Y, void* stream) {
+  if (!dtype_ok(t)) return fail(CCI_EINVAL, "unknown dtype code");
+  if (B < 0 || H < 1 || W < 1 || C < 1 || k < 1 || s < 1 || p < 0 || 2 * p > k ||
+      H + 2 * p < k || W + 2 * p < k)
+    return fail(CCI_EINVAL, "bad pooling geometry");
+  if (B * H * W * C >= (int64_t(1) << 40)) return fail(CCI_EINVAL, "tensor too large");
+  if (B == 0) return ok();
+  if (!X || !Y) return fail(CCI_EINVAL, "null pointer");
+  if (!aligned16(X) || !aligned16(Y)) return fail(CCI_EALIGN, "pointer not 16-byte aligned");
+  hipError_t e = cci::launch_maxpool(X, to_dt(t), B, H, W, C, k, s, p, Y,
+                                     static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(CCI_EHIP, "maxpool launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+cci_status cci_global_avgpool_nhwc(const void* X, cci_dtype x_t, int64_t B, int64_t H, int64_t W,
+                                   int64_t C, void* Y, cci_dtype y_t, void* stream) {
+  if (!dtype_ok(x_t) || !dtype_ok(y_t)) return fail(CCI_EINVAL, "unknown dtype code");
+  if (B < 0 || H < 1 || W < 1 || C < 1) return fail(CCI_EINVAL, "bad pooling geometry");
+  if (B * H * W * C >= (int64_t(1) << 40)) return fail(CCI_EINVAL, "tensor too large");
+  if (B == 0) return ok();
+  if (!X || !Y) return fail(CCI_EINVAL, "null pointer");
+  if (!aligned16(X) || !aligned16(Y)) return fail(CCI_EALIGN, "pointer not 16-byte aligned");
+  hipError_t e = cci::launch_avgpool(X, to_dt(x_t), B, H, W, C, Y, to_dt(y_t),
+                                     static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(CCI_EHIP, "avgpool launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,90 @@
+// CNN glue for the ResNet-shaped forward: NHWC max pooling and global average
+// pooling.  Memory-bound elementwise/reduction kernels; one lane per output
+// element, consecutive lanes on consecutive channels (coalesced).
+#include "cci_launch.hpp"
+
+namespace cci {
+namespace {
+
+constexpr int kThreads = 256;
+
+template <typename T>
+__global__ __launch_bounds__(kThreads) void maxpool_kernel(const T* __restrict__ X, int64_t B,
+                                                           int64_t H, int64_t W, int64_t C,
+                                                           int32_t k, int32_t st, int32_t p,
+                                                           int64_t Ho, int64_t Wo,
+                                                           T* __restrict__ Y) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
+  const int64_t total = B * Ho * Wo * C;
+  if (e >= total) return;
+  const int64_t c = e % C;
+  const int64_t pix = e / C;
+  const int64_t ow = pix % Wo;
+  const int64_t oh = (pix / Wo) % Ho;
+  const int64_t b = pix / (Wo * Ho);
+  float m = -__builtin_inff();
+  for (int32_t i = 0; i < k; ++i) {
+    const int64_t ih = oh * st - p + i;
+    if (ih < 0 || ih >= H) continue;
+    for (int32_t jj = 0; jj < k; ++jj) {
+      const int64_t iw = ow * st - p + jj;
+      if (iw < 0 || iw >= W) continue;
+      const float v = io<T>::load(X, ((b * H + ih) * W + iw) * C + c);
+      m = v > m ? v : m;
+    }
+  }
+  io<T>::store(Y, e, m);  // exact: m is one of the inputs
+}
+
+template <typename XT, typename YT>
+__global__ __launch_bounds__(kThreads) void avgpool_kernel(const XT* __restrict__ X, int64_t B,
+                                                           int64_t HW, int64_t C,
+                                                           YT* __restrict__ Y) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
+  if (e >= B * C) return;
+  const int64_t c = e % C;
+  const int64_t b = e / C;
+  float acc = 0.0f;
+  for (int64_t i = 0; i < HW; ++i) acc += io<XT>::load(X, (b * HW + i) * C + c);
+  io<YT>::store(Y, e, acc / static_cast<float>(HW));
+}
+
+}  // namespace
+
+hipError_t launch_maxpool(const void* X, DType t, int64_t B, int64_t H, int64_t W, int64_t C,
+                          int32_t k, int32_t st, int32_t p, void* Y, hipStream_t s) {
+  const int64_t Ho = (H + 2 * p - k) / st + 1;
+  const int64_t Wo = (W + 2 * p - k) / st + 1;
+  const int64_t total = B * Ho * Wo * C;
+  const dim3 grid(static_cast<uint32_t>((total + kThreads - 1) / kThreads));
+  if (t == DType::F32)
+    hipLaunchKernelGGL((maxpool_kernel<float>), grid, dim3(kThreads), 0, s,
+                       static_cast<const float*>(X), B, H, W, C, k, st, p, Ho, Wo,
+                       static_cast<float*>(Y));
+  else
+    hipLaunchKernelGGL((maxpool_kernel<bf16_t>), grid, dim3(kThreads), 0, s,
+                       static_cast<const bf16_t*>(X), B, H, W, C, k, st, p, Ho, Wo,
+                       static_cast<bf16_t*>(Y));
+  return hipGetLastError();
+}
+
+hipError_t launch_avgpool(const void* X, DType x_t, int64_t B, int64_t H, int64_t W, int64_t C,
+                          void* Y, DType y_t, hipStream_t s) {
+  const dim3 grid(static_cast<uint32_t>((B * C + kThreads - 1) / kThreads));
+  const int64_t HW = H * W;
+  if (x_t == DType::F32 && y_t == DType::F32)
+    hipLaunchKernelGGL((avgpool_kernel<float, float>), grid, dim3(kThreads), 0, s,
+                       static_cast<const float*>(X), B, HW, C, static_cast<float*>(Y));
+  else if (x_t == DType::BF16 && y_t == DType::F32)
+    hipLaunchKernelGGL((avgpool_kernel<bf16_t, float>), grid, dim3(kThreads), 0, s,
+                       static_cast<const bf16_t*>(X), B, HW, C, static_cast<float*>(Y));
+  else if (x_t == DType::BF16 && y_t == DType::BF16)
+    hipLaunchKernelGGL((avgpool_kernel<bf16_t, bf16_t>), grid, dim3(kThreads), 0, s,
+                       static_cast<const bf16_t*>(X), B, HW, C, static_cast<bf16_t*>(Y));
+  else
+    hipLaunchKernelGGL((avgpool_kernel<float, bf16_t>), grid, dim3(kThreads), 0, s,
+                       static_cast<const float*>(X), B, HW, C, static_cast<bf16_t*>(Y));
+  return hipGetLastError();
+}
+
+}  // namespace cci

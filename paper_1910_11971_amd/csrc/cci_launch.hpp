@@ -1,0 +1,51 @@
+// Host-side launcher interface between the C ABI layer (cci_api.cpp) and the
+// kernel translation units.  Every launcher assumes validated arguments and
+// returns the HIP status of its launch.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "cci_device.hpp"
+
+namespace cci {
+
+enum class DType { F32 = 0, BF16 = 1 };
+
+struct ProductArgs {
+  const void* X;
+  DType x_t;
+  int64_t N, C;          // GEMM rows / reduction length
+  bool conv;
+  int64_t B;             // conv: batch
+  ConvGeom geom;         // conv only
+  const void* vals;
+  DType val_t;
+  const uint8_t* idx;
+  int64_t O;
+  int32_t G, K;
+  const float* scale;
+  const float* bias;
+  const void* residual;
+  int32_t relu;
+  void* Y;
+  DType y_t;
+};
+
+hipError_t launch_pack(const float* W, int64_t O, int64_t C, int32_t G, int32_t K,
+                       void* vals, DType val_t, uint8_t* idx, hipStream_t s);
+
+// Alg. 1 dataflow on the vector ALUs (any dtype combination, G in {2,4,8,16,32}).
+bool sparse_mac_supports(const ProductArgs& a);
+hipError_t launch_sparse_mac(const ProductArgs& a, hipStream_t s);
+
+// Packed groups expanded to dense bf16 tiles in LDS, bf16 MFMA.
+bool dense_tile_supports(const ProductArgs& a);
+hipError_t launch_dense_tile(const ProductArgs& a, hipStream_t s);
+
+hipError_t launch_maxpool(const void* X, DType t, int64_t B, int64_t H, int64_t W, int64_t C,
+                          int32_t k, int32_t st, int32_t p, void* Y, hipStream_t s);
+hipError_t launch_avgpool(const void* X, DType x_t, int64_t B, int64_t H, int64_t W, int64_t C,
+                          void* Y, DType y_t, hipStream_t s);
+
+}  // namespace cci

@@ -1,0 +1,112 @@
+// Magnitude projection onto CCI sparsity (paper Sec. 5.1 with the group
+// constraint of Sec. 3.1): one lane per (group g, column c).
+//
+// HBM-bound: reads the G weights of its group column (consecutive lanes read
+// consecutive columns, so each of the G row reads is coalesced), ranks them by
+// |w| and writes the K survivors (value + intra-group row) in ascending row
+// order -- again coalesced along c.
+#include "cci_launch.hpp"
+
+namespace cci {
+namespace {
+
+constexpr int kPackThreads = 256;
+
+__device__ __forceinline__ uint32_t abs_bits(float w) { return __float_as_uint(w) & 0x7fffffffu; }
+
+template <typename VT> __device__ __forceinline__ void put(VT* p, int64_t i, float w);
+template <> __device__ __forceinline__ void put<float>(float* p, int64_t i, float w) { p[i] = w; }
+template <> __device__ __forceinline__ void put<bf16_t>(bf16_t* p, int64_t i, float w) {
+  p[i].bits = f32_to_bf16_rne(w);
+}
+
+// Register-resident group (G known at compile time): O(G^2) rank counting.
+template <int G, typename VT>
+__global__ __launch_bounds__(kPackThreads) void pack_fixed(const float* __restrict__ W, int64_t C,
+                                                           int64_t cblocks, int32_t K,
+                                                           VT* __restrict__ vals,
+                                                           uint8_t* __restrict__ idx) {
+  const int64_t blk = blockIdx.x;
+  const int64_t g = blk / cblocks;
+  const int64_t c = (blk % cblocks) * kPackThreads + threadIdx.x;
+  if (c >= C) return;
+  float w[G];
+  uint32_t key[G];
+#pragma unroll
+  for (int r = 0; r < G; ++r) {
+    w[r] = W[(g * G + r) * C + c];
+    key[r] = abs_bits(w[r]);
+  }
+  int slot = 0;
+#pragma unroll
+  for (int r = 0; r < G; ++r) {
+    int rank = 0;
+#pragma unroll
+    for (int q = 0; q < G; ++q)
+      rank += (key[q] > key[r]) || (key[q] == key[r] && q < r);
+    if (rank < K) {
+      const int64_t o = (g * K + slot) * C + c;
+      put<VT>(vals, o, w[r]);
+      idx[o] = static_cast<uint8_t>(r);
+      ++slot;
+    }
+  }
+}
+
+// Any G <= 256: the group column is re-read from cache for each rank count.
+template <typename VT>
+__global__ __launch_bounds__(kPackThreads) void pack_generic(const float* __restrict__ W, int64_t C,
+                                                             int64_t cblocks, int32_t G, int32_t K,
+                                                             VT* __restrict__ vals,
+                                                             uint8_t* __restrict__ idx) {
+  const int64_t blk = blockIdx.x;
+  const int64_t g = blk / cblocks;
+  const int64_t c = (blk % cblocks) * kPackThreads + threadIdx.x;
+  if (c >= C) return;
+  const float* col = W + g * G * C + c;
+  int slot = 0;
+  for (int r = 0; r < G && slot < K; ++r) {
+    const float wr = col[r * C];
+    const uint32_t kr = abs_bits(wr);
+    int rank = 0;
+    for (int q = 0; q < G; ++q) {
+      const uint32_t kq = abs_bits(col[q * C]);
+      rank += (kq > kr) || (kq == kr && q < r);
+    }
+    if (rank < K) {
+      const int64_t o = (g * K + slot) * C + c;
+      put<VT>(vals, o, wr);
+      idx[o] = static_cast<uint8_t>(r);
+      ++slot;
+    }
+  }
+}
+
+template <typename VT>
+hipError_t launch_typed(const float* W, int64_t O, int64_t C, int32_t G, int32_t K, VT* vals,
+                        uint8_t* idx, hipStream_t s) {
+  const int64_t cblocks = (C + kPackThreads - 1) / kPackThreads;
+  const dim3 grid(static_cast<uint32_t>((O / G) * cblocks));
+  const dim3 block(kPackThreads);
+  switch (G) {
+    case 2: hipLaunchKernelGGL((pack_fixed<2, VT>), grid, block, 0, s, W, C, cblocks, K, vals, idx); break;
+    case 4: hipLaunchKernelGGL((pack_fixed<4, VT>), grid, block, 0, s, W, C, cblocks, K, vals, idx); break;
+    case 8: hipLaunchKernelGGL((pack_fixed<8, VT>), grid, block, 0, s, W, C, cblocks, K, vals, idx); break;
+    case 16: hipLaunchKernelGGL((pack_fixed<16, VT>), grid, block, 0, s, W, C, cblocks, K, vals, idx); break;
+    case 32: hipLaunchKernelGGL((pack_fixed<32, VT>), grid, block, 0, s, W, C, cblocks, K, vals, idx); break;
+    default:
+      hipLaunchKernelGGL((pack_generic<VT>), grid, block, 0, s, W, C, cblocks, G, K, vals, idx);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_pack(const float* W, int64_t O, int64_t C, int32_t G, int32_t K, void* vals,
+                       DType val_t, uint8_t* idx, hipStream_t s) {
+  if (val_t == DType::F32)
+    return launch_typed<float>(W, O, C, G, K, static_cast<float*>(vals), idx, s);
+  return launch_typed<bf16_t>(W, O, C, G, K, static_cast<bf16_t*>(vals), idx, s);
+}
+
+}  // namespace cci

@@ -1,0 +1,114 @@
+"""CPU-only checks of the C ABI: the library loads, exports every function
+include/cci.h declares, and rejects bad arguments before touching the GPU."""
+import ctypes
+
+import pytest
+import torch
+
+from paper_1910_11971_amd import cci
+
+lib = cci.raw()
+FAKE = ctypes.c_void_p(0x10000)          # aligned, never dereferenced: validation fails first
+FAKE_MIS = ctypes.c_void_p(0x10008)      # 8-byte aligned only
+
+
+def test_exports_every_declared_symbol():
+    names = cci.header_functions()
+    assert {"cci_pack", "cci_spmm", "cci_conv_im2col", "cci_packed_sizes"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), f"libcci.so does not export {n}"
+    assert cci.version() >= 100
+
+
+def test_packed_sizes_arithmetic():
+    assert cci.packed_sizes(256, 256, 8, 4, torch.float32) == (256 // 8 * 4 * 256 * 4, 256 // 8 * 4 * 256)
+    assert cci.packed_sizes(64, 576, 8, 2, torch.bfloat16) == (8 * 2 * 576 * 2, 8 * 2 * 576)
+    vb, ib = cci.packed_sizes(4096, 4096, 16, 1)
+    assert ib == 4096 * 4096 // 16 and vb == 2 * ib
+
+
+@pytest.mark.parametrize("O,C,G,K", [(12, 5, 8, 2), (16, 5, 8, 0), (16, 5, 8, 9), (16, 0, 8, 2),
+                                     (512, 5, 512, 2), (16, 5, 0, 1)])
+def test_bad_group_arguments(O, C, G, K):
+    vb, ib = ctypes.c_size_t(77), ctypes.c_size_t(77)
+    assert lib.cci_packed_sizes(O, C, G, K, cci.BF16, ctypes.byref(vb), ctypes.byref(ib)) == cci.EINVAL
+    assert vb.value == 77 and ib.value == 77           # outputs untouched
+    assert lib.cci_last_error()
+    assert lib.cci_pack(FAKE, O, C, G, K, FAKE, cci.BF16, FAKE, None) == cci.EINVAL
+    assert lib.cci_spmm(FAKE, cci.BF16, 4, C, FAKE, cci.BF16, FAKE, O, G, K, None, FAKE,
+                        cci.BF16, 0, None) == cci.EINVAL
+
+
+def test_null_and_alignment_errors():
+    assert lib.cci_pack(None, 16, 8, 8, 2, FAKE, cci.F32, FAKE, None) == cci.EINVAL
+    assert lib.cci_pack(FAKE_MIS, 16, 8, 8, 2, FAKE, cci.F32, FAKE, None) == cci.EALIGN
+    assert lib.cci_spmm(FAKE, cci.F32, 4, 8, FAKE, cci.F32, FAKE, 16, 8, 2, None, None,
+                        cci.F32, 0, None) == cci.EINVAL
+    assert lib.cci_spmm(FAKE, cci.F32, 4, 8, FAKE, cci.F32, FAKE_MIS, 16, 8, 2, None, FAKE,
+                        cci.F32, 0, None) == cci.EALIGN
+    ep = cci.Epilogue(ctypes.c_void_p(0x10004), None, None, 0)
+    assert lib.cci_spmm(FAKE, cci.F32, 4, 8, FAKE, cci.F32, FAKE, 16, 8, 2, ctypes.byref(ep),
+                        FAKE, cci.F32, 0, None) == cci.EALIGN
+    assert "align" in lib.cci_last_error().decode()
+
+
+def test_dtype_combinations():
+    # f32 X with bf16 values, bf16 X with f32 values: unsupported
+    assert lib.cci_spmm(FAKE, cci.F32, 4, 8, FAKE, cci.BF16, FAKE, 16, 8, 2, None, FAKE,
+                        cci.F32, 0, None) == cci.EUNSUPPORTED
+    assert lib.cci_spmm(FAKE, cci.BF16, 4, 8, FAKE, cci.F32, FAKE, 16, 8, 2, None, FAKE,
+                        cci.BF16, 0, None) == cci.EUNSUPPORTED
+    assert lib.cci_spmm(FAKE, cci.F32, 4, 8, FAKE, cci.F32, FAKE, 16, 8, 2, None, FAKE,
+                        cci.BF16, 0, None) == cci.EUNSUPPORTED
+    assert lib.cci_spmm(FAKE, 7, 4, 8, FAKE, cci.F32, FAKE, 16, 8, 2, None, FAKE,
+                        cci.F32, 0, None) == cci.EINVAL
+
+
+def test_explicit_algo_requirements():
+    # dense-tile MFMA needs bf16 and C % 32 == 0; sparse-MAC needs G in {2,4,8,16,32}
+    assert lib.cci_spmm(FAKE, cci.F32, 4, 64, FAKE, cci.F32, FAKE, 16, 8, 2, None, FAKE,
+                        cci.F32, cci.ALGO_DENSE_TILE_MFMA, None) == cci.EUNSUPPORTED
+    assert lib.cci_spmm(FAKE, cci.BF16, 4, 40, FAKE, cci.BF16, FAKE, 16, 8, 2, None, FAKE,
+                        cci.BF16, cci.ALGO_DENSE_TILE_MFMA, None) == cci.EUNSUPPORTED
+    assert lib.cci_spmm(FAKE, cci.BF16, 4, 64, FAKE, cci.BF16, FAKE, 24, 6, 2, None, FAKE,
+                        cci.BF16, cci.ALGO_SPARSE_MAC, None) == cci.EUNSUPPORTED
+    assert lib.cci_spmm(FAKE, cci.BF16, 4, 64, FAKE, cci.BF16, FAKE, 16, 8, 2, None, FAKE,
+                        cci.BF16, 9, None) == cci.EINVAL
+
+
+def test_empty_is_a_noop():
+    # N == 0: nothing to do, no pointer is needed or touched
+    assert lib.cci_spmm(None, cci.BF16, 0, 64, None, cci.BF16, None, 16, 8, 2, None, None,
+                        cci.BF16, 0, None) == cci.OK
+    assert lib.cci_conv_im2col(None, cci.BF16, 0, 5, 5, 32, 3, 3, 1, 1, 1, 1, None, cci.BF16, None,
+                               16, 8, 2, None, None, cci.BF16, 0, None) == cci.OK
+
+
+def test_conv_geometry_errors():
+    args = dict(O=16, G=8, K=2)
+    bad = [(1, 5, 5, 32, 3, 3, 0, 1, 1, 1),   # stride 0
+           (1, 5, 5, 32, 3, 3, 1, 1, -1, 1),  # negative pad
+           (1, 1, 1, 32, 3, 3, 1, 1, 0, 0),   # kernel larger than input
+           (1, 5, 5, 0, 3, 3, 1, 1, 1, 1)]    # Cin 0
+    for B, H, W, Cin, KH, KW, sh, sw, ph, pw in bad:
+        assert lib.cci_conv_im2col(FAKE, cci.BF16, B, H, W, Cin, KH, KW, sh, sw, ph, pw, FAKE, cci.BF16,
+                                   FAKE, args["O"], args["G"], args["K"], None, FAKE, cci.BF16, 0,
+                                   None) == cci.EINVAL
+
+
+def test_auto_algo_cost_model():
+    # bf16, tile-friendly: expanded MFMA work wins while K/G > 1/32
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 100352, 576, 64, 64, 8, 2) == "dense_tile_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 4096, 4096, 4096, 4096, 16, 1) == "dense_tile_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 4096, 4096, 4096, 4096, 64, 1) == "sparse_mac"
+    # fp32, or a reduction the tile path cannot step through: sparse-MAC
+    assert cci.auto_algo(torch.float32, torch.float32, 64, 256, 256, 256, 8, 4) == "sparse_mac"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 1000, 147, 3, 64, 8, 8) == "sparse_mac"
+
+
+@pytest.mark.skipif(torch.cuda.is_available(), reason="checks the no-device error path only")
+def test_launch_without_device_reports_hip_error():
+    # passes validation, then the HIP runtime refuses: CCI_EHIP, message set
+    st = lib.cci_pack(FAKE, 16, 8, 8, 2, FAKE, cci.F32, FAKE, None)
+    assert st == cci.EHIP
+    assert lib.cci_last_error()

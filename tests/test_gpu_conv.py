@@ -1,0 +1,115 @@
+"""cci_conv_im2col on the GPU vs the oracle's direct convolution."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_common import (DEV, epilogue_terms, need_gpu, oracle_pack_vals, rand_epilogue, tol_for,
+                        x_as_f32)
+from parity import check_close, to_np_f32
+from paper_1910_11971_amd import workloads
+
+pytestmark = pytest.mark.gpu
+
+
+def run_conv(X: torch.Tensor, W: np.ndarray, G, K, k, stride, pad, y_dtype, algo, *, pixels=None,
+             ep=None):
+    from paper_1910_11971_amd import cci
+    vdt = torch.float32 if X.dtype == torch.float32 else torch.bfloat16
+    B, H, Wd, Cin = X.shape
+    O = W.shape[0]
+    s, b, r, r_t, relu = ep if ep is not None else (None, None, None, None, False)
+    kw = {}
+    if s is not None:
+        kw["scale"] = torch.from_numpy(s).to(DEV)
+    if b is not None:
+        kw["bias"] = torch.from_numpy(b).to(DEV)
+    Ho, Wo = cci.conv_out_hw(H, Wd, k, k, (stride, stride), (pad, pad))
+    if r_t is not None:
+        kw["residual"] = r_t.reshape(B, Ho, Wo, O).to(DEV)
+    vals, idx = cci.pack(torch.from_numpy(W).to(DEV), G, K, vdt)
+    Y = cci.conv_im2col(X.to(DEV), vals, idx, G, k, k, (stride, stride), (pad, pad), relu=relu,
+                        out_dtype=y_dtype, algo=algo, **kw)
+    torch.cuda.synchronize()
+    v_ref, idx_ref, _ = oracle_pack_vals(W, G, K, vdt)
+    Wmask = oracle.unpack(v_ref, idx_ref, G).reshape(O, k, k, Cin)
+    Yref, Yabs = oracle.conv2d_nhwc(x_as_f32(X), Wmask, (stride, stride), (pad, pad), scale=s, bias=b,
+                                    residual=r, relu=relu, pixels=pixels, want_abs=True)
+    got = to_np_f32(Y).reshape(-1, O)
+    if pixels is not None:
+        got = got[pixels]
+    rr = None if r is None else (r if pixels is None else r[pixels])
+    S = epilogue_terms(Yabs, s, b, rr)
+    return check_close(got, Yref, S, tol_for(y_dtype, X.dtype),
+                       f"conv {algo} {tuple(X.shape)} k{k} s{stride} p{pad} O={O} G={G} K={K}")
+
+
+def rand_x(shape, dtype, seed):
+    return torch.from_numpy(np.random.default_rng(seed).standard_normal(shape).astype(np.float32)).to(dtype)
+
+
+def rand_w(O, C, seed):
+    return (np.random.default_rng(seed).standard_normal((O, C)) / np.sqrt(C)).astype(np.float32)
+
+
+CASES = [  # B, H, W, Cin, O, k, stride, pad, G, K
+    (2, 9, 11, 32, 64, 3, 1, 1, 8, 2),
+    (3, 14, 14, 64, 64, 3, 2, 1, 8, 2),
+    (2, 7, 7, 64, 128, 1, 1, 0, 16, 4),
+    (2, 13, 10, 32, 64, 1, 2, 0, 8, 3),
+    (1, 6, 5, 96, 64, 3, 1, 0, 4, 1),
+    (4, 17, 19, 32, 192, 3, 2, 1, 16, 2),
+]
+
+
+@pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma"])
+@pytest.mark.parametrize("B,H,W,Cin,O,k,stride,pad,G,K", CASES)
+def test_conv_bf16(B, H, W, Cin, O, k, stride, pad, G, K, algo):
+    need_gpu()
+    X = rand_x((B, H, W, Cin), torch.bfloat16, B * H + Cin)
+    run_conv(X, rand_w(O, k * k * Cin, O + k), G, K, k, stride, pad, torch.bfloat16, algo)
+
+
+@pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma"])
+def test_conv_epilogue_residual_relu(algo):
+    need_gpu()
+    B, H, W, Cin, O, k = 2, 10, 10, 64, 64, 3
+    N = B * H * W
+    ep = rand_epilogue(O, N, torch.bfloat16, 11, residual=True, relu=True)
+    run_conv(rand_x((B, H, W, Cin), torch.bfloat16, 12), rand_w(O, k * k * Cin, 13), 8, 2, k, 1, 1,
+             torch.bfloat16, algo, ep=ep)
+
+
+def test_conv_stem_7x7_cin3_dense_control():
+    """ResNet stem shape: 7x7 stride 2 pad 3, Cin=3 (K=G: dense control)."""
+    need_gpu()
+    X = rand_x((2, 32, 32, 3), torch.bfloat16, 21)
+    run_conv(X, rand_w(64, 147, 22), 8, 8, 7, 2, 3, torch.bfloat16, "auto")
+
+
+def test_conv_fp32():
+    need_gpu()
+    X = rand_x((2, 8, 8, 5), torch.float32, 31)
+    run_conv(X, rand_w(16, 45, 32), 4, 2, 3, 1, 1, torch.float32, "auto")
+
+
+def sample_pixels(wl, n, seed):
+    rng = np.random.default_rng(seed)
+    Ho, Wo = wl.Ho, wl.Wo
+    corners = []
+    for b in (0, wl.B - 1):
+        for oh in (0, Ho - 1):
+            for ow in (0, Wo - 1):
+                corners.append((b * Ho + oh) * Wo + ow)
+    return np.unique(np.concatenate([corners, rng.integers(0, wl.N, n)]))
+
+
+@pytest.mark.parametrize("algo", ["auto", "sparse_mac"])
+@pytest.mark.parametrize("name", ["conv3x3", "conv1x1_k4", "conv1x1_k2"])
+def test_conv_full_size_sampled(name, algo):
+    """Full-size 3x3 and 1x1 bottleneck convolutions, sampled output pixels."""
+    need_gpu()
+    wl = workloads.WORKLOADS[name]
+    X, W = workloads.draw(wl)
+    run_conv(X, W, wl.G, wl.K, wl.KH, wl.stride, wl.pad, torch.bfloat16, algo,
+             pixels=sample_pixels(wl, 300, 7))

@@ -1,0 +1,113 @@
+"""cci_spmm on the GPU vs the oracle (Alg. 1 in double), both kernel families."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_common import (DEV, epilogue_terms, need_gpu, oracle_pack_vals, rand_epilogue, tol_for,
+                        x_as_f32)
+from parity import check_close, to_np_f32
+from paper_1910_11971_amd import workloads
+
+pytestmark = pytest.mark.gpu
+
+
+def run_case(X: torch.Tensor, W: np.ndarray, G, K, y_dtype, algo, *, rows=None, ep=None, seed=0):
+    from paper_1910_11971_amd import cci
+    vdt = torch.float32 if X.dtype == torch.float32 else torch.bfloat16
+    N, C = X.shape
+    O = W.shape[0]
+    s, b, r, r_t, relu = ep if ep is not None else (None, None, None, None, False)
+    Xd = X.to(DEV)
+    vals, idx = cci.pack(torch.from_numpy(W).to(DEV), G, K, vdt)
+    kw = {}
+    if s is not None:
+        kw["scale"] = torch.from_numpy(s).to(DEV)
+    if b is not None:
+        kw["bias"] = torch.from_numpy(b).to(DEV)
+    if r_t is not None:
+        kw["residual"] = r_t.to(DEV)
+    Y = cci.spmm(Xd, vals, idx, G, relu=relu, out_dtype=y_dtype, algo=algo, **kw)
+    torch.cuda.synchronize()
+    v_ref, idx_ref, _ = oracle_pack_vals(W, G, K, vdt)
+    Yref, Yabs = oracle.spmm_rows(x_as_f32(X), v_ref, idx_ref, G, scale=s, bias=b, residual=r,
+                                  relu=relu, rows=rows, want_abs=True)
+    got = to_np_f32(Y)
+    if rows is not None:
+        got = got[rows]
+    S = epilogue_terms(Yabs, s, b, None if r is None else (r if rows is None else r[rows]))
+    return check_close(got, Yref, S, tol_for(y_dtype, X.dtype), f"spmm {algo} N={N} C={C} O={O} G={G} K={K}")
+
+
+def rand_x(N, C, dtype, seed):
+    rng = np.random.default_rng(seed)
+    return torch.from_numpy(rng.standard_normal((N, C)).astype(np.float32)).to(dtype)
+
+
+def rand_w(O, C, seed):
+    return (np.random.default_rng(seed + 1).standard_normal((O, C)) / np.sqrt(C)).astype(np.float32)
+
+
+CASES = [  # N, C, O, G, K
+    (1, 32, 64, 8, 2), (37, 64, 64, 8, 2), (300, 96, 128, 16, 4), (1000, 256, 192, 8, 3),
+    (129, 32, 64, 2, 1), (70, 64, 64, 4, 4), (513, 128, 64, 32, 7), (2047, 64, 256, 16, 1),
+    (4500, 160, 64, 8, 8), (64, 576, 64, 8, 2),
+]
+
+
+@pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma"])
+@pytest.mark.parametrize("N,C,O,G,K", CASES)
+def test_spmm_bf16(N, C, O, G, K, algo):
+    need_gpu()
+    run_case(rand_x(N, C, torch.bfloat16, N + C), rand_w(O, C, O + G), G, K, torch.bfloat16, algo)
+
+
+@pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma"])
+def test_spmm_bf16_in_f32_out_with_epilogue(algo):
+    need_gpu()
+    N, C, O, G, K = 777, 128, 128, 8, 2
+    ep = rand_epilogue(O, N, torch.float32, 3, residual=True, relu=True)
+    run_case(rand_x(N, C, torch.bfloat16, 1), rand_w(O, C, 2), G, K, torch.float32, algo, ep=ep)
+
+
+@pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma"])
+def test_spmm_bf16_epilogue_bf16_residual(algo):
+    need_gpu()
+    N, C, O, G, K = 300, 64, 64, 16, 4
+    ep = rand_epilogue(O, N, torch.bfloat16, 4, residual=True, relu=True)
+    run_case(rand_x(N, C, torch.bfloat16, 5), rand_w(O, C, 6), G, K, torch.bfloat16, algo, ep=ep)
+
+
+@pytest.mark.parametrize("N,C,O,G,K", [(64, 256, 256, 8, 4), (5, 33, 16, 4, 2), (300, 45, 96, 32, 3),
+                                       (1000, 7, 8, 2, 1)])
+def test_spmm_fp32(N, C, O, G, K):
+    need_gpu()
+    run_case(rand_x(N, C, torch.float32, N), rand_w(O, C, C), G, K, torch.float32, "auto")
+
+
+def test_spmm_odd_c_bf16_auto_routes_to_sparse_mac():
+    need_gpu()
+    run_case(rand_x(200, 45, torch.bfloat16, 9), rand_w(32, 45, 9), 8, 2, torch.bfloat16, "auto")
+
+
+def test_spmm_fc256_full():
+    """Single FC layer, fp32, X [64,256], W [256,256], G=8, K=4 -- every output."""
+    need_gpu()
+    wl = workloads.WORKLOADS["fc256"]
+    X, W = workloads.draw(wl)
+    run_case(X, W, wl.G, wl.K, torch.float32, "auto")
+
+
+def sample_rows(N, n, seed):
+    rng = np.random.default_rng(seed)
+    return np.unique(np.concatenate([[0, 1, N // 2, N - 2, N - 1], rng.integers(0, N, n)]))
+
+
+@pytest.mark.parametrize("algo", ["auto", "sparse_mac"])
+@pytest.mark.parametrize("K", [1, 2, 4, 8, 16])
+def test_spmm_fc4096_full_size_sampled(K, algo):
+    """FC sweep at full size (4096^3, G=16), sampled rows vs the oracle."""
+    need_gpu()
+    wl = workloads.WORKLOADS[f"fc4096_k{K}"]
+    X, W = workloads.draw(wl)
+    run_case(X, W, wl.G, wl.K, torch.bfloat16, algo, rows=sample_rows(wl.N, 48, K))

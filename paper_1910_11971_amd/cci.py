@@ -117,8 +117,10 @@ def packed_sizes(O: int, C: int, G: int, K: int, val_dtype=torch.bfloat16):
     return vb.value, ib.value
 
 
-def pack(W: torch.Tensor, G: int, K: int, val_dtype=torch.bfloat16):
-    """cci_pack: W fp32 [O, C] (conv: [O, KH, KW, Cin]) -> (vals [O/G, K, C], idx uint8)."""
+def pack(W: torch.Tensor, G: int, K: int, val_dtype=torch.bfloat16, out=None):
+    """cci_pack: W fp32 [O, C] (conv: [O, KH, KW, Cin]) -> (vals [O/G, K, C], idx uint8).
+
+    `out=(vals, idx)` writes into caller tensors of exactly that shape and dtype."""
     _dev(W)
     if W.dtype != torch.float32:
         raise TypeError("W must be float32")
@@ -126,8 +128,16 @@ def pack(W: torch.Tensor, G: int, K: int, val_dtype=torch.bfloat16):
     C = W.numel() // max(O, 1)
     if O % G:
         raise ValueError("O must be a multiple of G")
-    vals = torch.empty((O // G, K, C), dtype=val_dtype, device=W.device)
-    idx = torch.empty((O // G, K, C), dtype=torch.uint8, device=W.device)
+    if out is None:
+        vals = torch.empty((O // G, K, C), dtype=val_dtype, device=W.device)
+        idx = torch.empty((O // G, K, C), dtype=torch.uint8, device=W.device)
+    else:
+        vals, idx = out
+        _dev(vals), _dev(idx)
+        if (tuple(vals.shape) != (O // G, K, C) or tuple(idx.shape) != (O // G, K, C)
+                or vals.dtype != val_dtype or idx.dtype != torch.uint8
+                or not vals.is_contiguous() or not idx.is_contiguous()):
+            raise ValueError("out must be contiguous (vals, idx) of shape [O/G, K, C] with the packed dtypes")
     _check(_lib.cci_pack(_ptr(W), O, C, G, K, _ptr(vals), _code(val_dtype), _ptr(idx), _stream(W)))
     return vals, idx
 

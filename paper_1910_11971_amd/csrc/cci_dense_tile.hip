@@ -48,15 +48,18 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 
 constexpr int kThreads = 512;
 constexpr int kWaves = 8;          // two per SIMD: one wave's stalls are the other's MFMA slots
+constexpr int kLoadWaves = 4;      // waves 0..3 stream activations; waves 4..7 expand weights
+constexpr int kRoleThreads = kLoadWaves * 64;
 constexpr int kBN = 64;            // outputs per wave
 constexpr int kKS = 32;            // reduction columns per MFMA k-step
 constexpr int kMT = 4;             // max 16-pixel tiles per wave
 constexpr int kBPad = 8;           // weight-tile row padding (bf16 elements)
 constexpr int kXcds = 8;
 constexpr int kLdsMax = 160 * 1024;
-constexpr int kDmaMax = 10;        // patch DMA instructions per thread per chunk
-constexpr int kRowMax = 4;         // packed rows per thread per chunk (expansion)
-constexpr int kPackedOps = 2 * kRowMax;  // vector loads of one chunk's packed rows
+constexpr int kDmaMax = 20;        // patch DMA instructions per loader thread per chunk
+constexpr int kDmaEarly = 2;       // of those, issued before the expanders' loads are queued
+constexpr int kRowMax = 8;         // packed-row segments per expander thread per expansion
+constexpr int kStPitch = kBN * 4 + 16;   // epilogue staging: bytes per pixel row (padded)
 constexpr uint32_t kOOB = 0x80000000u;   // buffer offset that reads as zero / drops a store
 constexpr int kRsrcWord3 = 0x00020000;   // raw buffer descriptor word 3 (gfx9 family)
 
@@ -86,26 +89,34 @@ struct Params {
   // convolution geometry; FC runs as a 1x1 convolution over N "pixels"
   int32_t H, W, Cin, KW, sh, sw, ph, pw, Ho, Wo, Bimg;
   int32_t strided;      // rows mode: 1x1 convolution with stride (input pixels are gathered)
-  // plan
+  // plan: work split
   int32_t WO, WP;       // wave arrangement (WO * WP == 8)
   int32_t nob;          // output super-blocks of WO*64 outputs
   int32_t part_len;     // rows mode: output pixels per partition; rect: output rows (RH)
   int32_t row_parts;    // rect: partitions per image
+  // plan: reduction chunks and LDS layout
   int32_t cinb;         // channels per chunk (power of two, multiple of 32)
   int32_t lg_cpp;       // log2(cinb / 8): 16-byte data chunks per patch pixel
   int32_t lg_ksteps;    // log2(cinb / 32)
   int32_t nchunks, taps;
+  int32_t wres;         // 1: one weight tile holds every chunk (expanded once); 0: ring of two
+  int32_t nwb;          // weight tiles in LDS (1, or 2 for the ring)
+  int32_t npb;          // patch buffers in LDS (ring; chunk j uses buffer j % npb)
   int32_t patch_cols;   // rect: staged input columns
   int32_t patch_pix;    // staged pixels per chunk
+  int32_t slots;        // 16-byte patch slots per chunk (patch_pix * (cpp + 1))
   int32_t b_pitch;      // bf16 elements per weight-tile row
-  int32_t b_bytes;      // bytes of one weight tile (WO*64 rows)
-  int32_t buf_bytes;    // weight tile + patch region
-  int32_t nbuf;         // 1 or 2
-  int32_t ncols8;       // 8-column blocks per weight-tile row
-  int32_t rstep;        // expansion: packed rows apart between one thread's rows
+  int32_t w_bytes;      // bytes of one weight tile (WO*64 rows)
+  int32_t p_bytes;      // bytes of one patch buffer
+  int32_t ncols8;       // 8-column blocks of one expansion (whole tile or one chunk)
+  int32_t nu;           // expansion units (group x 8-column block) per expander thread
   int32_t nrows;        // packed rows of one output super-block
   int32_t mt;           // 16-pixel tiles per wave (compile-time instantiation)
-  FastDiv fd_nob, fd_rparts, fd_wo, fd_pcols, fd_pps, fd_k, fd_ncols8, fd_howo;
+  uint32_t kw_mul;      // tap / KW == (tap * kw_mul) >> 20 for tap < 4096
+  // loader slot walk: each step advances 256 slots = dq pixels + dc slots;
+  // rect: dq pixels = dpr patch rows + diw patch columns
+  int32_t dq, dc, dpr, diw;
+  FastDiv fd_nob, fd_rparts, fd_wo, fd_pcols, fd_pps, fd_k, fd_ncols8, fd_tc, fd_howo;
 };
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(u32x4_t v) { return __builtin_bit_cast(bf16x8_t, v); }
@@ -122,7 +133,6 @@ __device__ __forceinline__ void wait_vm() {
   static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
-
 // Patch layout: pixel q occupies cpp + 1 consecutive 16-byte slots (cpp
 // data chunks and one pad slot).  The odd slot pitch spreads 8 consecutive
 // pixels reading the same chunk over all 32 banks, and makes the operand
@@ -154,152 +164,189 @@ __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wo = wave % p.WO;
-  const int wp = wave / p.WO;
-  const int lrow = lane & 15;
-  const int lk = lane >> 4;
+  const bool loader = wave < kLoadWaves;  // wave-uniform role
+  const int rt = threadIdx.x - (loader ? 0 : kRoleThreads);  // thread index within the role
   const int cpp = 1 << p.lg_cpp;
   const int pps = cpp + 1;
-  const int32_t o_wave = (ob * p.WO + wo) * kBN;
-  // Tiles wp, wp+WP, ... belong to this wave; only the last of its MT tile
-  // slots can be empty (then its MFMAs are skipped).
-  const bool last_tile = (wp + (MT - 1) * p.WP) * 16 < npix;
+  const int32_t wofs_patch = p.nwb * p.w_bytes;  // LDS offset of patch buffer 0
 
-  const __amdgpu_buffer_rsrc_t xr =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(p.X), (short)0, static_cast<int>(p.x_bytes), kRsrcWord3);
+  // ---- expanders: weight-tile build -----------------------------------------
+  // Unit u = (group gl, 8-column block col8) of one expansion (the whole tile,
+  // or one chunk): its G tile rows x 8 columns are zero-filled and receive
+  // the 8 columns of the group's K packed rows, all by one thread (program
+  // order is the only synchronisation).  Thread rt owns units rt + 256 j
+  // (j < nu); its packed-row segments ("slots", unit-major, K per unit) are
+  // loaded kRowMax at a time.  The tile column of col8 is 8 * col8, its
+  // source column tap * Cin + (chunk) * cinb + 8 * c8.
   const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(p.vals), (short)0, static_cast<int>(p.packed_n * 2u), kRsrcWord3);
   const __amdgpu_buffer_rsrc_t ir = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(p.idx), (short)0, static_cast<int>(p.packed_n), kRsrcWord3);
-
-  // ---- weight-tile expansion: thread -> one 8-column block, several packed rows ----
-  const int r0 = static_cast<int>(fdiv(threadIdx.x, p.fd_ncols8));
-  const int col8 = threadIdx.x - r0 * p.ncols8;
-  const int tap_e = col8 >> p.lg_cpp;  // 8-column blocks per tap == cpp
-  const int c8 = col8 - (tap_e << p.lg_cpp);
   const int gpb = (p.WO * kBN) / p.G;
-  uint32_t psrc[kRowMax];   // element offset of the packed row at chunk 0 (kOOB: none)
-  int32_t drow[kRowMax];    // bf16 element offset of the row's group in the tile (-1: none)
-#pragma unroll
-  for (int jr = 0; jr < kRowMax; ++jr) {
-    const int r = r0 + jr * p.rstep;
-    const int gl = static_cast<int>(fdiv(r, p.fd_k));
-    const int32_t gg = ob * gpb + gl;
-    const bool ok = r0 < p.rstep && r < p.nrows && gg * p.G < p.O;
-    psrc[jr] = ok ? static_cast<uint32_t>((gg * p.K + (r - gl * p.K)) * p.C + tap_e * p.Cin + 8 * c8) : kOOB;
-    drow[jr] = ok ? gl * p.G * p.b_pitch + tap_e * p.cinb + 8 * c8 : -1;
-  }
+  // groups that exist (the last super-block may be partial)
+  const int glim = p.O / p.G - ob * gpb < gpb ? p.O / p.G - ob * gpb : gpb;
+  const int nslots = p.nu * p.K;
   struct Packed {
     u32x4_t v[kRowMax];
     u32x2_t ix[kRowMax];
+    int32_t dst[kRowMax];  // tile element offset of the unit's first row (< 0: none); bit 30: first slot
   };
-  // kPackedOps loads, always issued (absent rows read zeros out of range)
-  auto load_packed = [&](int ch, Packed& P) {
-    const uint32_t add = static_cast<uint32_t>(ch * p.cinb);
+  constexpr int32_t kFirst = 1 << 30;
+  Packed P;
+  // load slots s0 .. s0+kRowMax-1 of the expansion of chunk ch
+  auto load_slots = [&](int ch, int s0) {
 #pragma unroll
-    for (int jr = 0; jr < kRowMax; ++jr) {
-      const uint32_t e = psrc[jr] == kOOB ? kOOB : psrc[jr] + add;
-      P.v[jr] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(vr, e == kOOB ? kOOB : e * 2u, 0, 0));
-      P.ix[jr] = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(ir, e, 0, 0));
+    for (int i = 0; i < kRowMax; ++i) {
+      const int sl = s0 + i;
+      const int j = static_cast<int>(fdiv(sl, p.fd_k));
+      const int k = sl - j * p.K;
+      const int u = rt + kRoleThreads * j;
+      const int gl = static_cast<int>(fdiv(u, p.fd_ncols8));
+      const int col8 = u - gl * p.ncols8;
+      const bool ok = sl < nslots && gl < glim;
+      const int chl = static_cast<int>(fdiv(col8, p.fd_tc));
+      const int rem = col8 - chl * (p.taps << p.lg_cpp);
+      const uint32_t e = static_cast<uint32_t>(((ob * gpb + gl) * p.K + k) * p.C + (rem >> p.lg_cpp) * p.Cin +
+                                               (chl + ch) * p.cinb + 8 * (rem & (cpp - 1)));
+      P.v[i] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(vr, ok ? e * 2u : kOOB, 0, 0));
+      P.ix[i] = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(ir, ok ? e : kOOB, 0, 0));
+      P.dst[i] = ok ? (gl * p.G * p.b_pitch + 8 * col8) | (k == 0 ? kFirst : 0) : -1;
     }
   };
-  auto zero_weights = [&](int buf) {
-    u32x4_t* b4 = reinterpret_cast<u32x4_t*>(lds + buf * p.buf_bytes);
-    const int n16 = p.b_bytes / 16;
-    for (int e = threadIdx.x; e < n16; e += kThreads) b4[e] = u32x4_t{0u, 0u, 0u, 0u};
-  };
-  // every kept weight goes to row G*g + idx of its column (Alg. 1's target row)
-  auto scatter_weights = [&](int buf, const Packed& P) {
-    uint16_t* bs = reinterpret_cast<uint16_t*>(lds + buf * p.buf_bytes);
+  // write the loaded slots into weight tile wb: a unit's first slot zero-fills
+  // its G rows; every kept weight goes to row G*g + idx (Alg. 1's target row)
+  auto scatter_slots = [&](int wb) {
+    uint16_t* bs = reinterpret_cast<uint16_t*>(lds + wb * p.w_bytes);
 #pragma unroll
-    for (int jr = 0; jr < kRowMax; ++jr) {
-      if (drow[jr] < 0) continue;
-      uint16_t* dst = bs + drow[jr];
-#pragma unroll
-      for (int jj = 0; jj < 8; ++jj) {
-        const uint32_t r = (P.ix[jr][jj >> 2] >> (8 * (jj & 3))) & 0xffu;
-        const uint16_t w = static_cast<uint16_t>(P.v[jr][jj >> 1] >> (16 * (jj & 1)));
-        if (r < static_cast<uint32_t>(p.G)) dst[r * p.b_pitch + jj] = w;
-      }
-    }
-  };
-
-  // ---- per-lane patch DMA offsets for channel chunk 0 ----
-  // Every thread issues exactly kDmaMax DMA instructions so that the
-  // compiler's (and our) counts of outstanding vector-memory operations are
-  // exact: slots past the wave's last one repeat that slot, rewriting the
-  // same bytes with the same data.  A wave with no slot at all writes zeros
-  // to its own first block, which the planner keeps inside the patch region.
-  const int32_t slots = p.patch_pix * pps;
-  const int32_t nd = slots > wave * 64 ? (slots - wave * 64 + kWaves * 64 - 1) / (kWaves * 64) : 0;
-  const int32_t ilast = nd > 0 ? nd - 1 : 0;
-  uint32_t doff[kDmaMax];
-  {
-    const int32_t ih_base = oh0 * p.sh - p.ph;
-    const uint32_t img = static_cast<uint32_t>(b_img * p.H);
-#pragma unroll
-    for (int i = 0; i < kDmaMax; ++i) {
-      const int32_t ie = i < ilast ? i : ilast;  // wave-uniform
-      const int32_t s = (wave + kWaves * ie) * 64 + lane;
-      const int32_t q = static_cast<int32_t>(fdiv(static_cast<uint32_t>(s), p.fd_pps));
-      const int32_t c = s - q * pps;  // c == cpp: pad slot
-      const bool slot_ok = s < slots && c < cpp;
-      uint32_t pix;
-      bool ok;
-      if constexpr (RECT) {
-        const int32_t pr = static_cast<int32_t>(fdiv(static_cast<uint32_t>(q), p.fd_pcols));
-        const int32_t ih = ih_base + pr;
-        const int32_t iw = q - pr * p.patch_cols - p.pw;
-        ok = slot_ok && static_cast<uint32_t>(ih) < static_cast<uint32_t>(p.H) &&
-             static_cast<uint32_t>(iw) < static_cast<uint32_t>(p.W);
-        pix = (img + static_cast<uint32_t>(ih)) * static_cast<uint32_t>(p.W) + static_cast<uint32_t>(iw);
-      } else {
-        ok = slot_ok && q < npix;
-        uint32_t nn = static_cast<uint32_t>(P0 + (q < npix ? q : 0));
-        if (p.strided) {  // strided 1x1 (uniform branch): gather the input pixel
-          const uint32_t b = fdiv(nn, p.fd_howo);
-          const uint32_t rem = nn - b * static_cast<uint32_t>(p.Ho * p.Wo);
-          const uint32_t oh = fdiv(rem, p.fd_wo);
-          nn = (b * p.H + oh * p.sh) * p.W + (rem - oh * p.Wo) * p.sw;
+    for (int i = 0; i < kRowMax; ++i) {
+      if (P.dst[i] >= 0) {
+        uint16_t* dst = bs + (P.dst[i] & (kFirst - 1));
+        if (P.dst[i] & kFirst) {
+          for (int r = 0; r < p.G; ++r)
+            *reinterpret_cast<u32x4_t*>(dst + r * p.b_pitch) = u32x4_t{0u, 0u, 0u, 0u};
         }
-        pix = nn;
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) {
+          const uint32_t row = (P.ix[i][jj >> 2] >> (8 * (jj & 3))) & 0xffu;  // idx: row in the group
+          const uint16_t w = static_cast<uint16_t>(P.v[i][jj >> 1] >> (16 * (jj & 1)));
+          if (row < static_cast<uint32_t>(p.G)) dst[row * p.b_pitch + jj] = w;
+        }
       }
-      doff[i] = ok ? (pix * static_cast<uint32_t>(p.Cin) + 8u * static_cast<uint32_t>(c)) * 2u : kOOB;
+    }
+  };
+  // whole expansion of chunk ch into tile wb; the first kRowMax slots may
+  // already be loaded (prefetched)
+  auto expand = [&](int ch, int wb, bool prefetched) {
+    for (int s0 = 0; s0 < nslots; s0 += kRowMax) {
+      if (s0 > 0 || !prefetched) load_slots(ch, s0);
+      scatter_slots(wb);
+    }
+  };
+  if (!loader) load_slots(0, 0);
+
+  // ---- loaders: patch DMA -------------------------------------------------
+  // Loader thread rt owns slots rt + 256 i (i < nd); consecutive slots of one
+  // pixel are its 16-byte channel chunks (the last one is the pad slot).  The
+  // offsets of chunk 0 are walked incrementally (the first kDmaEarly DMAs
+  // are issued as soon as their offsets are known, the rest after the
+  // expanders' packed-row loads are queued); chunk j reuses them plus
+  // j*cinb*2.
+  const __amdgpu_buffer_rsrc_t xr =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(p.X), (short)0, static_cast<int>(p.x_bytes), kRsrcWord3);
+  const int32_t nd = p.slots > wave * 64 ? (p.slots - wave * 64 + kRoleThreads - 1) / kRoleThreads : 0;
+  uint32_t doff[kDmaMax];
+  auto dma = [&](uint32_t pofs, int i, uint32_t off) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void_t*)(lds + pofs + (wave + kLoadWaves * i) * 1024), 16, off,
+                                             0, 0, 0);
+  };
+  if (loader) {
+    const int32_t cin2 = p.Cin * 2;
+    int32_t s = rt;
+    int32_t q = static_cast<int32_t>(fdiv(static_cast<uint32_t>(s), p.fd_pps));
+    int32_t c = s - q * pps;
+    if constexpr (RECT) {
+      int32_t pr = static_cast<int32_t>(fdiv(static_cast<uint32_t>(q), p.fd_pcols));
+      int32_t iw = q - pr * p.patch_cols;  // patch column
+      const int32_t ih0 = oh0 * p.sh - p.ph;
+      // the pixel index may be negative (padding): then the slot is invalid
+      int32_t off = ((b_img * p.H + ih0 + pr) * p.W + iw - p.pw) * cin2 + 16 * c;
+      const int32_t d_base = (p.dpr * p.W + p.diw) * cin2 + 16 * p.dc;
+      const int32_t d_carry = cin2 - 16 * pps;
+      const int32_t d_wrap = (p.W - p.patch_cols) * cin2;
+#pragma unroll
+      for (int i = 0; i < kDmaMax; ++i) {
+        if (i < nd) {
+          const int32_t ih = ih0 + pr, iwi = iw - p.pw;
+          const bool ok = s < p.slots && c < cpp && static_cast<uint32_t>(ih) < static_cast<uint32_t>(p.H) &&
+                          static_cast<uint32_t>(iwi) < static_cast<uint32_t>(p.W);
+          doff[i] = ok ? static_cast<uint32_t>(off) : kOOB;
+          if (i < kDmaEarly) dma(static_cast<uint32_t>(wofs_patch), i, doff[i]);
+          s += kRoleThreads;
+          c += p.dc;
+          const bool carry = c >= pps;
+          c -= carry ? pps : 0;
+          iw += p.diw + (carry ? 1 : 0);
+          const bool wrap = iw >= p.patch_cols;
+          iw -= wrap ? p.patch_cols : 0;
+          pr += p.dpr + (wrap ? 1 : 0);
+          off += d_base + (carry ? d_carry : 0) + (wrap ? d_wrap : 0);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < kDmaMax; ++i) {
+        if (i < nd) {
+          const bool ok = s < p.slots && c < cpp && q < npix;
+          uint32_t nn = static_cast<uint32_t>(P0 + (q < npix ? q : 0));
+          if (p.strided) {  // strided 1x1 (uniform branch): gather the input pixel
+            const uint32_t b = fdiv(nn, p.fd_howo);
+            const uint32_t rem = nn - b * static_cast<uint32_t>(p.Ho * p.Wo);
+            const uint32_t oh = fdiv(rem, p.fd_wo);
+            nn = (b * p.H + oh * p.sh) * p.W + (rem - oh * p.Wo) * p.sw;
+          }
+          doff[i] = ok ? nn * static_cast<uint32_t>(cin2) + 16u * static_cast<uint32_t>(c) : kOOB;
+          if (i < kDmaEarly) dma(static_cast<uint32_t>(wofs_patch), i, doff[i]);
+          s += kRoleThreads;
+          c += p.dc;
+          const bool carry = c >= pps;
+          c -= carry ? pps : 0;
+          q += p.diw + (carry ? 1 : 0);
+        }
+      }
     }
   }
-  auto issue_patch = [&](int ch, int buf) {
-    uint8_t* pbase = lds + buf * p.buf_bytes + p.b_bytes;
+  auto issue_patch = [&](int ch, uint32_t pofs) {
     const uint32_t add = static_cast<uint32_t>(ch * p.cinb) * 2u;
 #pragma unroll
     for (int i = 0; i < kDmaMax; ++i) {
-      const int32_t ie = i < ilast ? i : ilast;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void_t*)(pbase + (wave + kWaves * ie) * 1024), 16,
-                                               doff[i] + add, 0, 0, 0);
+      if (i < nd) dma(pofs, i, doff[i] + add);  // wave-uniform
     }
   };
 
   // ---- per-lane tile geometry: patch pixel of tap (0,0), output byte offset ----
-  int32_t qbase[MT];
-  uint32_t yoff[MT];
+  const int wo = wave % p.WO;
+  const int wp = wave / p.WO;
+  const int lrow = lane & 15;
+  const int lk = lane >> 4;
+  const int32_t o_wave = (ob * p.WO + wo) * kBN;
+  // Tiles wp, wp+WP, ... belong to this wave; only the last of its MT tile
+  // slots can be empty (then its MFMAs are skipped).
+  const bool last_tile = (wp + (MT - 1) * p.WP) * 16 < npix;
+  uint32_t abase[MT];  // A-fragment LDS byte offset of each tile at tap (0,0), k-step 0
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
     const int32_t px = (wp + mt * p.WP) * 16 + lrow;
-    const bool valid = px < npix;
-    const int32_t pc = valid ? px : 0;  // idle lanes read pixel 0 and store nothing
-    uint32_t n;
+    const int32_t pc = px < npix ? px : 0;  // idle lanes read pixel 0 and store nothing
+    int32_t qb;
     if constexpr (RECT) {
       const int32_t r = static_cast<int32_t>(fdiv(pc, p.fd_wo));
-      const int32_t ow = pc - r * p.Wo;
-      qbase[mt] = r * p.sh * p.patch_cols + ow * p.sw;
-      n = static_cast<uint32_t>((b_img * p.Ho + oh0 + r) * p.Wo + ow);
+      qb = r * p.sh * p.patch_cols + (pc - r * p.Wo) * p.sw;
     } else {
-      qbase[mt] = pc;
-      n = static_cast<uint32_t>(P0 + pc);
+      qb = pc;
     }
-    // an invalid pixel's offset is >= 2^31, so adding an output offset keeps
-    // it out of range (the store is dropped)
-    yoff[mt] = valid ? n * static_cast<uint32_t>(p.O) * ysz : kOOB;
+    abase[mt] = static_cast<uint32_t>((qb * pps + lk) * 16);
   }
+  const uint32_t bbase = static_cast<uint32_t>(((wo * kBN + lrow) * p.b_pitch + 8 * lk) * 2);
 
   f32x4_t acc[MT][4];
 #pragma unroll
@@ -307,7 +354,7 @@ __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
 #pragma unroll
     for (int ot = 0; ot < 4; ++ot) acc[mt][ot] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
 
-  // ---- multiply the chunk held in buffer `buf` ----
+  // ---- multiply one chunk: weights at LDS offset wofs (+ column col0), patch at pofs ----
   // Reduction steps of 32 columns run tap-major; the operand fragments of
   // step s+1 are read from LDS while the MFMAs of step s issue (two register
   // sets, statically alternated; every read is unconditional so the
@@ -316,22 +363,19 @@ __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
     bf16x8_t w[4];
     bf16x8_t x[MT];
   };
-  // A-fragment LDS byte offset of each tile at tap (0,0), k-step 0.
-  uint32_t abase[MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-    abase[mt] = static_cast<uint32_t>(p.b_bytes + (qbase[mt] * pps + lk) * 16);
-  const uint32_t bbase = static_cast<uint32_t>(((wo * kBN + lrow) * p.b_pitch + 8 * lk) * 2);
-  const uint32_t kw_mul = static_cast<uint32_t>((1u << 20) / p.KW + 1);  // tap / KW for tap < 4096
-
-  auto compute = [&](int buf) {
-    const uint8_t* base = lds + buf * p.buf_bytes;
+  // Loaders first issue the next chunk's patch DMA (chunk `dch` into LDS at
+  // `dofs`; dch < 0: none).  While a loader waits for room in the memory
+  // queue, the expander wave sharing its SIMD keeps the matrix core busy.
+  auto compute = [&](uint32_t wofs, uint32_t pofs, int dch, uint32_t dofs) {
+    const uint8_t* wb = lds + wofs + bbase;
+    const uint8_t* pb = lds + pofs;
+    if (loader && dch >= 0) issue_patch(dch, dofs);
     const int nsteps = p.taps << p.lg_ksteps;
     auto addr = [&](int st, uint32_t& aoff, uint32_t& boff) {
       // step -> (tap, kb) -> (kh, kw): shifts and one multiply, all scalar
       const int tap = st >> p.lg_ksteps;
       const int kb = st & ((1 << p.lg_ksteps) - 1);
-      const int kh = static_cast<int>((static_cast<uint32_t>(tap) * kw_mul) >> 20);
+      const int kh = static_cast<int>((static_cast<uint32_t>(tap) * p.kw_mul) >> 20);
       const int kw = tap - kh * p.KW;
       const int32_t dq = RECT ? kh * p.patch_cols + kw : 0;
       aoff = static_cast<uint32_t>(dq * pps * 16 + kb * 64);
@@ -340,10 +384,10 @@ __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
     auto load_w = [&](uint32_t boff, Frags& f) {
 #pragma unroll
       for (int ot = 0; ot < 4; ++ot)
-        f.w[ot] = as_bf16x8(*reinterpret_cast<const u32x4_t*>(base + bbase + boff + ot * 16 * p.b_pitch * 2));
+        f.w[ot] = as_bf16x8(*reinterpret_cast<const u32x4_t*>(wb + boff + ot * 16 * p.b_pitch * 2));
     };
     auto load_x = [&](uint32_t aoff, int mt, Frags& f) {
-      f.x[mt] = as_bf16x8(*reinterpret_cast<const u32x4_t*>(base + abase[mt] + aoff));
+      f.x[mt] = as_bf16x8(*reinterpret_cast<const u32x4_t*>(pb + abase[mt] + aoff));
     };
     // One reduction step on `cur` while the fragments of step `nst` stream
     // into `nxt`: each tile's 4 MFMAs are followed by one LDS read, so every
@@ -380,108 +424,146 @@ __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
   };
 
   // ---- chunk pipeline -----------------------------------------------------
-  // Chunk j's packed rows are loaded into registers before its patch DMA is
-  // issued, so the expansion waits only for them (the DMA keeps streaming);
-  // the DMA of chunk j is waited for just before chunk j is multiplied.
-  // With two buffers, chunk j+1's loads, DMA and zero fill are issued before
-  // chunk j is multiplied.  One call site for compute() keeps the
-  // accumulators in place (no copies at control-flow joins).
-  const bool dbl = p.nbuf == 2;
-  Packed P;
-  load_packed(0, P);
-  issue_patch(0, 0);
-  zero_weights(0);
-  lds_barrier();             // zero fill visible to every wave
-  scatter_weights(0, P);     // waits for the packed loads only
-  if (dbl && p.nchunks > 1) {
-    load_packed(1, P);
-    issue_patch(1, 1);
-    zero_weights(1);
-    wait_vm<kPackedOps + kDmaMax>();  // chunk 0's patch landed
+  // Loaders stream patches through npb (1 or 2) buffers: chunk 0 from the
+  // first instructions, chunk j+1 during chunk j's MFMAs.  Expanders build
+  // the weight tile, once (resident) or per chunk through a ring of two
+  // tiles; a loader's MFMAs fill the SIMD its partner expander shares while
+  // that one builds.  One call site for compute() keeps the accumulators in
+  // place.
+  // The packed-row loads go into the memory queue ahead of the bulk of the
+  // patch DMA, which would otherwise hold them up.
+  lds_barrier();
+  if (loader) {
+#pragma unroll
+    for (int i = kDmaEarly; i < kDmaMax; ++i)
+      if (i < nd) dma(static_cast<uint32_t>(wofs_patch), i, doff[i]);
+    wait_vm<0>();  // chunk 0 landed (this wave's part)
   } else {
-    wait_vm<0>();
+    expand(0, 0, true);
+    if (!p.wres && p.nchunks > 1) {
+      expand(1, 1, false);
+      if (p.nchunks > 2) load_slots(2, 0);
+    }
   }
   lds_barrier();
+  int pb = 0;
   for (int ch = 0; ch < p.nchunks; ++ch) {
-    const int buf = dbl ? (ch & 1) : 0;
-    compute(buf);
+    const uint32_t wofs = p.wres ? static_cast<uint32_t>(ch * p.taps * p.cinb * 2) : static_cast<uint32_t>((ch & 1) * p.w_bytes);
+    const int nb = p.npb == 2 ? pb ^ 1 : 0;
+    // with two patch buffers the next chunk streams in during this one
+    const int dch = p.npb == 2 && ch + 1 < p.nchunks ? ch + 1 : -1;
+    compute(wofs, static_cast<uint32_t>(wofs_patch + pb * p.p_bytes), dch, static_cast<uint32_t>(wofs_patch + nb * p.p_bytes));
     if (ch + 1 < p.nchunks) {
-      lds_barrier();  // every wave is done with `buf`; a pending zero fill is visible
-      if (!dbl) {
-        load_packed(ch + 1, P);
-        issue_patch(ch + 1, 0);
-        zero_weights(0);
-        lds_barrier();
-        scatter_weights(0, P);
-        wait_vm<0>();
-      } else {
-        scatter_weights(buf ^ 1, P);
-        if (ch + 2 < p.nchunks) {
-          load_packed(ch + 2, P);
-          issue_patch(ch + 2, buf);
-          zero_weights(buf);
-          wait_vm<kPackedOps + kDmaMax>();  // chunk ch+1's patch landed
-        } else {
-          wait_vm<0>();
+      const bool refill_w = !p.wres && ch + 2 < p.nchunks;
+      if (refill_w || p.npb == 1) {
+        lds_barrier();  // every wave is done with chunk ch's buffers
+        if (loader) {
+          if (p.npb == 1) issue_patch(ch + 1, static_cast<uint32_t>(wofs_patch));
+        } else if (refill_w) {
+          expand(ch + 2, ch & 1, true);
+          if (ch + 3 < p.nchunks) load_slots(ch + 3, 0);
         }
       }
+      if (loader) wait_vm<0>();  // chunk ch+1 landed
       lds_barrier();
+      pb = nb;
     }
   }
 
-  // ---- fused epilogue: lane holds outputs o..o+3 (o = o_wave+16ot+4lk) of one pixel ----
+  // ---- fused epilogue, staged through LDS ---------------------------------
+  // A lane's accumulators are 4 consecutive outputs of one pixel per (tile,
+  // 16-output block).  Each wave parks its fp32 block (MT*16 pixels x 64
+  // outputs) in LDS and reads it back transposed: a lane then owns 8
+  // consecutive outputs of one pixel, applies scale/bias/residual/ReLU,
+  // rounds once and writes them with one store, so 8 lanes write a pixel's
+  // whole run of 64 outputs.
+  lds_barrier();  // every wave is done with the operand buffers
+  uint8_t* stg = lds + wave * (MT * 16 * kStPitch);
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int ot = 0; ot < 4; ++ot)
+      *reinterpret_cast<f32x4_t*>(stg + (mt * 16 + lrow) * kStPitch + (ot * 16 + 4 * lk) * 4) = acc[mt][ot];
   const __amdgpu_buffer_rsrc_t yr =
       __builtin_amdgcn_make_buffer_rsrc(p.Y, (short)0, static_cast<int>(p.y_bytes), kRsrcWord3);
   const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<void*>(p.residual), (short)0, p.residual ? static_cast<int>(p.y_bytes) : 0, kRsrcWord3);
-  f32x4_t sc[4], bi[4];
-  uint32_t ooff[4];
+  const int c8 = lane & 7;                 // 8-output block of the wave's 64
+  const int32_t o = o_wave + 8 * c8;
+  // O % 4 == 0: a block holds 8, 4 (the last one) or no valid outputs
+  const int nvalid = o + 8 <= p.O ? 8 : (o < p.O ? 4 : 0);
+  f32x4_t sc0{1.f, 1.f, 1.f, 1.f}, sc1{1.f, 1.f, 1.f, 1.f}, bi0{0.f, 0.f, 0.f, 0.f}, bi1{0.f, 0.f, 0.f, 0.f};
+  if (p.scale && nvalid) sc0 = *reinterpret_cast<const f32x4_t*>(p.scale + o);
+  if (p.scale && nvalid == 8) sc1 = *reinterpret_cast<const f32x4_t*>(p.scale + o + 4);
+  if (p.bias && nvalid) bi0 = *reinterpret_cast<const f32x4_t*>(p.bias + o);
+  if (p.bias && nvalid == 8) bi1 = *reinterpret_cast<const f32x4_t*>(p.bias + o + 4);
 #pragma unroll
-  for (int ot = 0; ot < 4; ++ot) {
-    const int32_t o = o_wave + ot * 16 + 4 * lk;
-    const bool ok = o < p.O;
-    ooff[ot] = ok ? static_cast<uint32_t>(o) * ysz : kOOB;
-    sc[ot] = (p.scale && ok) ? *reinterpret_cast<const f32x4_t*>(p.scale + o) : f32x4_t{1.f, 1.f, 1.f, 1.f};
-    bi[ot] = (p.bias && ok) ? *reinterpret_cast<const f32x4_t*>(p.bias + o) : f32x4_t{0.f, 0.f, 0.f, 0.f};
-  }
+  for (int r = 0; r < MT * 2; ++r) {  // 8 pixels per pass
+    const int lp = r * 8 + (lane >> 3);  // wave-local staged pixel
+    const int mt = r >> 1;
+    if (mt == MT - 1 && !last_tile) break;  // wave-uniform: empty tile slot
+    const int32_t px = (wp + mt * p.WP) * 16 + (lp & 15);
+    const f32x4_t a0 = *reinterpret_cast<const f32x4_t*>(stg + lp * kStPitch + c8 * 32);
+    const f32x4_t a1 = *reinterpret_cast<const f32x4_t*>(stg + lp * kStPitch + c8 * 32 + 16);
+    uint32_t n;
+    if constexpr (RECT) {
+      const int32_t orow = static_cast<int32_t>(fdiv(px, p.fd_wo));
+      n = static_cast<uint32_t>((b_img * p.Ho + oh0 + orow) * p.Wo + (px - orow * p.Wo));
+    } else {
+      n = static_cast<uint32_t>(P0 + px);
+    }
+    const bool ok = px < npix && nvalid > 0;
+    const uint32_t off = ok ? (n * static_cast<uint32_t>(p.O) + static_cast<uint32_t>(o)) * ysz : kOOB;
+    const uint32_t off_hi = ok && nvalid == 8 ? off + 4 * ysz : kOOB;  // outputs o+4..o+7
+    f32x4_t y0, y1;
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {  // padding tiles have out-of-range offsets
-#pragma unroll
-    for (int ot = 0; ot < 4; ++ot) {
-      const uint32_t off = yoff[mt] + ooff[ot];  // >= 2^31 if either is out of range
-      f32x4_t y;
-#pragma unroll
-      for (int jj = 0; jj < 4; ++jj) y[jj] = __builtin_fmaf(acc[mt][ot][jj], sc[ot][jj], bi[ot][jj]);
+    for (int jj = 0; jj < 4; ++jj) {
+      y0[jj] = __builtin_fmaf(a0[jj], sc0[jj], bi0[jj]);
+      y1[jj] = __builtin_fmaf(a1[jj], sc1[jj], bi1[jj]);
+    }
+    if (p.residual) {
       if constexpr (ysz == 2) {
-        if (p.residual) {
-          const u32x2_t rv = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(rr, off, 0, 0));
-          y[0] += __uint_as_float(rv[0] << 16);
-          y[1] += __uint_as_float(rv[0] & 0xffff0000u);
-          y[2] += __uint_as_float(rv[1] << 16);
-          y[3] += __uint_as_float(rv[1] & 0xffff0000u);
-        }
-        if (p.relu) {
-#pragma unroll
-          for (int jj = 0; jj < 4; ++jj) y[jj] = y[jj] > 0.0f ? y[jj] : (y[jj] != y[jj] ? y[jj] : 0.0f);
-        }
-        // v_cvt_pk_bf16_f32: round to nearest even
-        const bf16x2_t lo = __builtin_convertvector((f32x2_t{y[0], y[1]}), bf16x2_t);
-        const bf16x2_t hi = __builtin_convertvector((f32x2_t{y[2], y[3]}), bf16x2_t);
-        const u32x2_t pk = {__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
-        __builtin_amdgcn_raw_buffer_store_b64(
-            __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b64(yr, 0, 0, 0)), pk), yr, off, 0, 0);
+        const u32x2_t r0 = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(rr, off, 0, 0));
+        const u32x2_t r1 = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(rr, off_hi, 0, 0));
+        y0[0] += __uint_as_float(r0[0] << 16);
+        y0[1] += __uint_as_float(r0[0] & 0xffff0000u);
+        y0[2] += __uint_as_float(r0[1] << 16);
+        y0[3] += __uint_as_float(r0[1] & 0xffff0000u);
+        y1[0] += __uint_as_float(r1[0] << 16);
+        y1[1] += __uint_as_float(r1[0] & 0xffff0000u);
+        y1[2] += __uint_as_float(r1[1] << 16);
+        y1[3] += __uint_as_float(r1[1] & 0xffff0000u);
       } else {
-        if (p.residual) {
-          const f32x4_t rv = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rr, off, 0, 0));
-          y += rv;
-        }
-        if (p.relu) {
-#pragma unroll
-          for (int jj = 0; jj < 4; ++jj) y[jj] = y[jj] > 0.0f ? y[jj] : (y[jj] != y[jj] ? y[jj] : 0.0f);
-        }
-        __builtin_amdgcn_raw_buffer_store_b128(
-            __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b128(yr, 0, 0, 0)), y), yr, off, 0, 0);
+        y0 += __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rr, off, 0, 0));
+        y1 += __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rr, off_hi, 0, 0));
       }
+    }
+    if (p.relu) {
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        y0[jj] = y0[jj] > 0.0f ? y0[jj] : (y0[jj] != y0[jj] ? y0[jj] : 0.0f);
+        y1[jj] = y1[jj] > 0.0f ? y1[jj] : (y1[jj] != y1[jj] ? y1[jj] : 0.0f);
+      }
+    }
+    if constexpr (ysz == 2) {
+      // v_cvt_pk_bf16_f32: round to nearest even
+      const u32x4_t pk = {__builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{y0[0], y0[1]}), bf16x2_t)),
+                          __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{y0[2], y0[3]}), bf16x2_t)),
+                          __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{y1[0], y1[1]}), bf16x2_t)),
+                          __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{y1[2], y1[3]}), bf16x2_t))};
+      if (nvalid == 8 || !ok) {
+        __builtin_amdgcn_raw_buffer_store_b128(
+            __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b128(yr, 0, 0, 0)), pk), yr, off, 0, 0);
+      } else {  // last block of 4
+        const u32x2_t lo = {pk[0], pk[1]};
+        __builtin_amdgcn_raw_buffer_store_b64(
+            __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b64(yr, 0, 0, 0)), lo), yr, off, 0, 0);
+      }
+    } else {
+      __builtin_amdgcn_raw_buffer_store_b128(
+          __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b128(yr, 0, 0, 0)), y0), yr, off, 0, 0);
+      __builtin_amdgcn_raw_buffer_store_b128(
+          __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b128(yr, 0, 0, 0)), y1), yr, off_hi, 0, 0);
     }
   }
 }
@@ -499,46 +581,85 @@ int ilog2(int v) {
   return l;
 }
 
-// Fill the LDS layout for a channel chunk; false if it does not fit the LDS,
-// the per-thread DMA budget or the per-thread expansion budget.
-bool layout(Params& pl, int32_t cinb, int32_t Cin, int32_t nbuf, int32_t G, int32_t K) {
+// Fill the chunk and LDS layout; false if it does not fit the LDS, the
+// per-thread DMA budget or the per-thread expansion budget.
+bool layout(Params& pl, int32_t cinb, int32_t Cin, int32_t wres, int32_t npb, int32_t G, int32_t K) {
   pl.cinb = cinb;
   pl.lg_cpp = ilog2(cinb / 8);
   pl.lg_ksteps = ilog2(cinb / kKS);
   pl.nchunks = Cin / cinb;
-  pl.b_pitch = pl.taps * cinb + kBPad;
-  pl.b_bytes = pl.WO * kBN * pl.b_pitch * 2;
-  const int64_t slots = static_cast<int64_t>(pl.patch_pix) * (cinb / 8 + 1);
-  if (slots > static_cast<int64_t>(kDmaMax) * kThreads) return false;
-  pl.ncols8 = pl.taps * (cinb / 8);
-  if (pl.ncols8 > kThreads) return false;
-  pl.rstep = kThreads / pl.ncols8;
+  if (!wres && pl.nchunks < 2) return false;
+  if (npb < 1 || npb > pl.nchunks) return false;
+  const int32_t cpp = cinb / 8, pps = cpp + 1;
+  const int64_t slots = static_cast<int64_t>(pl.patch_pix) * pps;
+  if (slots > static_cast<int64_t>(kDmaMax) * kRoleThreads) return false;
+  pl.slots = static_cast<int32_t>(slots);
+  const int32_t tc = pl.taps * cpp;
+  pl.wres = wres;
+  pl.ncols8 = wres ? pl.nchunks * tc : tc;
+  pl.b_pitch = pl.ncols8 * 8 + kBPad;
+  pl.w_bytes = pl.WO * kBN * pl.b_pitch * 2;
   pl.nrows = (pl.WO * kBN / G) * K;
-  if ((pl.nrows + pl.rstep - 1) / pl.rstep > kRowMax) return false;
-  // The DMA writes whole 64-slot (1 KiB) blocks: round the patch up so the
-  // tail of its last block stays inside this buffer, and keep at least one
-  // block per wave (a wave without a slot writes its first block).
-  int64_t patch_bytes = (slots * 16 + 1023) / 1024 * 1024;
-  if (patch_bytes < kWaves * 1024) patch_bytes = kWaves * 1024;
-  const int64_t buf = pl.b_bytes + patch_bytes;
-  if (buf * nbuf > kLdsMax) return false;
-  pl.buf_bytes = static_cast<int32_t>(buf);
-  pl.nbuf = nbuf;
-  pl.fd_pps = make_fastdiv(cinb / 8 + 1);
+  pl.nu = ((pl.WO * kBN / G) * pl.ncols8 + kRoleThreads - 1) / kRoleThreads;
+  if (pl.nu * K > 4 * kRowMax) return false;  // at most four load rounds per expansion
+  pl.nwb = wres ? 1 : 2;
+  // the DMA writes whole 64-slot (1 KiB) blocks: round the patch up so the
+  // tail of its last block stays inside its buffer
+  pl.p_bytes = static_cast<int32_t>((slots * 16 + 1023) / 1024 * 1024);
+  pl.npb = npb;
+  if (static_cast<int64_t>(pl.nwb) * pl.w_bytes + static_cast<int64_t>(npb) * pl.p_bytes > kLdsMax) return false;
+  pl.dq = kRoleThreads / pps;
+  pl.dc = kRoleThreads % pps;
+  // rect: dq pixels = dpr patch rows + diw patch columns; rows: diw = dq pixels
+  pl.dpr = pl.patch_cols > 0 ? pl.dq / pl.patch_cols : 0;
+  pl.diw = pl.patch_cols > 0 ? pl.dq % pl.patch_cols : pl.dq;
+  pl.fd_pps = make_fastdiv(pps);
   pl.fd_k = make_fastdiv(K);
   pl.fd_ncols8 = make_fastdiv(pl.ncols8);
+  pl.fd_tc = make_fastdiv(tc);
   return true;
 }
 
-// Choose the wave arrangement, pixel partition and channel chunk.  Costs are
-// in MFMA issue slots (16 cycles) on the busiest CU (one workgroup per CU at
-// a time): the MFMAs of its busiest wave, the exposed patch loads (bytes at
-// one CU's share of HBM bandwidth, ~13 B/clk), the weight-tile expansion and
-// a charge for re-reading activations once per extra output super-block.
+// Modelled duration (cycles) of one workgroup: a chunk's patch streams at
+// one CU's share of HBM bandwidth (~13 B/clk) once its buffer is free (two
+// buffers: from the start of the previous chunk's MFMAs); its MFMAs start
+// when it has arrived, its weights are expanded and the previous chunk is
+// done.
+double model_cycles(const Params& t, double mfma_chunk, double store, int K) {
+  const double load = t.patch_pix * static_cast<double>(t.cinb) * 2.0 / 13.0;
+  // expansion by the 256 expander threads: zero fill (b128 writes) and
+  // K packed-row segments per unit
+  const double build = t.w_bytes / 16.0 / kRoleThreads * 8.0 + t.nu * K * 120.0;
+  const double latency = 1500.0, barrier = 150.0, setup = 1500.0;
+  const double e_first = setup + latency + build * (t.wres ? 1 : 2);
+  double arrive = setup / 2 + latency + load, done = 0.0, start = 0.0;
+  double done2 = 0.0;  // done time of chunk c-2
+  const int n = t.nchunks;
+  for (int c = 0; c < n; ++c) {
+    if (c > 0) {
+      const double issue = t.npb == 2 ? start : done + barrier;
+      arrive = (issue > arrive ? issue : arrive) + load;
+    }
+    double ready_w = e_first;
+    if (!t.wres && c >= 2) ready_w = done2 + barrier + build;
+    double st = c == 0 ? 0.0 : done + barrier;
+    st = st > arrive ? st : arrive;
+    st = st > ready_w ? st : ready_w;
+    start = st;
+    done2 = done;
+    done = st + mfma_chunk;
+  }
+  return done + store;
+}
+
+// Choose the wave arrangement, pixel partition, channel chunk and LDS plan
+// with the smallest modelled time on the busiest CU (one workgroup per CU at
+// a time).
 bool make_plan(const ProductArgs& a, Params& best, uint32_t& grid) {
   const int32_t Cin = a.conv ? a.geom.Cin : static_cast<int32_t>(a.C);
   const bool rows = is_rows_mode(a);
   const int32_t taps = a.conv ? a.geom.KH * a.geom.KW : 1;
+  const int64_t ysz = a.y_t == DType::F32 ? 4 : 2;
   double best_cost = 1e300;
   bool found = false;
   for (int WO = 1; WO <= 8; WO *= 2) {
@@ -558,6 +679,7 @@ bool make_plan(const ProductArgs& a, Params& best, uint32_t& grid) {
         parts = (a.N + pix_per_part - 1) / pix_per_part;
         pl.part_len = static_cast<int32_t>(pix_per_part);
         pl.patch_pix = static_cast<int32_t>(pix_per_part);
+        pl.patch_cols = 0;
       } else {
         const int64_t RH = len;
         if (RH > a.geom.Ho) break;
@@ -570,29 +692,7 @@ bool make_plan(const ProductArgs& a, Params& best, uint32_t& grid) {
         const int32_t prow = static_cast<int32_t>((RH - 1) * a.geom.sh + a.geom.KH);
         pl.patch_pix = prow * pl.patch_cols;
       }
-      double cbest = 1e300;
-      Params pbest{};
-      for (int32_t cinb = 512; cinb >= kKS; cinb /= 2) {
-        if (Cin % cinb) continue;
-        for (int32_t nbuf = 1; nbuf <= 2; ++nbuf) {
-          Params t = pl;
-          if (nbuf == 2 && Cin / cinb < 2) continue;
-          if (!layout(t, cinb, Cin, nbuf, a.G, a.K)) continue;
-          // the first chunk's patch streams under its expansion; with two
-          // buffers later patches stream under the MFMAs
-          const double load = t.patch_pix * static_cast<double>(cinb) * 2.0 / 208.0;
-          const double expand = t.b_bytes / 2048.0 + 16.0;
-          const double first = load > expand ? load : expand;
-          const double rest = (t.nchunks - 1) * (nbuf == 2 ? expand * 0.5 : load + expand);
-          const double c = first + rest + 8.0 * (t.nchunks - 1);
-          if (c < cbest) {
-            cbest = c;
-            pbest = t;
-          }
-        }
-      }
-      if (cbest >= 1e299) continue;
-      const int64_t wgs = parts * pbest.nob;
+      const int64_t wgs = parts * pl.nob;
       const int64_t per_cu = (wgs + 255) / 256;
       const int64_t tiles = (pix_per_part + 15) / 16;
       const int64_t tiles_per_wave = (tiles + WP - 1) / WP;  // instantiated: 1..4
@@ -606,17 +706,26 @@ bool make_plan(const ProductArgs& a, Params& best, uint32_t& grid) {
         }
         simd_tiles = t2 > simd_tiles ? t2 : simd_tiles;
       }
-      const double mfma = static_cast<double>(simd_tiles) * taps * (Cin / kKS) * 4.0;
-      const double reread = (pbest.nob - 1) * static_cast<double>(pix_per_part) * taps * Cin * 2.0 / 4096.0 / 16.0;
-      const double cost = static_cast<double>(per_cu) * (mfma + cbest + reread);
-      if (cost < best_cost) {
-        best_cost = cost;
-        best = pbest;
-        const int64_t parts8 = (parts + kXcds - 1) / kXcds * kXcds;
-        best.fd_nob = make_fastdiv(static_cast<uint32_t>(best.nob));
-        best.mt = static_cast<int32_t>(tiles_per_wave);
-        grid = static_cast<uint32_t>(parts8 * best.nob);
-        found = true;
+      const double store = static_cast<double>(pix_per_part) * WO * kBN * ysz / 13.0;
+      for (int32_t cinb = 512; cinb >= kKS; cinb /= 2) {
+        if (Cin % cinb) continue;
+        const double mfma_chunk = static_cast<double>(simd_tiles) * taps * (cinb / kKS) * 4.0 * 16.0;
+        for (int32_t wres = 1; wres >= 0; --wres) {
+          for (int32_t npb = 1; npb <= 2; ++npb) {
+            Params t = pl;
+            if (!layout(t, cinb, Cin, wres, npb, a.G, a.K)) continue;
+            const double cost = static_cast<double>(per_cu) * model_cycles(t, mfma_chunk, store, a.K);
+            if (cost < best_cost) {
+              best_cost = cost;
+              best = t;
+              const int64_t parts8 = (parts + kXcds - 1) / kXcds * kXcds;
+              best.fd_nob = make_fastdiv(static_cast<uint32_t>(best.nob));
+              best.mt = static_cast<int32_t>(tiles_per_wave);
+              grid = static_cast<uint32_t>(parts8 * best.nob);
+              found = true;
+            }
+          }
+        }
       }
     }
   }
@@ -667,6 +776,7 @@ void fill_params(const ProductArgs& a, Params& p) {
   p.fd_wo = make_fastdiv(static_cast<uint32_t>(g.Wo));
   p.fd_pcols = make_fastdiv(static_cast<uint32_t>(p.patch_cols > 0 ? p.patch_cols : 1));
   p.fd_howo = make_fastdiv(static_cast<uint32_t>(g.Ho * g.Wo));
+  p.kw_mul = static_cast<uint32_t>((1u << 20) / static_cast<uint32_t>(g.KW) + 1);
 }
 
 template <typename YT, bool RECT, int MT>
@@ -675,7 +785,9 @@ hipError_t launch_yrm(const Params& p, uint32_t grid, hipStream_t s) {
       reinterpret_cast<const void*>(&dense_tile_kernel<YT, RECT, MT>), hipFuncAttributeMaxDynamicSharedMemorySize,
       kLdsMax);
   if (attr != hipSuccess) return attr;
-  const size_t lds = static_cast<size_t>(p.buf_bytes) * p.nbuf;
+  size_t lds = static_cast<size_t>(p.nwb) * p.w_bytes + static_cast<size_t>(p.npb) * p.p_bytes;
+  const size_t staging = static_cast<size_t>(kWaves) * MT * 16 * kStPitch;  // epilogue reuses the LDS
+  if (lds < staging) lds = staging;
   hipLaunchKernelGGL((dense_tile_kernel<YT, RECT, MT>), dim3(grid), dim3(kThreads), lds, s, p);
   return hipGetLastError();
 }
@@ -703,7 +815,9 @@ bool dense_tile_supports(const ProductArgs& a) {
   const int64_t y_bytes = a.N * a.O * (a.y_t == DType::F32 ? 4 : 2);
   const int64_t p_bytes = (a.O / a.G) * a.K * a.C * 2;
   const int64_t lim = static_cast<int64_t>(kOOB);
-  if (x_elems * 2 >= lim || y_bytes >= lim || p_bytes >= lim) return false;
+  // (the loaders walk signed byte offsets that may pass the last image by
+  // a few rows of padding: keep X well below the limit)
+  if (x_elems * 2 >= lim / 2 || y_bytes >= lim || p_bytes >= lim) return false;
   Params pl;
   uint32_t grid;
   return make_plan(a, pl, grid);

@@ -18,6 +18,14 @@ The layer shapes stand in for the paper's ImageNet / CIFAR CNN layers
              W ~ N(0, 2/1024), G=16, K=4 or 2 (75% / 87.5%)
   fc4096     FC sweep, X bf16 [4096,4096] ~ N(0,1), W [4096,4096] ~ N(0,1/4096),
              G=16, K in {1,2,4,8,16} (K=16 is the dense control)
+  resnet50   ResNet-50-shaped forward (torchvision v1.5 layout: stride on the 3x3
+             conv), images bf16 [B,224,224,3] ~ N(0,1); every conv He-initialised
+             W ~ N(0, 2/fan_in) with CCI G=8, K=2 except the first conv (dense:
+             K=G); batch norm at its initial state folded into the epilogue
+             (scale 1/sqrt(1+1e-5), bias 0); FC 2048->1000 W ~ N(0, 1/2048),
+             dense (K=G), fp32 logits.  Draw order: images, then every conv in
+             network order (stem, then per bottleneck c1, c2, c3, downsample),
+             then the FC.
 """
 from __future__ import annotations
 
@@ -142,3 +150,86 @@ def draw_epilogue(wl: Workload, *, scale=True, bias=True, residual=False, seed_o
 def small(wl: Workload, **kw) -> Workload:
     """A reduced copy of a workload (same G, K, dtypes, distributions)."""
     return wl.with_(**kw)
+
+
+# ---------------------------------------------------------------------------
+# ResNet-50-shaped forward
+
+
+@dataclass(frozen=True)
+class ConvLayer:
+    name: str
+    Cin: int
+    Cout: int
+    k: int
+    stride: int
+    pad: int
+    K: int                 # kept weights per group (K == G: dense)
+    relu: bool             # ReLU in the epilogue
+    residual: str = ""     # c3 only: "identity" or "downsample"
+
+    @property
+    def fan_in(self) -> int:
+        return self.k * self.k * self.Cin
+
+
+BN_EPS = 1e-5
+RESNET50_STAGES = ((64, 256, 3, 1), (128, 512, 4, 2), (256, 1024, 6, 2), (512, 2048, 3, 2))
+
+
+def resnet50_layers(G: int = 8, K: int = 2) -> list[ConvLayer]:
+    """The 53 convolutions of ResNet-50 (v1.5) in network order."""
+    layers = [ConvLayer("conv1", 3, 64, 7, 2, 3, G, True)]
+    cin = 64
+    for si, (mid, out, blocks, stride) in enumerate(RESNET50_STAGES):
+        for bi in range(blocks):
+            s = stride if bi == 0 else 1
+            pre = f"layer{si + 1}.{bi}"
+            ds = bi == 0
+            layers.append(ConvLayer(f"{pre}.c1", cin, mid, 1, 1, 0, K, True))
+            layers.append(ConvLayer(f"{pre}.c2", mid, mid, 3, s, 1, K, True))
+            layers.append(ConvLayer(f"{pre}.c3", mid, out, 1, 1, 0, K, True,
+                                    "downsample" if ds else "identity"))
+            if ds:
+                layers.append(ConvLayer(f"{pre}.ds", cin, out, 1, s, 0, K, False))
+            cin = out
+    return layers
+
+
+@dataclass(frozen=True)
+class ResNet50:
+    B: int = 64
+    HW: int = 224
+    G: int = 8
+    K: int = 2
+    classes: int = 1000
+    seed: int = 0
+
+    @property
+    def layers(self) -> list[ConvLayer]:
+        return resnet50_layers(self.G, self.K)
+
+
+def draw_resnet50(net: ResNet50):
+    """Return (X, conv_weights, fc_weight): X torch bf16 NHWC [B, HW, HW, 3];
+    conv_weights a list of fp32 numpy [Cout, k*k*Cin] ((kh, kw, cin) order),
+    one per layer of ``net.layers``; fc_weight fp32 numpy [classes, 2048]."""
+    import torch
+
+    rng = np.random.Generator(np.random.PCG64(net.seed))
+    x = rng.standard_normal((net.B, net.HW, net.HW, 3)).astype(np.float32)
+    X = torch.from_numpy(x).to(torch.bfloat16)
+    ws = []
+    for L in net.layers:
+        w = rng.standard_normal((L.Cout, L.fan_in)) * (2.0 / L.fan_in) ** 0.5
+        ws.append(np.ascontiguousarray(w.astype(np.float32)))
+    fc_in = RESNET50_STAGES[-1][1]
+    fcw = rng.standard_normal((net.classes, fc_in)) * (1.0 / fc_in) ** 0.5
+    return X, ws, np.ascontiguousarray(fcw.astype(np.float32))
+
+
+def bn_fold(C: int):
+    """Batch norm at its initial state (gamma 1, beta 0, mean 0, var 1) folded
+    into a per-channel scale and bias (fp32 numpy)."""
+    scale = np.full(C, 1.0 / np.sqrt(1.0 + BN_EPS), np.float32)
+    return scale, np.zeros(C, np.float32)

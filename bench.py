@@ -46,6 +46,9 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target wall time of the CPU oracle sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-dense", action="store_true")
+    p.add_argument("--sweep", action="store_true",
+                   help="instead of the headline line: one JSON line per configuration (FC, 1x1, 3x3, "
+                        "FC K-sweep, ResNet-50 forward) with CCI and dense bf16 times")
     p.add_argument("--calibrate-copy-mb", type=float, default=0.0,
                    help="only run a plain device copy of this many MB (x5) and exit: the reference "
                         "kernel for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes")
@@ -77,8 +80,8 @@ def load_traffic(workload: str, kernel: str, src_hash: str):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: the CCI path has no multi-GPU part in this build "
-              "(rows or output groups would shard with no exchange; see DESIGN.md). Use --gpus 1.",
+        print("bench.py measures one GPU: the CCI product shards by rows or by output groups with no "
+              "exchange, and only the one-GPU kernel is implemented. Use --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
 
@@ -95,6 +98,9 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"calibration_copy_bytes_each_way": n * 4, "launches": 5}), flush=True)
         return
+
+    if args.sweep:
+        return sweep(args)
 
     wl = workloads.WORKLOADS[args.workload]
     if not wl.conv:
@@ -279,6 +285,194 @@ def main():
         "source_hash": src_hash,
     }
     print(json.dumps(out), flush=True)
+
+
+def _graph_time(fn, n_launch, reps, stream):
+    """Average duration of fn(i) for i < n_launch, captured in one HIP graph
+    and replayed `reps` times (no host launch cost between kernels)."""
+    import torch
+    with torch.cuda.stream(stream):
+        for i in range(n_launch):
+            fn(i)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        for i in range(n_launch):
+            fn(i)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        g.replay()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(reps):
+            g.replay()
+        b.record(stream)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / (reps * n_launch)
+
+
+def _eager_time(fn, n, stream):
+    import torch
+    with torch.cuda.stream(stream):
+        for i in range(5):
+            fn(i)
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for i in range(n):
+            fn(i)
+        b.record(stream)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / n
+
+
+def _roof(kname, flop, dense_flop, alg_bytes, t_ms):
+    if kname == "cci_dense_tile":
+        t_hbm = alg_bytes / (PEAK["hbm_GBps"] * 1e9)
+        t_mfma = dense_flop / (PEAK["mfma_bf16_TFLOPs"] * 1e12)
+        if t_hbm >= t_mfma:
+            return {"bound": "hbm", "frac": round(t_hbm / (t_ms * 1e-3), 4)}
+        return {"bound": "mfma", "frac": round(t_mfma / (t_ms * 1e-3), 4)}
+    t_alu = flop / (PEAK["valu_fp32_TFLOPs"] * 1e12)
+    return {"bound": "alu", "frac": round(t_alu / (t_ms * 1e-3), 4)}
+
+
+def sweep(args):
+    """One JSON line per configuration: CCI kernel time (HIP-graph replays over
+    rotated inputs), cci_pack time, effective TFLOP/s (2*N*nnz), the roofline
+    fraction, and the dense bf16 comparators of the same shape."""
+    import numpy as np
+    import torch
+    from paper_1910_11971_amd import cci, workloads
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.Stream(device=dev)
+    names = ["fc256", "conv3x3", "conv1x1_k4", "conv1x1_k2"] + [f"fc4096_k{k}" for k in (1, 2, 4, 8, 16)]
+    for name in names:
+        wl = workloads.WORKLOADS[name]
+        X_cpu, W_np = workloads.draw(wl)
+        xdt = torch.bfloat16 if wl.x_dtype == "bf16" else torch.float32
+        ydt = torch.bfloat16 if wl.y_dtype == "bf16" else torch.float32
+        ysz = 2 if ydt == torch.bfloat16 else 4
+        x_bytes = X_cpu.numel() * X_cpu.element_size()
+        y_bytes = wl.N * wl.O * ysz
+        ncopy = max(1, int(np.ceil(args.rotate_mb * 1e6 / (x_bytes + y_bytes)))) if args.rotate_mb > 0 else 1
+        ncopy = min(ncopy, 24)
+        Xs = [X_cpu.to(dev) for _ in range(ncopy)]
+        if wl.conv:
+            Ys = [torch.empty((wl.B, wl.Ho, wl.Wo, wl.O), dtype=ydt, device=dev) for _ in range(ncopy)]
+        else:
+            Ys = [torch.empty((wl.N, wl.O), dtype=ydt, device=dev) for _ in range(ncopy)]
+        W = torch.from_numpy(W_np).to(dev)
+        vals, idx = cci.pack(W, wl.G, wl.K, xdt)
+        algo = cci.auto_algo(xdt, xdt, wl.N, wl.C, wl.Cin, wl.O, wl.G, wl.K)
+        kname = "cci_dense_tile" if algo == "dense_tile_mfma" else "cci_sparse_mac"
+        if wl.conv:
+            f = lambda i: cci.conv_im2col(Xs[i % ncopy], vals, idx, wl.G, wl.KH, wl.KW, (wl.stride,) * 2,
+                                          (wl.pad,) * 2, out_dtype=ydt, out=Ys[i % ncopy])
+        else:
+            f = lambda i: cci.spmm(Xs[i % ncopy], vals, idx, wl.G, out_dtype=ydt, out=Ys[i % ncopy])
+        n_launch = max(ncopy, 8)
+        t_cci = _graph_time(f, n_launch, max(2, 200 // n_launch), stream)
+        t_pack = _graph_time(lambda i: cci.pack(W, wl.G, wl.K, xdt, out=(vals, idx)), 16, 10, stream)
+        flop = 2.0 * wl.N * wl.nnz
+        dense_flop = 2.0 * wl.N * wl.C * wl.O
+        alg_bytes = x_bytes + wl.nnz * ((2 if xdt == torch.bfloat16 else 4) + 1) + y_bytes
+        out = {"workload": name, "N": wl.N, "C": wl.C, "O": wl.O, "G": wl.G, "K": wl.K, "algo": algo,
+               "cci_ms": round(t_cci, 5), "pack_ms": round(t_pack, 5),
+               "eff_TFLOPs": round(flop / (t_cci * 1e-3) / 1e12, 3),
+               "roofline": _roof(kname, flop, dense_flop, alg_bytes, t_cci), "rotated_copies": ncopy}
+        if xdt == torch.bfloat16:
+            Wd = W.to(torch.bfloat16)
+            Bt = Wd.t().contiguous()
+            if wl.conv and not (wl.KH == 1 and wl.stride == 1 and wl.pad == 0):
+                A = torch.nn.functional.unfold(Xs[0].permute(0, 3, 1, 2).float(), (wl.KH, wl.KW), padding=wl.pad,
+                                               stride=wl.stride)
+                A = A.reshape(wl.B, wl.Cin, wl.KH, wl.KW, -1).permute(0, 4, 2, 3, 1).reshape(wl.N, wl.C)
+                As = [A.to(torch.bfloat16).contiguous()]
+                del A
+            else:
+                As = [x.reshape(wl.N, wl.C) for x in Xs]
+            t_gemm = _eager_time(lambda i: torch.matmul(As[i % len(As)], Bt), 30, stream)
+            out["dense_gemm_ms"] = round(t_gemm, 5)
+            out["speedup_vs_dense_gemm"] = round(t_gemm / t_cci, 3)
+            if wl.conv:
+                Wc = W.reshape(wl.O, wl.KH, wl.KW, wl.Cin).permute(0, 3, 1, 2).to(torch.bfloat16).contiguous(
+                    memory_format=torch.channels_last)
+                Xn = [x.permute(0, 3, 1, 2) for x in Xs]
+                t_conv = _eager_time(lambda i: torch.nn.functional.conv2d(Xn[i % ncopy], Wc, stride=wl.stride,
+                                                                          padding=wl.pad), 30, stream)
+                out["miopen_conv2d_ms"] = round(t_conv, 5)
+                out["speedup_vs_conv2d"] = round(t_conv / t_cci, 3)
+            del As
+        print(json.dumps(out), flush=True)
+        del Xs, Ys, W, vals, idx
+        torch.cuda.empty_cache()
+    sweep_resnet50(stream)
+
+
+def sweep_resnet50(stream):
+    """ResNet-50-shaped forward at batch 64: the CCI network (one HIP graph per
+    forward) against the same network with dense bf16 weights on torch's
+    channels-last convolutions."""
+    import numpy as np
+    import torch
+    from paper_1910_11971_amd import workloads
+    from paper_1910_11971_amd.resnet import ResNet50CCI
+
+    net = workloads.ResNet50()
+    X, ws, fcw = workloads.draw_resnet50(net)
+    dev = torch.device("cuda:0")
+    model = ResNet50CCI(net, ws, fcw, device=dev)
+    Xd = X.to(dev)
+    t_cci = _graph_time(lambda i: model.forward(Xd), 1, 10, stream)
+    # effective flop of the CCI network: 2 * N * nnz summed over its layers
+    flop = 0.0
+    rec = []
+    model.forward(Xd, record=rec)
+    torch.cuda.synchronize()
+    for kind, key, inp, out, res in rec:
+        if kind == "conv":
+            L = net.layers[key]
+            flop += 2.0 * (out.numel() // L.Cout) * L.Cout * L.fan_in * L.K / net.G
+        elif kind == "fc":
+            flop += 2.0 * out.shape[0] * out.shape[1] * inp.shape[1]
+    del rec
+    # dense bf16 reference network, same layer sequence
+    sc = torch.tensor(1.0 / np.sqrt(1.0 + workloads.BN_EPS), device=dev)
+    Wd = [torch.from_numpy(w).to(dev).reshape(L.Cout, L.k, L.k, L.Cin).permute(0, 3, 1, 2)
+          .to(torch.bfloat16).contiguous(memory_format=torch.channels_last) for L, w in zip(net.layers, ws)]
+    Wfc = torch.from_numpy(fcw).to(dev).to(torch.bfloat16)
+    Xn = Xd.permute(0, 3, 1, 2)
+    F = torch.nn.functional
+
+    def dense_forward(_i):
+        def cv(i, x):
+            L = net.layers[i]
+            return F.conv2d(x, Wd[i], stride=L.stride, padding=L.pad) * sc.to(torch.bfloat16)
+        x = F.relu(cv(0, Xn))
+        x = F.max_pool2d(x, 3, 2, 1)
+        i = 1
+        while i < len(net.layers):
+            ds = i + 3 < len(net.layers) and net.layers[i + 3].name.endswith(".ds")
+            y = F.relu(cv(i, x))
+            y = F.relu(cv(i + 1, y))
+            ident = cv(i + 3, x) if ds else x
+            x = F.relu(cv(i + 2, y) + ident)
+            i += 4 if ds else 3
+        p = x.float().mean(dim=(2, 3)).to(torch.bfloat16)
+        return torch.matmul(p, Wfc.t().contiguous()).float()
+
+    t_dense = _eager_time(dense_forward, 5, stream)
+    print(json.dumps({"workload": "resnet50", "B": net.B, "HW": net.HW, "G": net.G, "K": net.K,
+                      "cci_forward_ms": round(t_cci, 4), "eff_TFLOPs": round(flop / (t_cci * 1e-3) / 1e12, 3),
+                      "dense_bf16_forward_ms": round(t_dense, 4),
+                      "speedup_vs_dense": round(t_dense / t_cci, 3),
+                      "images_per_s": round(net.B / (t_cci * 1e-3), 1)}), flush=True)
 
 
 if __name__ == "__main__":

@@ -12,7 +12,10 @@
 //     and the index selects an accumulator through a uniform branch tree --
 //     no per-lane dynamic register indexing;
 //   - the 4 waves of a workgroup share one X tile staged in LDS as fp32
-//     (each activation read from HBM once per workgroup, converted once).
+//     (each activation read from HBM once per workgroup, converted once);
+//   - each wave stages its groups' packed stream for the same columns in LDS
+//     (coalesced loads), so the per-slot reads in the inner loop are LDS
+//     broadcasts instead of dependent global loads.
 //
 // General path: any dtype combination, any C, conv through implicit im2col.
 #include "cci_launch.hpp"
@@ -23,6 +26,7 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
 constexpr int kCB = 32;  // reduction columns per LDS chunk
+constexpr int kSlotRows = 32;  // packed rows (group x slot) per wave: GPW*K <= 32
 
 // acc[r][i] += v * x[i] for the uniform row r, via a binary tree of uniform
 // branches over [LO, HI).
@@ -64,6 +68,8 @@ __global__ __launch_bounds__(kThreads) void sparse_mac_kernel(
   constexpr int PITCH = kCB + 1;  // odd pitch: lanes hit distinct banks
   __shared__ float xs[ROWS * PITCH];
   __shared__ int32_t pix_b[CONV ? ROWS : 1], pix_h[CONV ? ROWS : 1], pix_w[CONV ? ROWS : 1];
+  __shared__ float pv[kWaves][kSlotRows][kCB];    // packed values of this chunk (fp32)
+  __shared__ uint8_t pi[kWaves][kSlotRows][kCB];  // their intra-group row indices
 
   const int lane = threadIdx.x & 63;
   const int wave = uniform_i(threadIdx.x >> 6);
@@ -133,24 +139,68 @@ __global__ __launch_bounds__(kThreads) void sparse_mac_kernel(
         xs[r * PITCH + col] = v;
       }
     }
+    {  // this wave's packed rows (gi, k) for columns c0 .. c0+31
+      const int col = lane & (kCB - 1);
+      const int64_t c = c0 + col;
+      const int nrow = GPW * K;
+      for (int rr = lane >> 5; rr < nrow; rr += 2) {
+        const int gi = rr / K;
+        const int k = rr - gi * K;
+        const int64_t g = g0 + gi;
+        float v = 0.0f;
+        uint8_t ix = 0xff;  // no row: never matches
+        if (g < ngroups && c < C) {
+          const int64_t off = (g * K + k) * C + c;
+          v = io<VT>::load(vals, off);
+          ix = idx[off];
+        }
+        pv[wave][rr][col] = v;
+        pi[wave][rr][col] = ix;
+      }
+    }
     __syncthreads();
 
     const int cmax = static_cast<int>(C - c0 < kCB ? C - c0 : kCB);
+    if (K == G) {
+      // every row of a group is kept and the kept rows are stored in
+      // ascending order, so slot k targets row k: no dispatch needed
+      for (int cc = 0; cc < cmax; ++cc) {
+        float x[R];
+#pragma unroll
+        for (int i = 0; i < R; ++i) x[i] = xs[(lane + 64 * i) * PITCH + cc];
+#pragma unroll
+        for (int gi = 0; gi < GPW; ++gi) {
+#pragma unroll
+          for (int k = 0; k < G; ++k) {
+            const float v = uniform_f(pv[wave][gi * G + k][cc]);
+#pragma unroll
+            for (int i = 0; i < R; ++i) acc[gi][k][i] = __builtin_fmaf(v, x[i], acc[gi][k][i]);
+          }
+        }
+      }
+    } else {
 #pragma unroll 2
-    for (int cc = 0; cc < cmax; ++cc) {
-      float x[R];
+      for (int cc = 0; cc < cmax; ++cc) {
+        float x[R];
 #pragma unroll
-      for (int i = 0; i < R; ++i) x[i] = xs[(lane + 64 * i) * PITCH + cc];
-      const int64_t c = c0 + cc;
+        for (int i = 0; i < R; ++i) x[i] = xs[(lane + 64 * i) * PITCH + cc];
 #pragma unroll
-      for (int gi = 0; gi < GPW; ++gi) {
-        const int64_t g = g0 + gi;
-        if (g >= ngroups) break;
-        for (int k = 0; k < K; ++k) {
-          const int64_t off = (g * K + k) * C + c;
-          const int r = uniform_i(idx[off]);
-          const float v = uniform_f(io<VT>::load(vals, off));
-          RowDispatch<0, G, G, R>::run(acc[gi], r, v, x);
+        for (int gi = 0; gi < GPW; ++gi) {
+          // slots in batches of 4: the LDS reads of a batch are issued
+          // together, then dispatched (absent slots carry row 0xff)
+          for (int k0 = 0; k0 < K; k0 += 4) {
+            int r[4];
+            float v[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const int k = k0 + j < K ? k0 + j : K - 1;
+              r[j] = k0 + j < K ? uniform_i(pi[wave][gi * K + k][cc]) : 0xff;
+              v[j] = uniform_f(pv[wave][gi * K + k][cc]);
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+              if (r[j] < G) RowDispatch<0, G, G, R>::run(acc[gi], r[j], v[j], x);
+          }
         }
       }
     }

@@ -59,6 +59,8 @@ constexpr int kLdsMax = 160 * 1024;
 constexpr int kDmaMax = 20;        // patch DMA instructions per loader thread per chunk
 constexpr int kDmaEarly = 2;       // of those, issued before the expanders' loads are queued
 constexpr int kRowMax = 8;         // packed-row segments per expander thread per expansion
+constexpr int kUnitMax = 4;        // ring: staged scatter units per expander thread
+constexpr int kPkMax = 4;          // ring: staging DMA instructions (value, index) per loader thread
 constexpr int kStPitch = kBN * 4 + 16;   // epilogue staging: bytes per pixel row (padded)
 constexpr uint32_t kOOB = 0x80000000u;   // buffer offset that reads as zero / drops a store
 constexpr int kRsrcWord3 = 0x00020000;   // raw buffer descriptor word 3 (gfx9 family)
@@ -99,8 +101,8 @@ struct Params {
   int32_t lg_cpp;       // log2(cinb / 8): 16-byte data chunks per patch pixel
   int32_t lg_ksteps;    // log2(cinb / 32)
   int32_t nchunks, taps;
-  int32_t wres;         // 1: one weight tile holds every chunk (expanded once); 0: ring of two
-  int32_t nwb;          // weight tiles in LDS (1, or 2 for the ring)
+  int32_t wres;         // 1: one weight tile holds every chunk (expanded once); 0: ring of three
+  int32_t nwb;          // weight tiles in LDS (1, or 3 for the ring)
   int32_t npb;          // patch buffers in LDS (ring; chunk j uses buffer j % npb)
   int32_t patch_cols;   // rect: staged input columns
   int32_t patch_pix;    // staged pixels per chunk
@@ -108,8 +110,14 @@ struct Params {
   int32_t b_pitch;      // bf16 elements per weight-tile row
   int32_t w_bytes;      // bytes of one weight tile (WO*64 rows)
   int32_t p_bytes;      // bytes of one patch buffer
+  int32_t s_bytes;      // ring: bytes of one packed-row staging buffer (0: resident)
+  int32_t s_vslots;     // ring: 16-byte value slots of one staging buffer (the index slots follow
+                        // at a 1 KiB boundary, s_vblk64 * 64 slots in)
+  int32_t s_islots;     // ring: 16-byte index slots
+  int32_t s_vblk64;     // ring: value slots rounded up to 64
   int32_t ncols8;       // 8-column blocks of one expansion (whole tile or one chunk)
   int32_t nu;           // expansion units (group x 8-column block) per expander thread
+  int32_t nus;          // ring: staged scatter units (packed row x 8-column block) per expander thread
   int32_t nrows;        // packed rows of one output super-block
   int32_t mt;           // 16-pixel tiles per wave (compile-time instantiation)
   uint32_t kw_mul;      // tap / KW == (tap * kw_mul) >> 20 for tap < 4096
@@ -117,6 +125,7 @@ struct Params {
   // rect: dq pixels = dpr patch rows + diw patch columns
   int32_t dq, dc, dpr, diw;
   FastDiv fd_nob, fd_rparts, fd_wo, fd_pcols, fd_pps, fd_k, fd_ncols8, fd_tc, fd_howo;
+  FastDiv fd_taps, fd_v8, fd_v16;  // ring staging: taps, cinb/8, cinb/16
 };
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(u32x4_t v) { return __builtin_bit_cast(bf16x8_t, v); }
@@ -186,6 +195,7 @@ __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
   // groups that exist (the last super-block may be partial)
   const int glim = p.O / p.G - ob * gpb < gpb ? p.O / p.G - ob * gpb : gpb;
   const int nslots = p.nu * p.K;
+  const uint32_t gmask = static_cast<uint32_t>(p.G - 1);
   struct Packed {
     u32x4_t v[kRowMax];
     u32x2_t ix[kRowMax];
@@ -227,9 +237,11 @@ __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
         }
 #pragma unroll
         for (int jj = 0; jj < 8; ++jj) {
-          const uint32_t row = (P.ix[i][jj >> 2] >> (8 * (jj & 3))) & 0xffu;  // idx: row in the group
+          // idx: row in the group (< G, a power of two on this path; the
+          // mask keeps a corrupt index inside its own group)
+          const uint32_t row = (P.ix[i][jj >> 2] >> (8 * (jj & 3))) & gmask;
           const uint16_t w = static_cast<uint16_t>(P.v[i][jj >> 1] >> (16 * (jj & 1)));
-          if (row < static_cast<uint32_t>(p.G)) dst[row * p.b_pitch + jj] = w;
+          dst[row * p.b_pitch + jj] = w;
         }
       }
     }
@@ -423,48 +435,155 @@ __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
     }
   };
 
+  // ---- ring mode: packed rows staged in LDS by the loaders ----------------
+  // Chunk j's packed rows (value segments, then index segments, each 16-byte
+  // slot-linear: [row][tap][channel]) are DMA'd two chunks ahead into one of
+  // two staging buffers; the expanders build chunk j's tile from there while
+  // chunk j-1 is multiplied.
+  const int32_t sofs = wofs_patch + p.npb * p.p_bytes;  // LDS offset of staging buffer 0
+  // loader thread rt's staging slots: value slot rt + 256 i and index slot
+  // rt + 256 i, element offsets at chunk 0 (kOOB: none)
+  uint32_t pk_v[kPkMax], pk_i[kPkMax];
+  if (loader && !p.wres) {
+    const int32_t rowbase = ob * gpb * p.K;
+    const int32_t rlim = glim * p.K;
+#pragma unroll
+    for (int i = 0; i < kPkMax; ++i) {
+      const int32_t sl = rt + kRoleThreads * i;
+      {
+        const int32_t r = static_cast<int32_t>(fdiv(static_cast<uint32_t>(sl), p.fd_v8));  // (row, tap) pair
+        const int32_t j = sl - r * cpp;
+        const int32_t row = static_cast<int32_t>(fdiv(static_cast<uint32_t>(r), p.fd_taps));
+        const int32_t tap = r - row * p.taps;
+        pk_v[i] = sl < p.s_vslots && row < rlim
+                      ? static_cast<uint32_t>((rowbase + row) * p.C + tap * p.Cin + 8 * j) : kOOB;
+      }
+      {
+        const int32_t r = static_cast<int32_t>(fdiv(static_cast<uint32_t>(sl), p.fd_v16));  // (row, tap) pair
+        const int32_t j = sl - r * (cpp >> 1);
+        const int32_t row = static_cast<int32_t>(fdiv(static_cast<uint32_t>(r), p.fd_taps));
+        const int32_t tap = r - row * p.taps;
+        pk_i[i] = sl < p.s_islots && row < rlim
+                      ? static_cast<uint32_t>((rowbase + row) * p.C + tap * p.Cin + 16 * j) : kOOB;
+      }
+    }
+  }
+  const int npv = p.s_vslots > wave * 64 ? (p.s_vslots - wave * 64 + kRoleThreads - 1) / kRoleThreads : 0;
+  const int npi = p.s_islots > wave * 64 ? (p.s_islots - wave * 64 + kRoleThreads - 1) / kRoleThreads : 0;
+  auto issue_packed = [&](int ch, int sb) {
+    const uint32_t stg = static_cast<uint32_t>(sofs + sb * p.s_bytes);
+    const uint32_t istg = stg + static_cast<uint32_t>(p.s_vblk64) * 16u;
+    const uint32_t add = static_cast<uint32_t>(ch * p.cinb);
+#pragma unroll
+    for (int i = 0; i < kPkMax; ++i) {
+      if (i < npv)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_void_t*)(lds + stg + (wave + kLoadWaves * i) * 1024), 16,
+                                                 pk_v[i] == kOOB ? kOOB : (pk_v[i] + add) * 2u, 0, 0, 0);
+      if (i < npi)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(ir, (lds_void_t*)(lds + istg + (wave + kLoadWaves * i) * 1024), 16,
+                                                 pk_i[i] == kOOB ? kOOB : pk_i[i] + add, 0, 0, 0);
+    }
+  };
+  // Scatter one chunk's staged packed rows into weight tile wb, which was
+  // zero-filled a chunk earlier.  Unit = (packed row, 8-column block), so the
+  // work spreads over K times more threads than whole groups would.  With
+  // K == G every row is kept in ascending order: a row is copied whole.
+  // per-thread scatter units of the staged path, decoded once:
+  // staged byte offset of the unit's value segment, tile element offset
+  int32_t su_src[kUnitMax], su_dst[kUnitMax];
+  if (!loader && !p.wres) {
+    const int rowpitch = 8 * p.ncols8;  // staged elements per packed row
+    const int rlim = glim * p.K;
+#pragma unroll
+    for (int j = 0; j < kUnitMax; ++j) {
+      const int u = rt + kRoleThreads * j;
+      const int r = static_cast<int>(fdiv(u, p.fd_ncols8));
+      const int col8 = u - r * p.ncols8;
+      const int gl = static_cast<int>(fdiv(r, p.fd_k));
+      const bool ok = j < p.nus && r < rlim;
+      su_src[j] = ok ? (r * rowpitch + 8 * col8) : -1;
+      su_dst[j] = gl * p.G * p.b_pitch + 8 * col8 + (p.K == p.G ? (r - gl * p.K) * p.b_pitch : 0);
+    }
+  }
+  auto scatter_staged = [&](int wb, int sb) {
+    const uint8_t* stg = lds + sofs + sb * p.s_bytes;
+    uint16_t* bs = reinterpret_cast<uint16_t*>(lds + wb * p.w_bytes);
+#pragma unroll
+    for (int j = 0; j < kUnitMax; ++j) {
+      if (su_src[j] < 0) continue;
+      uint16_t* dst = bs + su_dst[j];
+      const u32x4_t v = *reinterpret_cast<const u32x4_t*>(stg + su_src[j] * 2);
+      if (p.K == p.G) {  // every row kept, in order: the row is copied whole
+        *reinterpret_cast<u32x4_t*>(dst) = v;
+        continue;
+      }
+      const u32x2_t ix = *reinterpret_cast<const u32x2_t*>(stg + p.s_vblk64 * 16 + su_src[j]);
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) {
+        const uint32_t rr = (ix[jj >> 2] >> (8 * (jj & 3))) & gmask;  // idx: row in the group
+        const uint16_t w = static_cast<uint16_t>(v[jj >> 1] >> (16 * (jj & 1)));
+        dst[rr * p.b_pitch + jj] = w;
+      }
+    }
+  };
+  // zero fill of weight tile wb by the loaders (not needed when K == G)
+  auto zero_tile = [&](int wb) {
+    if (p.K == p.G) return;
+    u32x4_t* b4 = reinterpret_cast<u32x4_t*>(lds + wb * p.w_bytes);
+    const int n16 = p.w_bytes / 16;
+    for (int e = rt; e < n16; e += kRoleThreads) b4[e] = u32x4_t{0u, 0u, 0u, 0u};
+  };
+
   // ---- chunk pipeline -----------------------------------------------------
   // Loaders stream patches through npb (1 or 2) buffers: chunk 0 from the
   // first instructions, chunk j+1 during chunk j's MFMAs.  Expanders build
-  // the weight tile, once (resident) or per chunk through a ring of two
-  // tiles; a loader's MFMAs fill the SIMD its partner expander shares while
-  // that one builds.  One call site for compute() keeps the accumulators in
-  // place.
+  // the weight tile: once (resident), or (ring) chunk 0 from registers and
+  // chunk j+1 from its staged packed rows while chunk j is multiplied, into
+  // the other of two tiles.  A loader's MFMAs fill the SIMD its partner
+  // expander shares while that one builds.  One barrier per chunk; one call
+  // site for compute() keeps the accumulators in place.
   // The packed-row loads go into the memory queue ahead of the bulk of the
   // patch DMA, which would otherwise hold them up.
   lds_barrier();
+  const bool ring = !p.wres;
   if (loader) {
 #pragma unroll
     for (int i = kDmaEarly; i < kDmaMax; ++i)
       if (i < nd) dma(static_cast<uint32_t>(wofs_patch), i, doff[i]);
-    wait_vm<0>();  // chunk 0 landed (this wave's part)
+    if (ring && p.nchunks > 1) {
+      issue_packed(1, 1);
+      zero_tile(1);
+    }
+    wait_vm<0>();  // chunk 0 (and chunk 1's packed rows) landed
   } else {
     expand(0, 0, true);
-    if (!p.wres && p.nchunks > 1) {
-      expand(1, 1, false);
-      if (p.nchunks > 2) load_slots(2, 0);
-    }
   }
   lds_barrier();
   int pb = 0;
   for (int ch = 0; ch < p.nchunks; ++ch) {
-    const uint32_t wofs = p.wres ? static_cast<uint32_t>(ch * p.taps * p.cinb * 2) : static_cast<uint32_t>((ch & 1) * p.w_bytes);
+    const int wcur = ch % 3;  // ring tile of chunk ch
+    const uint32_t wofs = p.wres ? static_cast<uint32_t>(ch * p.taps * p.cinb * 2) : static_cast<uint32_t>(wcur * p.w_bytes);
     const int nb = p.npb == 2 ? pb ^ 1 : 0;
+    if (ring && ch + 1 < p.nchunks) {
+      const int wnext = wcur == 2 ? 0 : wcur + 1;
+      if (loader) {
+        if (ch + 2 < p.nchunks) {
+          issue_packed(ch + 2, ch & 1);
+          zero_tile(wnext == 2 ? 0 : wnext + 1);  // the tile of chunk ch+2 (last read by chunk ch-1)
+        }
+      } else {
+        scatter_staged(wnext, (ch + 1) & 1);
+      }
+    }
     // with two patch buffers the next chunk streams in during this one
     const int dch = p.npb == 2 && ch + 1 < p.nchunks ? ch + 1 : -1;
     compute(wofs, static_cast<uint32_t>(wofs_patch + pb * p.p_bytes), dch, static_cast<uint32_t>(wofs_patch + nb * p.p_bytes));
     if (ch + 1 < p.nchunks) {
-      const bool refill_w = !p.wres && ch + 2 < p.nchunks;
-      if (refill_w || p.npb == 1) {
-        lds_barrier();  // every wave is done with chunk ch's buffers
-        if (loader) {
-          if (p.npb == 1) issue_patch(ch + 1, static_cast<uint32_t>(wofs_patch));
-        } else if (refill_w) {
-          expand(ch + 2, ch & 1, true);
-          if (ch + 3 < p.nchunks) load_slots(ch + 3, 0);
-        }
+      if (p.npb == 1) {
+        lds_barrier();  // every wave is done with the patch buffer
+        if (loader) issue_patch(ch + 1, static_cast<uint32_t>(wofs_patch));
       }
-      if (loader) wait_vm<0>();  // chunk ch+1 landed
+      if (loader) wait_vm<0>();  // chunk ch+1's patch (and chunk ch+2's packed rows) landed
       lds_barrier();
       pb = nb;
     }
@@ -601,13 +720,28 @@ bool layout(Params& pl, int32_t cinb, int32_t Cin, int32_t wres, int32_t npb, in
   pl.w_bytes = pl.WO * kBN * pl.b_pitch * 2;
   pl.nrows = (pl.WO * kBN / G) * K;
   pl.nu = ((pl.WO * kBN / G) * pl.ncols8 + kRoleThreads - 1) / kRoleThreads;
+  pl.nus = (pl.nrows * pl.ncols8 + kRoleThreads - 1) / kRoleThreads;
+  if (!wres && pl.nus > kUnitMax) return false;
   if (pl.nu * K > 4 * kRowMax) return false;  // at most four load rounds per expansion
-  pl.nwb = wres ? 1 : 2;
+  pl.nwb = wres ? 1 : 3;
   // the DMA writes whole 64-slot (1 KiB) blocks: round the patch up so the
   // tail of its last block stays inside its buffer
   pl.p_bytes = static_cast<int32_t>((slots * 16 + 1023) / 1024 * 1024);
   pl.npb = npb;
-  if (static_cast<int64_t>(pl.nwb) * pl.w_bytes + static_cast<int64_t>(npb) * pl.p_bytes > kLdsMax) return false;
+  pl.s_bytes = pl.s_vslots = pl.s_islots = pl.s_vblk64 = 0;
+  if (!wres) {  // packed-row staging: nrows x taps x (cinb/8 value + cinb/16 index) slots
+    pl.s_vslots = pl.nrows * pl.taps * (cinb / 8);
+    pl.s_islots = pl.nrows * pl.taps * (cinb / 16);
+    pl.s_vblk64 = (pl.s_vslots + 63) / 64 * 64;
+    pl.s_bytes = (pl.s_vblk64 + (pl.s_islots + 63) / 64 * 64) * 16;
+    if (pl.s_vslots > kPkMax * kRoleThreads || pl.s_islots > kPkMax * kRoleThreads) return false;
+  }
+  if (static_cast<int64_t>(pl.nwb) * pl.w_bytes + static_cast<int64_t>(npb) * pl.p_bytes +
+          2 * static_cast<int64_t>(pl.s_bytes) > kLdsMax)
+    return false;
+  pl.fd_taps = make_fastdiv(pl.taps);
+  pl.fd_v8 = make_fastdiv(cinb / 8);
+  pl.fd_v16 = make_fastdiv(cinb / 16);
   pl.dq = kRoleThreads / pps;
   pl.dc = kRoleThreads % pps;
   // rect: dq pixels = dpr patch rows + diw patch columns; rows: diw = dq pixels
@@ -641,7 +775,8 @@ double model_cycles(const Params& t, double mfma_chunk, double store, int K) {
       arrive = (issue > arrive ? issue : arrive) + load;
     }
     double ready_w = e_first;
-    if (!t.wres && c >= 2) ready_w = done2 + barrier + build;
+    // ring: chunk c is scattered during chunk c-1's MFMAs by the expander half
+    if (!t.wres && c >= 1) ready_w = (c >= 2 ? done2 : e_first) + barrier + t.nus * 8.0 * 16.0;
     double st = c == 0 ? 0.0 : done + barrier;
     st = st > arrive ? st : arrive;
     st = st > ready_w ? st : ready_w;
@@ -785,7 +920,8 @@ hipError_t launch_yrm(const Params& p, uint32_t grid, hipStream_t s) {
       reinterpret_cast<const void*>(&dense_tile_kernel<YT, RECT, MT>), hipFuncAttributeMaxDynamicSharedMemorySize,
       kLdsMax);
   if (attr != hipSuccess) return attr;
-  size_t lds = static_cast<size_t>(p.nwb) * p.w_bytes + static_cast<size_t>(p.npb) * p.p_bytes;
+  size_t lds = static_cast<size_t>(p.nwb) * p.w_bytes + static_cast<size_t>(p.npb) * p.p_bytes +
+               2 * static_cast<size_t>(p.s_bytes);
   const size_t staging = static_cast<size_t>(kWaves) * MT * 16 * kStPitch;  // epilogue reuses the LDS
   if (lds < staging) lds = staging;
   hipLaunchKernelGGL((dense_tile_kernel<YT, RECT, MT>), dim3(grid), dim3(kThreads), lds, s, p);

@@ -69,10 +69,10 @@ constexpr int kRsrcWord3 = 0x00020000;   // raw buffer descriptor word 3 (gfx9 f
 // with m = floor(2^32 / d) + 1, exact for n * d < 2^32.  d == 1 has m = 0 and
 // an all-ones `one` mask that passes n through, so there is no branch.
 struct FastDiv {
-  uint32_t d, m, one;
+  uint32_t m, one;
 };
 __host__ __device__ inline FastDiv make_fastdiv(uint32_t d) {
-  return FastDiv{d, d > 1 ? static_cast<uint32_t>((uint64_t(1) << 32) / d + 1) : 0u, d > 1 ? 0u : ~0u};
+  return FastDiv{d > 1 ? static_cast<uint32_t>((uint64_t(1) << 32) / d + 1) : 0u, d > 1 ? 0u : ~0u};
 }
 __device__ __forceinline__ uint32_t fdiv(uint32_t n, FastDiv f) { return __umulhi(n, f.m) + (n & f.one); }
 
@@ -526,12 +526,15 @@ __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
       }
     }
   };
-  // zero fill of weight tile wb by the loaders (not needed when K == G)
+  // zero fill of weight tile wb by the loaders (not needed when K == G): DMA
+  // with an out-of-range source offset writes zeros into LDS without reading
+  // memory, so a loader never waits on the LDS queue for it (a tile is a
+  // whole number of KiB)
   auto zero_tile = [&](int wb) {
     if (p.K == p.G) return;
-    u32x4_t* b4 = reinterpret_cast<u32x4_t*>(lds + wb * p.w_bytes);
-    const int n16 = p.w_bytes / 16;
-    for (int e = rt; e < n16; e += kRoleThreads) b4[e] = u32x4_t{0u, 0u, 0u, 0u};
+    const int nblk = p.w_bytes / 1024;
+    for (int b = wave; b < nblk; b += kLoadWaves)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void_t*)(lds + wb * p.w_bytes + b * 1024), 16, kOOB, 0, 0, 0);
   };
 
   // ---- chunk pipeline -----------------------------------------------------

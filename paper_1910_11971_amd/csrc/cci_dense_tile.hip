@@ -23,8 +23,9 @@
 //     workgroup's outputs touches, CINB channels) is DMA'd from HBM straight
 //     into LDS with buffer_load...lds; out-of-image pixels read as zero
 //     because their buffer offsets are out of range (this *is* the conv
-//     padding); each pixel's 16-byte chunks are followed by one pad slot so
-//     the MFMA operand reads are bank-conflict free;
+//     padding); the patch is stored in blocks of 16 pixels, chunk-major
+//     inside a block, and the weight tile in MFMA-fragment order, so that
+//     the operand reads are bank-conflict free;
 //   - the expanded weight tile of the chunk is built in LDS while the patch
 //     streams in (the packed rows are loaded into registers first);
 //   - with two buffers, chunk j+1 is in flight while chunk j is multiplied.
@@ -53,12 +54,10 @@ constexpr int kRoleThreads = kLoadWaves * 64;
 constexpr int kBN = 64;            // outputs per wave
 constexpr int kKS = 32;            // reduction columns per MFMA k-step
 constexpr int kMT = 4;             // max 16-pixel tiles per wave
-constexpr int kBPad = 8;           // weight-tile row padding (bf16 elements)
 constexpr int kXcds = 8;
 constexpr int kLdsMax = 160 * 1024;
 constexpr int kDmaMax = 20;        // patch DMA instructions per loader thread per chunk
-constexpr int kDmaEarly = 2;       // of those, issued before the expanders' loads are queued
-constexpr int kRowMax = 8;         // packed-row segments per expander thread per expansion
+constexpr int kDmaEarly = 2;       // of those, issued before the expanders' staging DMAs are queued
 constexpr int kUnitMax = 4;        // ring: staged scatter units per expander thread
 constexpr int kPkMax = 4;          // ring: staging DMA instructions (value, index) per loader thread
 constexpr int kStPitch = kBN * 4 + 16;   // epilogue staging: bytes per pixel row (padded)
@@ -88,6 +87,7 @@ struct Params {
   void* Y;
   uint32_t x_bytes, y_bytes, packed_n;  // buffer extents: bytes, bytes, packed elements
   int32_t N, C, O, G, K, relu;
+  int32_t ngroups;      // O / G
   // convolution geometry; FC runs as a 1x1 convolution over N "pixels"
   int32_t H, W, Cin, KW, sh, sw, ph, pw, Ho, Wo, Bimg;
   int32_t strided;      // rows mode: 1x1 convolution with stride (input pixels are gathered)
@@ -106,8 +106,12 @@ struct Params {
   int32_t npb;          // patch buffers in LDS (ring; chunk j uses buffer j % npb)
   int32_t patch_cols;   // rect: staged input columns
   int32_t patch_pix;    // staged pixels per chunk
-  int32_t slots;        // 16-byte patch slots per chunk (patch_pix * (cpp + 1))
-  int32_t b_pitch;      // bf16 elements per weight-tile row
+  int32_t slots;        // 16-byte patch slots per chunk
+  int32_t pp;           // rect: slot pitch of a patch pixel (cpp + 1, odd)
+  // rect loader walk: 16^-1 mod pp; a step of 256 slots moves dcs chunks
+  // (mod pp) and dqs pixels (16 more when the chunk wraps)
+  int32_t inv16, dcs, dqs;
+  int32_t nkb;          // bytes of one 16-row block of a weight tile (1 KiB per 32-column k-step)
   int32_t w_bytes;      // bytes of one weight tile (WO*64 rows)
   int32_t p_bytes;      // bytes of one patch buffer
   int32_t s_bytes;      // ring: bytes of one packed-row staging buffer (0: resident)
@@ -115,17 +119,20 @@ struct Params {
                         // at a 1 KiB boundary, s_vblk64 * 64 slots in)
   int32_t s_islots;     // ring: 16-byte index slots
   int32_t s_vblk64;     // ring: value slots rounded up to 64
+  int32_t fofs;         // LDS offset of the first tile's packed-row staging
+  int32_t f_vblk64;     // its value slots rounded up to 64 (the index slots follow)
+  int32_t lds_bytes;    // LDS used by the operand pipeline
   int32_t ncols8;       // 8-column blocks of one expansion (whole tile or one chunk)
-  int32_t nu;           // expansion units (group x 8-column block) per expander thread
+  int32_t nu;           // first-tile expansion units per expander lane (bound over the waves)
+  int32_t lg_gpb;       // log2(groups per output super-block)
+  int32_t epg;          // first tile: groups per expander wave (max(1, 16 WO / G))
   int32_t nus;          // ring: staged scatter units (packed row x 8-column block) per expander thread
   int32_t nrows;        // packed rows of one output super-block
   int32_t mt;           // 16-pixel tiles per wave (compile-time instantiation)
   uint32_t kw_mul;      // tap / KW == (tap * kw_mul) >> 20 for tap < 4096
-  // loader slot walk: each step advances 256 slots = dq pixels + dc slots;
-  // rect: dq pixels = dpr patch rows + diw patch columns
-  int32_t dq, dc, dpr, diw;
-  FastDiv fd_nob, fd_rparts, fd_wo, fd_pcols, fd_pps, fd_k, fd_ncols8, fd_tc, fd_howo;
-  FastDiv fd_taps, fd_v8, fd_v16;  // ring staging: taps, cinb/8, cinb/16
+  FastDiv fd_nob, fd_rparts, fd_wo, fd_pcols, fd_k, fd_howo;
+  FastDiv fd_ncols8, fd_nc2, fd_cin8;  // staging: ncols8, ncols8 / 2; Cin / 8
+  FastDiv fd_pp, fd_taps;
 };
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(u32x4_t v) { return __builtin_bit_cast(bf16x8_t, v); }
@@ -142,13 +149,49 @@ __device__ __forceinline__ void wait_vm() {
   static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
-// Patch layout: pixel q occupies cpp + 1 consecutive 16-byte slots (cpp
-// data chunks and one pad slot).  The odd slot pitch spreads 8 consecutive
-// pixels reading the same chunk over all 32 banks, and makes the operand
-// address of any tap a single add.
+// Touch every 64-byte line of the launch arguments with one batch of
+// scalar loads and a single wait.  Arguments reach a wave through the
+// scalar cache, which starts each launch cold; the compiler loads them
+// lazily, as values are needed, so without this each first touch of a line
+// would stall the wave for its own round trip.
+__device__ __forceinline__ void prefetch_args() {
+  static_assert(sizeof(Params) <= 6 * 64, "six lines cover the arguments");
+  const auto ka = __builtin_amdgcn_kernarg_segment_ptr();
+  uint32_t k0, k1, k2, k3, k4, k5;
+  asm volatile(
+      "s_load_dword %0, %6, 0x0\n\ts_load_dword %1, %6, 0x40\n\ts_load_dword %2, %6, 0x80\n\t"
+      "s_load_dword %3, %6, 0xc0\n\ts_load_dword %4, %6, 0x100\n\ts_load_dword %5, %6, 0x140\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=s"(k0), "=s"(k1), "=s"(k2), "=s"(k3), "=s"(k4), "=s"(k5)
+      : "s"(ka)
+      : "memory");
+}
+
+// LDS layouts.  A wave's 16-byte LDS read runs without bank conflicts when,
+// in each half of the wave, the 32 addresses fall into distinct 16-byte
+// slots modulo 512 bytes (measured on gfx950; a row pitch of an odd number
+// of slots is not enough).  An MFMA operand fragment is read by lanes
+// (row = lane % 16, k-chunk = lane / 16), so:
+//   - weight tile: element (o, k) at byte
+//       ((o / 16) * NK + k / 32) * 1024 + (k / 8 % 4) * 256 + (o % 16) * 16 + (k % 8) * 2
+//     (NK = 32-column k-steps of the tile): a fragment is 1 KiB, lane l reads
+//     bytes 16 l .. 16 l + 15;
+//   - rows-mode patch (FC, 1x1): pixel q, 16-byte channel chunk c at slot
+//       ((q / 16) * cpp + c) * 16 + q % 16
+//     (cpp = chunks per pixel, even): a tile's 16 pixels of one chunk are
+//     256 contiguous bytes;
+//   - rect-mode patch (k x k): slot (cpp + 1) q + 16 c.  The address is
+//     linear in the pixel, so every tap reads at a uniform offset from the
+//     tap-(0,0) address; with an odd pixel pitch and chunks 16 slots apart
+//     the 16 pixels x 2 chunks of a half-wave land in distinct slots
+//     modulo 512 bytes (only tiles that straddle an output row can see a
+//     two-way conflict).  A DMA instruction still fetches runs of a few
+//     neighbouring pixels (its rate falls with the number of distinct
+//     cache lines it touches); one slot in cpp + 1 is a hole.
 template <typename YT, bool RECT, int MT>
 __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  prefetch_args();
   constexpr uint32_t ysz = sizeof(YT);
 
   // ---- workgroup -> (pixel partition, output super-block), XCD-aware ----
@@ -176,93 +219,146 @@ __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
   const bool loader = wave < kLoadWaves;  // wave-uniform role
   const int rt = threadIdx.x - (loader ? 0 : kRoleThreads);  // thread index within the role
   const int cpp = 1 << p.lg_cpp;
-  const int pps = cpp + 1;
   const int32_t wofs_patch = p.nwb * p.w_bytes;  // LDS offset of patch buffer 0
+  // weight-tile byte offsets of row o and of 8-column block col8 (they add)
+  auto rowaddr = [&](int o) { return (o >> 4) * p.nkb + (o & 15) * 16; };
+  auto coladdr = [](int col8) { return (col8 >> 2) * 1024 + (col8 & 3) * 256; };
+  const int32_t nkbm = p.nkb - 256;  // rowaddr(r) == 16 r + (r >> 4) * nkbm
 
-  // ---- expanders: weight-tile build -----------------------------------------
-  // Unit u = (group gl, 8-column block col8) of one expansion (the whole tile,
-  // or one chunk): its G tile rows x 8 columns are zero-filled and receive
-  // the 8 columns of the group's K packed rows, all by one thread (program
-  // order is the only synchronisation).  Thread rt owns units rt + 256 j
-  // (j < nu); its packed-row segments ("slots", unit-major, K per unit) are
-  // loaded kRowMax at a time.  The tile column of col8 is 8 * col8, its
-  // source column tap * Cin + (chunk) * cinb + 8 * c8.
+  // ---- expanders: first weight tile ---------------------------------------
+  // Packed rows are staged in LDS row-major: value slot r * ncols8 + j holds
+  // the 8 values of packed row r in column block j of the expansion, index
+  // slot r * ncols8 / 2 + j / 2 the 16 indices of blocks j and j + 1 (ncols8
+  // is even).  The ring stages one chunk in tile order (block j is tile
+  // column block j); the first tile is staged in memory order (block j is
+  // source columns 8 j .. 8 j + 7), so each packed row is one contiguous
+  // copy.
+  // The resident tile (every chunk), or the ring's chunk-0 tile, is built by
+  // the four expander waves from a staging area at fofs.  Expander wave e
+  // owns groups [e * epg, (e + 1) * epg) -- tile rows [16 WO e, 16 WO (e + 1))
+  // when G <= 16 WO, else one group (waves past the last group idle) --
+  // i.e. whole groups and a contiguous run of packed rows: it DMAs those
+  // rows, zero-fills its rows' fragments, then writes every kept weight of
+  // them; program order alone puts its zero fill before its writes, and no
+  // other wave touches them.
+  // Rolled loops keep this code short: it runs once per workgroup, from a
+  // cold instruction cache.
   const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(p.vals), (short)0, static_cast<int>(p.packed_n * 2u), kRsrcWord3);
   const __amdgpu_buffer_rsrc_t ir = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(p.idx), (short)0, static_cast<int>(p.packed_n), kRsrcWord3);
-  const int gpb = (p.WO * kBN) / p.G;
+  const int gpb = 1 << p.lg_gpb;  // groups per output super-block
   // groups that exist (the last super-block may be partial)
-  const int glim = p.O / p.G - ob * gpb < gpb ? p.O / p.G - ob * gpb : gpb;
-  const int nslots = p.nu * p.K;
+  const int glim = p.ngroups - ob * gpb < gpb ? p.ngroups - ob * gpb : gpb;
+  const int rlim = glim * p.K;               // packed rows that exist
+  const int32_t rowbase = ob * gpb * p.K;    // first packed row of the super-block
   const uint32_t gmask = static_cast<uint32_t>(p.G - 1);
-  struct Packed {
-    u32x4_t v[kRowMax];
-    u32x2_t ix[kRowMax];
-    int32_t dst[kRowMax];  // tile element offset of the unit's first row (< 0: none); bit 30: first slot
+  const int ewave = wave - kLoadWaves;       // expander index (negative on loaders)
+  // packed rows of this expander wave (none on waves past the last group)
+  const int erows = ewave * p.epg < gpb ? p.epg * p.K : 0;
+  const int er0 = ewave * p.epg * p.K;       // its first packed row
+  // tile column block of first-tile staged block j (memory order)
+  auto first_col8 = [&](int j) {
+    const int tap = static_cast<int>(fdiv(j, p.fd_cin8));
+    const int cin8 = j - tap * (p.Cin >> 3);
+    return ((cin8 >> p.lg_cpp) * p.taps + tap) * cpp + (cin8 & (cpp - 1));
   };
-  constexpr int32_t kFirst = 1 << 30;
-  Packed P;
-  // load slots s0 .. s0+kRowMax-1 of the expansion of chunk ch
-  auto load_slots = [&](int ch, int s0) {
+  // write staged packed-row segment (row r, tile column block col8) into the
+  // tile at tb: every kept weight goes to row G*g + idx (Alg. 1's target
+  // row); with K == G every row is kept in ascending order and the segment
+  // is copied whole.  sv / si: byte offsets of its value and index slots.
+  auto scatter_unit = [&](uint8_t* tb, const uint8_t* stg, int sv, int si, int col8, int r) {
+    const int gl = static_cast<int>(fdiv(r, p.fd_k));
+    uint8_t* dst = tb + rowaddr(gl * p.G) + coladdr(col8);
+    const u32x4_t v = *reinterpret_cast<const u32x4_t*>(stg + sv);
+    if (p.K == p.G) {
+      *reinterpret_cast<u32x4_t*>(dst + rowaddr(r - gl * p.K)) = v;
+      return;
+    }
+    const u32x2_t ix = *reinterpret_cast<const u32x2_t*>(stg + si);
 #pragma unroll
-    for (int i = 0; i < kRowMax; ++i) {
-      const int sl = s0 + i;
-      const int j = static_cast<int>(fdiv(sl, p.fd_k));
-      const int k = sl - j * p.K;
-      const int u = rt + kRoleThreads * j;
-      const int gl = static_cast<int>(fdiv(u, p.fd_ncols8));
-      const int col8 = u - gl * p.ncols8;
-      const bool ok = sl < nslots && gl < glim;
-      const int chl = static_cast<int>(fdiv(col8, p.fd_tc));
-      const int rem = col8 - chl * (p.taps << p.lg_cpp);
-      const uint32_t e = static_cast<uint32_t>(((ob * gpb + gl) * p.K + k) * p.C + (rem >> p.lg_cpp) * p.Cin +
-                                               (chl + ch) * p.cinb + 8 * (rem & (cpp - 1)));
-      P.v[i] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(vr, ok ? e * 2u : kOOB, 0, 0));
-      P.ix[i] = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(ir, ok ? e : kOOB, 0, 0));
-      P.dst[i] = ok ? (gl * p.G * p.b_pitch + 8 * col8) | (k == 0 ? kFirst : 0) : -1;
+    for (int jj = 0; jj < 8; ++jj) {
+      // idx: row in the group (< G, a power of two on this path; the mask
+      // keeps a corrupt index inside its own group)
+      const int32_t rr = static_cast<int32_t>((ix[jj >> 2] >> (8 * (jj & 3))) & gmask);
+      const uint16_t w = static_cast<uint16_t>(v[jj >> 1] >> (16 * (jj & 1)));
+      *reinterpret_cast<uint16_t*>(dst + (rr << 4) + (rr >> 4) * nkbm + 2 * jj) = w;
     }
   };
-  // write the loaded slots into weight tile wb: a unit's first slot zero-fills
-  // its G rows; every kept weight goes to row G*g + idx (Alg. 1's target row)
-  auto scatter_slots = [&](int wb) {
-    uint16_t* bs = reinterpret_cast<uint16_t*>(lds + wb * p.w_bytes);
-#pragma unroll
-    for (int i = 0; i < kRowMax; ++i) {
-      if (P.dst[i] >= 0) {
-        uint16_t* dst = bs + (P.dst[i] & (kFirst - 1));
-        if (P.dst[i] & kFirst) {
-          for (int r = 0; r < p.G; ++r)
-            *reinterpret_cast<u32x4_t*>(dst + r * p.b_pitch) = u32x4_t{0u, 0u, 0u, 0u};
-        }
-#pragma unroll
-        for (int jj = 0; jj < 8; ++jj) {
-          // idx: row in the group (< G, a power of two on this path; the
-          // mask keeps a corrupt index inside its own group)
-          const uint32_t row = (P.ix[i][jj >> 2] >> (8 * (jj & 3))) & gmask;
-          const uint16_t w = static_cast<uint16_t>(P.v[i][jj >> 1] >> (16 * (jj & 1)));
-          dst[row * p.b_pitch + jj] = w;
-        }
-      }
+  // source element of staged block j of packed row r, chunk ch (ring: tile
+  // order; the resident first tile uses memory order, see stage_first)
+  auto ring_src = [&](int r, int j, int ch) -> uint32_t {
+    return __umul24(rowbase + r, p.C) + __umul24(j >> p.lg_cpp, p.Cin) + ch * p.cinb + 8 * (j & (cpp - 1));
+  };
+  // this wave's staging DMAs (lanes past the end of its range stay idle).
+  // Resident: its packed rows are one contiguous run of memory, copied as
+  // is; ring: the chunk-0 columns of each row.
+  auto stage_first = [&]() {
+    const int nv = erows * p.ncols8;
+    const int32_t rows_ok = rlim - er0;  // rows of this wave that exist
+    uint8_t* const vdst = lds + p.fofs + er0 * p.ncols8 * 16;
+    uint8_t* const idst = lds + p.fofs + (p.f_vblk64 + (er0 * p.ncols8 >> 1)) * 16;
+    if (p.wres) {  // one contiguous run: byte offsets step by 16 per slot
+      const int nok = rows_ok * p.ncols8;  // value slots of rows that exist
+      const uint32_t v0 = static_cast<uint32_t>(__umul24(rowbase + er0, p.C)) * 2u + 16u * lane;
+      const uint32_t i0 = static_cast<uint32_t>(__umul24(rowbase + er0, p.C)) + 16u * lane;
+#pragma unroll 1
+      for (int b = 0; b < nv; b += 64)
+        if (b + lane < nv)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_void_t*)(vdst + b * 16), 16,
+                                                   b + lane < nok ? v0 + 16u * b : kOOB, 0, 0, 0);
+#pragma unroll 1
+      for (int b = 0; b < (nv >> 1); b += 64)
+        if (b + lane < (nv >> 1))
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(ir, (lds_void_t*)(idst + b * 16), 16,
+                                                   b + lane < (nok >> 1) ? i0 + 16u * b : kOOB, 0, 0, 0);
+      return;
+    }
+#pragma unroll 1
+    for (int b = 0; b < nv; b += 64) {
+      const int sl = b + lane;
+      const int rl = static_cast<int>(fdiv(sl, p.fd_ncols8));
+      const uint32_t off = rl < rows_ok ? ring_src(er0 + rl, sl - rl * p.ncols8, 0) * 2u : kOOB;
+      if (sl < nv) __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_void_t*)(vdst + b * 16), 16, off, 0, 0, 0);
+    }
+#pragma unroll 1
+    for (int b = 0; b < (nv >> 1); b += 64) {
+      const int sl = b + lane;
+      const int rl = static_cast<int>(fdiv(sl, p.fd_nc2));
+      const uint32_t off = rl < rows_ok ? ring_src(er0 + rl, 2 * (sl - rl * (p.ncols8 >> 1)), 0) : kOOB;
+      if (sl < (nv >> 1)) __builtin_amdgcn_raw_ptr_buffer_load_lds(ir, (lds_void_t*)(idst + b * 16), 16, off, 0, 0, 0);
     }
   };
-  // whole expansion of chunk ch into tile wb; the first kRowMax slots may
-  // already be loaded (prefetched)
-  auto expand = [&](int ch, int wb, bool prefetched) {
-    for (int s0 = 0; s0 < nslots; s0 += kRowMax) {
-      if (s0 > 0 || !prefetched) load_slots(ch, s0);
-      scatter_slots(wb);
+  // zero fill of this wave's tile rows (not needed when K == G: every
+  // element is written), then the scatter once its staging DMAs have landed
+  auto expand_first = [&]() {
+    if (p.K != p.G && erows > 0) {
+      // tile rows [e * epg * G, (e + 1) * epg * G): whole 16-row blocks
+      const int z1 = ((ewave + 1) * p.epg * p.G >> 4) * (p.nkb >> 4);
+#pragma unroll 1
+      for (int z = (ewave * p.epg * p.G >> 4) * (p.nkb >> 4) + lane; z < z1; z += 64)
+        *reinterpret_cast<u32x4_t*>(lds + z * 16) = u32x4_t{0u, 0u, 0u, 0u};
+    }
+    wait_vm<0>();
+    const int n = erows * p.ncols8;
+    const int nmax = (rlim - er0) * p.ncols8;  // units of rows that exist
+#pragma unroll 1
+    for (int u = lane; u < n; u += 64) {
+      if (u >= nmax) break;
+      const int rl = static_cast<int>(fdiv(u, p.fd_ncols8)), j = u - rl * p.ncols8;
+      const int sl = er0 * p.ncols8 + u;  // value slot
+      scatter_unit(lds, lds + p.fofs, sl * 16, (p.f_vblk64 + (sl >> 1)) * 16 + (j & 1) * 8,
+                   p.wres ? first_col8(j) : j, er0 + rl);
     }
   };
-  if (!loader) load_slots(0, 0);
+  if (!loader) stage_first();
 
   // ---- loaders: patch DMA -------------------------------------------------
-  // Loader thread rt owns slots rt + 256 i (i < nd); consecutive slots of one
-  // pixel are its 16-byte channel chunks (the last one is the pad slot).  The
-  // offsets of chunk 0 are walked incrementally (the first kDmaEarly DMAs
-  // are issued as soon as their offsets are known, the rest after the
-  // expanders' packed-row loads are queued); chunk j reuses them plus
-  // j*cinb*2.
+  // Loader thread rt owns slots rt + 256 i (i < nd).  Rect mode: slot s
+  // holds chunk s % (cpp + 1) of patch pixel s / (cpp + 1) (the last one is
+  // a pad slot); rows mode: chunk (s / 16) % cpp of pixel
+  // 16 * (s / (16 cpp)) + s % 16.  The source offsets of chunk 0 are
+  // computed once; chunk j reuses them plus j*cinb*2.
   const __amdgpu_buffer_rsrc_t xr =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(p.X), (short)0, static_cast<int>(p.x_bytes), kRsrcWord3);
   const int32_t nd = p.slots > wave * 64 ? (p.slots - wave * 64 + kRoleThreads - 1) / kRoleThreads : 0;
@@ -272,43 +368,40 @@ __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
                                              0, 0, 0);
   };
   if (loader) {
-    const int32_t cin2 = p.Cin * 2;
-    int32_t s = rt;
-    int32_t q = static_cast<int32_t>(fdiv(static_cast<uint32_t>(s), p.fd_pps));
-    int32_t c = s - q * pps;
+    const uint32_t cin2 = static_cast<uint32_t>(p.Cin * 2);
+    // rect: slot s = pp q + 16 c.  The walk state of s = rt + 256 i --
+    // chunk c = s / 16 mod pp and patch pixel q = (s - 16 c) / pp -- steps
+    // by dcs chunks and dqs pixels (16 more when c wraps)
+    int32_t c = 0, q = 0;
+    const int32_t ih0 = oh0 * p.sh - p.ph;
     if constexpr (RECT) {
-      int32_t pr = static_cast<int32_t>(fdiv(static_cast<uint32_t>(q), p.fd_pcols));
-      int32_t iw = q - pr * p.patch_cols;  // patch column
-      const int32_t ih0 = oh0 * p.sh - p.ph;
-      // the pixel index may be negative (padding): then the slot is invalid
-      int32_t off = ((b_img * p.H + ih0 + pr) * p.W + iw - p.pw) * cin2 + 16 * c;
-      const int32_t d_base = (p.dpr * p.W + p.diw) * cin2 + 16 * p.dc;
-      const int32_t d_carry = cin2 - 16 * pps;
-      const int32_t d_wrap = (p.W - p.patch_cols) * cin2;
+      const int32_t t = rt * p.inv16;
+      c = t - static_cast<int32_t>(fdiv(static_cast<uint32_t>(t), p.fd_pp)) * p.pp;
+      q = (rt - 16 * c) / p.pp;  // exact; negative before the first pixel of chunk c
+    }
 #pragma unroll
-      for (int i = 0; i < kDmaMax; ++i) {
-        if (i < nd) {
-          const int32_t ih = ih0 + pr, iwi = iw - p.pw;
-          const bool ok = s < p.slots && c < cpp && static_cast<uint32_t>(ih) < static_cast<uint32_t>(p.H) &&
-                          static_cast<uint32_t>(iwi) < static_cast<uint32_t>(p.W);
-          doff[i] = ok ? static_cast<uint32_t>(off) : kOOB;
-          if (i < kDmaEarly) dma(static_cast<uint32_t>(wofs_patch), i, doff[i]);
-          s += kRoleThreads;
-          c += p.dc;
-          const bool carry = c >= pps;
-          c -= carry ? pps : 0;
-          iw += p.diw + (carry ? 1 : 0);
-          const bool wrap = iw >= p.patch_cols;
-          iw -= wrap ? p.patch_cols : 0;
-          pr += p.dpr + (wrap ? 1 : 0);
-          off += d_base + (carry ? d_carry : 0) + (wrap ? d_wrap : 0);
-        }
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < kDmaMax; ++i) {
-        if (i < nd) {
-          const bool ok = s < p.slots && c < cpp && q < npix;
+    for (int i = 0; i < kDmaMax; ++i) {
+      if (i < nd) {
+        const int32_t s = rt + kRoleThreads * i;
+        bool ok;
+        uint32_t off;
+        if constexpr (RECT) {
+          const int32_t qq = q > 0 ? q : 0;
+          const int32_t pr = static_cast<int32_t>(fdiv(static_cast<uint32_t>(qq), p.fd_pcols));
+          const int32_t ih = ih0 + pr, iw = qq - pr * p.patch_cols - p.pw;
+          // holes (c >= cpp), pixels past the patch and out-of-image pixels
+          // (the padding) read as zero
+          ok = c < cpp && q >= 0 && q < p.patch_pix && static_cast<uint32_t>(ih) < static_cast<uint32_t>(p.H) &&
+               static_cast<uint32_t>(iw) < static_cast<uint32_t>(p.W);
+          off = __umul24(__umul24(b_img * p.H + ih, p.W) + iw, cin2) + 16 * c;
+          c += p.dcs;
+          const bool wrap = c >= p.pp;
+          c -= wrap ? p.pp : 0;
+          q += p.dqs + (wrap ? 16 : 0);
+        } else {
+          const int32_t q = ((s >> (4 + p.lg_cpp)) << 4) | (s & 15);  // patch pixel
+          const int32_t c = (s >> 4) & (cpp - 1);                       // 16-byte chunk
+          ok = s < p.slots && q < npix;
           uint32_t nn = static_cast<uint32_t>(P0 + (q < npix ? q : 0));
           if (p.strided) {  // strided 1x1 (uniform branch): gather the input pixel
             const uint32_t b = fdiv(nn, p.fd_howo);
@@ -316,14 +409,10 @@ __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
             const uint32_t oh = fdiv(rem, p.fd_wo);
             nn = (b * p.H + oh * p.sh) * p.W + (rem - oh * p.Wo) * p.sw;
           }
-          doff[i] = ok ? nn * static_cast<uint32_t>(cin2) + 16u * static_cast<uint32_t>(c) : kOOB;
-          if (i < kDmaEarly) dma(static_cast<uint32_t>(wofs_patch), i, doff[i]);
-          s += kRoleThreads;
-          c += p.dc;
-          const bool carry = c >= pps;
-          c -= carry ? pps : 0;
-          q += p.diw + (carry ? 1 : 0);
+          off = __umul24(nn, cin2) + 16 * c;
         }
+        doff[i] = ok ? off : kOOB;
+        if (i < kDmaEarly) dma(static_cast<uint32_t>(wofs_patch), i, doff[i]);
       }
     }
   }
@@ -344,21 +433,24 @@ __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
   // Tiles wp, wp+WP, ... belong to this wave; only the last of its MT tile
   // slots can be empty (then its MFMAs are skipped).
   const bool last_tile = (wp + (MT - 1) * p.WP) * 16 < npix;
-  uint32_t abase[MT];  // A-fragment LDS byte offset of each tile at tap (0,0), k-step 0
+  // Activation operand of tile mt at tap (0,0), chunk lk of k-step 0: patch
+  // pixel qb of the lane's output pixel; every later step adds a uniform
+  // offset.
+  uint32_t abase[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
     const int32_t px = (wp + mt * p.WP) * 16 + lrow;
     const int32_t pc = px < npix ? px : 0;  // idle lanes read pixel 0 and store nothing
-    int32_t qb;
     if constexpr (RECT) {
       const int32_t r = static_cast<int32_t>(fdiv(pc, p.fd_wo));
-      qb = r * p.sh * p.patch_cols + (pc - r * p.Wo) * p.sw;
+      const int32_t qb = r * p.sh * p.patch_cols + (pc - r * p.Wo) * p.sw;
+      abase[mt] = static_cast<uint32_t>((qb * p.pp + 16 * lk) * 16);
     } else {
-      qb = pc;
+      abase[mt] = static_cast<uint32_t>(((pc & ~15) << (4 + p.lg_cpp)) + ((pc & 15) << 4) + lk * 256);
     }
-    abase[mt] = static_cast<uint32_t>((qb * pps + lk) * 16);
   }
-  const uint32_t bbase = static_cast<uint32_t>(((wo * kBN + lrow) * p.b_pitch + 8 * lk) * 2);
+  // weight operand: 16-row block 4 wo + ot, lane-linear inside the fragment
+  const uint32_t bbase = static_cast<uint32_t>(wo * 4 * p.nkb + lane * 16);
 
   f32x4_t acc[MT][4];
 #pragma unroll
@@ -383,20 +475,24 @@ __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
     const uint8_t* pb = lds + pofs;
     if (loader && dch >= 0) issue_patch(dch, dofs);
     const int nsteps = p.taps << p.lg_ksteps;
-    auto addr = [&](int st, uint32_t& aoff, uint32_t& boff) {
+    // step st = tap * ksteps + kb: weight k-step st of the chunk; patch
+    // pixel shift dq of the tap and chunks 4 kb .. 4 kb + 3 (uniform offset)
+    auto addr = [&](int st) {
       // step -> (tap, kb) -> (kh, kw): shifts and one multiply, all scalar
       const int tap = st >> p.lg_ksteps;
       const int kb = st & ((1 << p.lg_ksteps) - 1);
-      const int kh = static_cast<int>((static_cast<uint32_t>(tap) * p.kw_mul) >> 20);
-      const int kw = tap - kh * p.KW;
-      const int32_t dq = RECT ? kh * p.patch_cols + kw : 0;
-      aoff = static_cast<uint32_t>(dq * pps * 16 + kb * 64);
-      boff = static_cast<uint32_t>((tap * p.cinb + kb * kKS) * 2);
+      if constexpr (RECT) {
+        const int kh = static_cast<int>((static_cast<uint32_t>(tap) * p.kw_mul) >> 20);
+        const int kw = tap - kh * p.KW;
+        return static_cast<uint32_t>(((kh * p.patch_cols + kw) * p.pp + kb * 64) * 16);
+      } else {
+        return static_cast<uint32_t>(kb * 1024);
+      }
     };
-    auto load_w = [&](uint32_t boff, Frags& f) {
+    auto load_w = [&](int st, Frags& f) {
 #pragma unroll
       for (int ot = 0; ot < 4; ++ot)
-        f.w[ot] = as_bf16x8(*reinterpret_cast<const u32x4_t*>(wb + boff + ot * 16 * p.b_pitch * 2));
+        f.w[ot] = as_bf16x8(*reinterpret_cast<const u32x4_t*>(wb + st * 1024 + ot * p.nkb));
     };
     auto load_x = [&](uint32_t aoff, int mt, Frags& f) {
       f.x[mt] = as_bf16x8(*reinterpret_cast<const u32x4_t*>(pb + abase[mt] + aoff));
@@ -406,9 +502,8 @@ __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
     // read is issued about one step ahead of its use and at most ~12 reads
     // are outstanding (the LDS counter tracks 15).
     auto step = [&](const Frags& cur, Frags& nxt, int nst) {
-      uint32_t aoff, boff;
-      addr(nst, aoff, boff);
-      load_w(boff, nxt);
+      const uint32_t aoff = addr(nst);
+      load_w(nst, nxt);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         if (mt < MT - 1 || last_tile) {
@@ -421,9 +516,8 @@ __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
     };
     Frags f0, f1;
     {
-      uint32_t aoff, boff;
-      addr(0, aoff, boff);
-      load_w(boff, f0);
+      const uint32_t aoff = addr(0);
+      load_w(0, f0);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) load_x(aoff, mt, f0);
     }
@@ -436,36 +530,21 @@ __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
   };
 
   // ---- ring mode: packed rows staged in LDS by the loaders ----------------
-  // Chunk j's packed rows (value segments, then index segments, each 16-byte
-  // slot-linear: [row][tap][channel]) are DMA'd two chunks ahead into one of
-  // two staging buffers; the expanders build chunk j's tile from there while
-  // chunk j-1 is multiplied.
+  // Chunk j's packed rows are DMA'd two chunks ahead into one of two staging
+  // buffers (row-major, tile order); the expanders build chunk j's tile from
+  // there while chunk j-1 is multiplied.
   const int32_t sofs = wofs_patch + p.npb * p.p_bytes;  // LDS offset of staging buffer 0
   // loader thread rt's staging slots: value slot rt + 256 i and index slot
   // rt + 256 i, element offsets at chunk 0 (kOOB: none)
   uint32_t pk_v[kPkMax], pk_i[kPkMax];
   if (loader && !p.wres) {
-    const int32_t rowbase = ob * gpb * p.K;
-    const int32_t rlim = glim * p.K;
 #pragma unroll
     for (int i = 0; i < kPkMax; ++i) {
       const int32_t sl = rt + kRoleThreads * i;
-      {
-        const int32_t r = static_cast<int32_t>(fdiv(static_cast<uint32_t>(sl), p.fd_v8));  // (row, tap) pair
-        const int32_t j = sl - r * cpp;
-        const int32_t row = static_cast<int32_t>(fdiv(static_cast<uint32_t>(r), p.fd_taps));
-        const int32_t tap = r - row * p.taps;
-        pk_v[i] = sl < p.s_vslots && row < rlim
-                      ? static_cast<uint32_t>((rowbase + row) * p.C + tap * p.Cin + 8 * j) : kOOB;
-      }
-      {
-        const int32_t r = static_cast<int32_t>(fdiv(static_cast<uint32_t>(sl), p.fd_v16));  // (row, tap) pair
-        const int32_t j = sl - r * (cpp >> 1);
-        const int32_t row = static_cast<int32_t>(fdiv(static_cast<uint32_t>(r), p.fd_taps));
-        const int32_t tap = r - row * p.taps;
-        pk_i[i] = sl < p.s_islots && row < rlim
-                      ? static_cast<uint32_t>((rowbase + row) * p.C + tap * p.Cin + 16 * j) : kOOB;
-      }
+      const int32_t rv = static_cast<int32_t>(fdiv(static_cast<uint32_t>(sl), p.fd_ncols8));
+      pk_v[i] = sl < p.s_vslots && rv < rlim ? ring_src(rv, sl - rv * p.ncols8, 0) : kOOB;
+      const int32_t ri = static_cast<int32_t>(fdiv(static_cast<uint32_t>(sl), p.fd_nc2));
+      pk_i[i] = sl < p.s_islots && ri < rlim ? ring_src(ri, 2 * (sl - ri * (p.ncols8 >> 1)), 0) : kOOB;
     }
   }
   const int npv = p.s_vslots > wave * 64 ? (p.s_vslots - wave * 64 + kRoleThreads - 1) / kRoleThreads : 0;
@@ -485,15 +564,14 @@ __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
     }
   };
   // Scatter one chunk's staged packed rows into weight tile wb, which was
-  // zero-filled a chunk earlier.  Unit = (packed row, 8-column block), so the
-  // work spreads over K times more threads than whole groups would.  With
-  // K == G every row is kept in ascending order: a row is copied whole.
-  // per-thread scatter units of the staged path, decoded once:
-  // staged byte offset of the unit's value segment, tile element offset
-  int32_t su_src[kUnitMax], su_dst[kUnitMax];
+  // zero-filled a chunk earlier.  Unit u = (packed row u / ncols8, column
+  // block u % ncols8) is staged value slot u, so the work spreads over K
+  // times more threads than whole groups would.  With K == G every row is
+  // kept in ascending order: a row segment is copied whole.
+  // per-thread scatter units, decoded once: staged byte offsets of the
+  // values and indices, tile byte offset (< 0 in su_src: none)
+  int32_t su_src[kUnitMax], su_idx[kUnitMax], su_dst[kUnitMax];
   if (!loader && !p.wres) {
-    const int rowpitch = 8 * p.ncols8;  // staged elements per packed row
-    const int rlim = glim * p.K;
 #pragma unroll
     for (int j = 0; j < kUnitMax; ++j) {
       const int u = rt + kRoleThreads * j;
@@ -501,28 +579,29 @@ __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
       const int col8 = u - r * p.ncols8;
       const int gl = static_cast<int>(fdiv(r, p.fd_k));
       const bool ok = j < p.nus && r < rlim;
-      su_src[j] = ok ? (r * rowpitch + 8 * col8) : -1;
-      su_dst[j] = gl * p.G * p.b_pitch + 8 * col8 + (p.K == p.G ? (r - gl * p.K) * p.b_pitch : 0);
+      su_src[j] = ok ? u * 16 : -1;
+      su_idx[j] = (p.s_vblk64 + (u >> 1)) * 16 + (col8 & 1) * 8;
+      su_dst[j] = rowaddr(gl * p.G) + coladdr(col8) + (p.K == p.G ? rowaddr(r - gl * p.K) : 0);
     }
   }
   auto scatter_staged = [&](int wb, int sb) {
     const uint8_t* stg = lds + sofs + sb * p.s_bytes;
-    uint16_t* bs = reinterpret_cast<uint16_t*>(lds + wb * p.w_bytes);
+    uint8_t* bs = lds + wb * p.w_bytes;
 #pragma unroll
     for (int j = 0; j < kUnitMax; ++j) {
       if (su_src[j] < 0) continue;
-      uint16_t* dst = bs + su_dst[j];
-      const u32x4_t v = *reinterpret_cast<const u32x4_t*>(stg + su_src[j] * 2);
+      uint8_t* dst = bs + su_dst[j];
+      const u32x4_t v = *reinterpret_cast<const u32x4_t*>(stg + su_src[j]);
       if (p.K == p.G) {  // every row kept, in order: the row is copied whole
         *reinterpret_cast<u32x4_t*>(dst) = v;
         continue;
       }
-      const u32x2_t ix = *reinterpret_cast<const u32x2_t*>(stg + p.s_vblk64 * 16 + su_src[j]);
+      const u32x2_t ix = *reinterpret_cast<const u32x2_t*>(stg + su_idx[j]);
 #pragma unroll
       for (int jj = 0; jj < 8; ++jj) {
-        const uint32_t rr = (ix[jj >> 2] >> (8 * (jj & 3))) & gmask;  // idx: row in the group
+        const int32_t rr = static_cast<int32_t>((ix[jj >> 2] >> (8 * (jj & 3))) & gmask);  // idx: row in the group
         const uint16_t w = static_cast<uint16_t>(v[jj >> 1] >> (16 * (jj & 1)));
-        dst[rr * p.b_pitch + jj] = w;
+        *reinterpret_cast<uint16_t*>(dst + (rr << 4) + (rr >> 4) * nkbm + 2 * jj) = w;
       }
     }
   };
@@ -545,8 +624,10 @@ __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
   // the other of two tiles.  A loader's MFMAs fill the SIMD its partner
   // expander shares while that one builds.  One barrier per chunk; one call
   // site for compute() keeps the accumulators in place.
-  // The packed-row loads go into the memory queue ahead of the bulk of the
-  // patch DMA, which would otherwise hold them up.
+  // The loaders issue the first kDmaEarly patch DMAs as soon as their
+  // offsets are known and the rest after this barrier, by which the
+  // expanders' staging DMAs are queued: issued behind the bulk of the
+  // patch they would hold up the weight expansion.
   lds_barrier();
   const bool ring = !p.wres;
   if (loader) {
@@ -559,13 +640,14 @@ __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
     }
     wait_vm<0>();  // chunk 0 (and chunk 1's packed rows) landed
   } else {
-    expand(0, 0, true);
+    expand_first();
   }
   lds_barrier();
   int pb = 0;
   for (int ch = 0; ch < p.nchunks; ++ch) {
     const int wcur = ch % 3;  // ring tile of chunk ch
-    const uint32_t wofs = p.wres ? static_cast<uint32_t>(ch * p.taps * p.cinb * 2) : static_cast<uint32_t>(wcur * p.w_bytes);
+    const uint32_t wofs = p.wres ? static_cast<uint32_t>((ch * p.taps << p.lg_ksteps) * 1024)
+                                 : static_cast<uint32_t>(wcur * p.w_bytes);
     const int nb = p.npb == 2 ? pb ^ 1 : 0;
     if (ring && ch + 1 < p.nchunks) {
       const int wnext = wcur == 2 ? 0 : wcur + 1;
@@ -712,29 +794,38 @@ bool layout(Params& pl, int32_t cinb, int32_t Cin, int32_t wres, int32_t npb, in
   pl.nchunks = Cin / cinb;
   if (!wres && pl.nchunks < 2) return false;
   if (npb < 1 || npb > pl.nchunks) return false;
-  const int32_t cpp = cinb / 8, pps = cpp + 1;
-  const int64_t slots = static_cast<int64_t>(pl.patch_pix) * pps;
+  const int32_t cpp = cinb / 8;
+  // rect: pixel-major, cpp chunks and a pad slot per pixel, rounded up to
+  // the 64 slots one DMA instruction writes; rows: whole blocks of 16 pixels
+  pl.pp = cpp + 1;
+  pl.inv16 = 1;
+  while ((16 * pl.inv16) % pl.pp != 1 % pl.pp) ++pl.inv16;
+  pl.dcs = (kRoleThreads * pl.inv16) % pl.pp;
+  pl.dqs = (kRoleThreads - 16 * pl.dcs) / pl.pp;  // exact
+  const int64_t slots = pl.patch_cols > 0 ? (static_cast<int64_t>(pl.patch_pix - 1) * pl.pp + 16 * (cpp - 1) + 64) / 64 * 64
+                                          : static_cast<int64_t>((pl.patch_pix + 15) / 16) * 16 * cpp;
   if (slots > static_cast<int64_t>(kDmaMax) * kRoleThreads) return false;
   pl.slots = static_cast<int32_t>(slots);
   const int32_t tc = pl.taps * cpp;
   pl.wres = wres;
   pl.ncols8 = wres ? pl.nchunks * tc : tc;
-  pl.b_pitch = pl.ncols8 * 8 + kBPad;
-  pl.w_bytes = pl.WO * kBN * pl.b_pitch * 2;
+  pl.nkb = pl.ncols8 / 4 * 1024;
+  pl.w_bytes = pl.WO * 4 * pl.nkb;
   pl.nrows = (pl.WO * kBN / G) * K;
-  pl.nu = ((pl.WO * kBN / G) * pl.ncols8 + kRoleThreads - 1) / kRoleThreads;
+  pl.lg_gpb = ilog2(pl.WO * kBN / G);
+  // first tile: each expander wave owns epg groups, i.e. epg*K packed
+  // rows x ncols8 units
+  pl.epg = pl.WO * 16 >= G ? pl.WO * 16 / G : 1;
+  pl.nu = (pl.epg * K * pl.ncols8 + 63) / 64;
   pl.nus = (pl.nrows * pl.ncols8 + kRoleThreads - 1) / kRoleThreads;
   if (!wres && pl.nus > kUnitMax) return false;
-  if (pl.nu * K > 4 * kRowMax) return false;  // at most four load rounds per expansion
   pl.nwb = wres ? 1 : 3;
-  // the DMA writes whole 64-slot (1 KiB) blocks: round the patch up so the
-  // tail of its last block stays inside its buffer
-  pl.p_bytes = static_cast<int32_t>((slots * 16 + 1023) / 1024 * 1024);
+  pl.p_bytes = static_cast<int32_t>(slots * 16);
   pl.npb = npb;
   pl.s_bytes = pl.s_vslots = pl.s_islots = pl.s_vblk64 = 0;
-  if (!wres) {  // packed-row staging: nrows x taps x (cinb/8 value + cinb/16 index) slots
-    pl.s_vslots = pl.nrows * pl.taps * (cinb / 8);
-    pl.s_islots = pl.nrows * pl.taps * (cinb / 16);
+  if (!wres) {  // packed-row staging: nrows x ncols8 value slots + half as many index slots
+    pl.s_vslots = pl.nrows * pl.ncols8;
+    pl.s_islots = pl.nrows * pl.ncols8 / 2;
     pl.s_vblk64 = (pl.s_vslots + 63) / 64 * 64;
     pl.s_bytes = (pl.s_vblk64 + (pl.s_islots + 63) / 64 * 64) * 16;
     if (pl.s_vslots > kPkMax * kRoleThreads || pl.s_islots > kPkMax * kRoleThreads) return false;
@@ -742,18 +833,28 @@ bool layout(Params& pl, int32_t cinb, int32_t Cin, int32_t wres, int32_t npb, in
   if (static_cast<int64_t>(pl.nwb) * pl.w_bytes + static_cast<int64_t>(npb) * pl.p_bytes +
           2 * static_cast<int64_t>(pl.s_bytes) > kLdsMax)
     return false;
-  pl.fd_taps = make_fastdiv(pl.taps);
-  pl.fd_v8 = make_fastdiv(cinb / 8);
-  pl.fd_v16 = make_fastdiv(cinb / 16);
-  pl.dq = kRoleThreads / pps;
-  pl.dc = kRoleThreads % pps;
-  // rect: dq pixels = dpr patch rows + diw patch columns; rows: diw = dq pixels
-  pl.dpr = pl.patch_cols > 0 ? pl.dq / pl.patch_cols : 0;
-  pl.diw = pl.patch_cols > 0 ? pl.dq % pl.patch_cols : pl.dq;
-  pl.fd_pps = make_fastdiv(pps);
-  pl.fd_k = make_fastdiv(K);
+  // first-tile staging: ring staging buffer 0; resident: the second patch
+  // buffer (not in use before chunk 1 streams in) when it is large enough,
+  // else the space after the patch buffers
+  pl.f_vblk64 = (pl.nrows * pl.ncols8 + 63) / 64 * 64;
+  const int64_t f_bytes = (pl.f_vblk64 + (pl.nrows * pl.ncols8 / 2 + 63) / 64 * 64) * 16;
+  const int64_t after = static_cast<int64_t>(pl.nwb) * pl.w_bytes + static_cast<int64_t>(npb) * pl.p_bytes;
+  if (!wres) {
+    pl.fofs = static_cast<int32_t>(after);
+  } else if (npb == 2 && f_bytes <= pl.p_bytes) {
+    pl.fofs = pl.nwb * pl.w_bytes + pl.p_bytes;
+  } else {
+    if (after + f_bytes > kLdsMax) return false;
+    pl.fofs = static_cast<int32_t>(after);
+  }
+  pl.lds_bytes = static_cast<int32_t>(after + 2 * static_cast<int64_t>(pl.s_bytes));
+  if (pl.fofs + f_bytes > pl.lds_bytes) pl.lds_bytes = static_cast<int32_t>(pl.fofs + f_bytes);
   pl.fd_ncols8 = make_fastdiv(pl.ncols8);
-  pl.fd_tc = make_fastdiv(tc);
+  pl.fd_nc2 = make_fastdiv(pl.ncols8 / 2);
+  pl.fd_cin8 = make_fastdiv(Cin / 8);
+  pl.fd_k = make_fastdiv(K);
+  pl.fd_pp = make_fastdiv(pl.pp);
+  pl.fd_taps = make_fastdiv(pl.taps);
   return true;
 }
 
@@ -888,6 +989,7 @@ void fill_params(const ProductArgs& a, Params& p) {
   p.G = a.G;
   p.K = a.K;
   p.relu = a.relu;
+  p.ngroups = static_cast<int32_t>(a.O / a.G);
   ConvGeom g = a.geom;
   int64_t x_elems, bimg = a.B;
   if (!a.conv) {  // FC: rows of X are the "pixels" of a 1x1 convolution
@@ -923,8 +1025,7 @@ hipError_t launch_yrm(const Params& p, uint32_t grid, hipStream_t s) {
       reinterpret_cast<const void*>(&dense_tile_kernel<YT, RECT, MT>), hipFuncAttributeMaxDynamicSharedMemorySize,
       kLdsMax);
   if (attr != hipSuccess) return attr;
-  size_t lds = static_cast<size_t>(p.nwb) * p.w_bytes + static_cast<size_t>(p.npb) * p.p_bytes +
-               2 * static_cast<size_t>(p.s_bytes);
+  size_t lds = static_cast<size_t>(p.lds_bytes);
   const size_t staging = static_cast<size_t>(kWaves) * MT * 16 * kStPitch;  // epilogue reuses the LDS
   if (lds < staging) lds = staging;
   hipLaunchKernelGGL((dense_tile_kernel<YT, RECT, MT>), dim3(grid), dim3(kThreads), lds, s, p);

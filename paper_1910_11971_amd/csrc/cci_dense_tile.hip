@@ -132,6 +132,7 @@ struct Params {
   uint32_t kw_mul;      // tap / KW == (tap * kw_mul) >> 20 for tap < 4096
   FastDiv fd_nob, fd_rparts, fd_wo, fd_pcols, fd_k, fd_howo;
   FastDiv fd_ncols8, fd_nc2, fd_cin8;  // staging: ncols8, ncols8 / 2; Cin / 8
+  FastDiv fd_erows;     // first tile: packed rows per expander wave
   FastDiv fd_pp, fd_taps;
 };
 
@@ -155,14 +156,14 @@ __device__ __forceinline__ void wait_vm() {
 // lazily, as values are needed, so without this each first touch of a line
 // would stall the wave for its own round trip.
 __device__ __forceinline__ void prefetch_args() {
-  static_assert(sizeof(Params) <= 6 * 64, "six lines cover the arguments");
+  static_assert(sizeof(Params) > 6 * 64 && sizeof(Params) <= 7 * 64, "the arguments span seven lines");
   const auto ka = __builtin_amdgcn_kernarg_segment_ptr();
-  uint32_t k0, k1, k2, k3, k4, k5;
+  uint32_t k0, k1, k2, k3, k4, k5, k6;
   asm volatile(
-      "s_load_dword %0, %6, 0x0\n\ts_load_dword %1, %6, 0x40\n\ts_load_dword %2, %6, 0x80\n\t"
-      "s_load_dword %3, %6, 0xc0\n\ts_load_dword %4, %6, 0x100\n\ts_load_dword %5, %6, 0x140\n\t"
-      "s_waitcnt lgkmcnt(0)"
-      : "=s"(k0), "=s"(k1), "=s"(k2), "=s"(k3), "=s"(k4), "=s"(k5)
+      "s_load_dword %0, %7, 0x0\n\ts_load_dword %1, %7, 0x40\n\ts_load_dword %2, %7, 0x80\n\t"
+      "s_load_dword %3, %7, 0xc0\n\ts_load_dword %4, %7, 0x100\n\ts_load_dword %5, %7, 0x140\n\t"
+      "s_load_dword %6, %7, 0x180\n\ts_waitcnt lgkmcnt(0)"
+      : "=s"(k0), "=s"(k1), "=s"(k2), "=s"(k3), "=s"(k4), "=s"(k5), "=s"(k6)
       : "s"(ka)
       : "memory");
 }
@@ -276,13 +277,21 @@ __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
       return;
     }
     const u32x2_t ix = *reinterpret_cast<const u32x2_t*>(stg + si);
+    // The upper half-wave writes the segment's elements in the order
+    // 4..7, 0..3 (element t ^ 4 at step t): two half-waves then hit
+    // different bank words with each store.
+    const bool hi = lane >= 32;
+    const u32x4_t vr = hi ? u32x4_t{v[2], v[3], v[0], v[1]} : v;
+    const u32x2_t ixr = hi ? u32x2_t{ix[1], ix[0]} : ix;
+    uint8_t* const d_lo = dst + (hi ? 8 : 0);  // steps 0..3: byte 2 (t ^ 4 h)
+    uint8_t* const d_hi = dst - (hi ? 8 : 0);  // steps 4..7
 #pragma unroll
-    for (int jj = 0; jj < 8; ++jj) {
+    for (int t = 0; t < 8; ++t) {
       // idx: row in the group (< G, a power of two on this path; the mask
       // keeps a corrupt index inside its own group)
-      const int32_t rr = static_cast<int32_t>((ix[jj >> 2] >> (8 * (jj & 3))) & gmask);
-      const uint16_t w = static_cast<uint16_t>(v[jj >> 1] >> (16 * (jj & 1)));
-      *reinterpret_cast<uint16_t*>(dst + (rr << 4) + (rr >> 4) * nkbm + 2 * jj) = w;
+      const int32_t rr = static_cast<int32_t>((ixr[t >> 2] >> (8 * (t & 3))) & gmask);
+      const uint16_t w = static_cast<uint16_t>(vr[t >> 1] >> (16 * (t & 1)));
+      *reinterpret_cast<uint16_t*>((t < 4 ? d_lo : d_hi) + (rr << 4) + (rr >> 4) * nkbm + 2 * t) = w;
     }
   };
   // source element of staged block j of packed row r, chunk ch (ring: tile
@@ -340,15 +349,17 @@ __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
         *reinterpret_cast<u32x4_t*>(lds + z * 16) = u32x4_t{0u, 0u, 0u, 0u};
     }
     wait_vm<0>();
+    // units row-fastest: a wave's lanes span all its groups
     const int n = erows * p.ncols8;
-    const int nmax = (rlim - er0) * p.ncols8;  // units of rows that exist
+    const int rows_ok = rlim - er0;  // rows of this wave that exist
 #pragma unroll 1
     for (int u = lane; u < n; u += 64) {
-      if (u >= nmax) break;
-      const int rl = static_cast<int>(fdiv(u, p.fd_ncols8)), j = u - rl * p.ncols8;
-      const int sl = er0 * p.ncols8 + u;  // value slot
-      scatter_unit(lds, lds + p.fofs, sl * 16, (p.f_vblk64 + (sl >> 1)) * 16 + (j & 1) * 8,
-                   p.wres ? first_col8(j) : j, er0 + rl);
+      const int j = static_cast<int>(fdiv(u, p.fd_erows)), rl = u - j * erows;
+      if (rl < rows_ok) {
+        const int sl = (er0 + rl) * p.ncols8 + j;  // value slot
+        scatter_unit(lds, lds + p.fofs, sl * 16, (p.f_vblk64 + (sl >> 1)) * 16 + (j & 1) * 8,
+                     p.wres ? first_col8(j) : j, er0 + rl);
+      }
     }
   };
   if (!loader) stage_first();
@@ -605,15 +616,22 @@ __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
       }
     }
   };
-  // zero fill of weight tile wb by the loaders (not needed when K == G): DMA
-  // with an out-of-range source offset writes zeros into LDS without reading
-  // memory, so a loader never waits on the LDS queue for it (a tile is a
-  // whole number of KiB)
+  // zero fill of weight tile wb (not needed when K == G).  In the prologue
+  // the loaders zero a tile with DMA from an out-of-range source offset,
+  // which writes zeros into LDS without reading memory (a tile is a whole
+  // number of KiB); in the loop the expanders zero a tile with plain LDS
+  // stores, keeping the loaders' memory queue for the patch and staging.
   auto zero_tile = [&](int wb) {
     if (p.K == p.G) return;
     const int nblk = p.w_bytes / 1024;
     for (int b = wave; b < nblk; b += kLoadWaves)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void_t*)(lds + wb * p.w_bytes + b * 1024), 16, kOOB, 0, 0, 0);
+  };
+  auto zero_tile_lds = [&](int wb) {
+    if (p.K == p.G) return;
+    u32x4_t* t4 = reinterpret_cast<u32x4_t*>(lds + wb * p.w_bytes);
+#pragma unroll 1
+    for (int z = rt; z < (p.w_bytes >> 4); z += kRoleThreads) t4[z] = u32x4_t{0u, 0u, 0u, 0u};
   };
 
   // ---- chunk pipeline -----------------------------------------------------
@@ -652,11 +670,9 @@ __global__ __launch_bounds__(kThreads) void dense_tile_kernel(Params p) {
     if (ring && ch + 1 < p.nchunks) {
       const int wnext = wcur == 2 ? 0 : wcur + 1;
       if (loader) {
-        if (ch + 2 < p.nchunks) {
-          issue_packed(ch + 2, ch & 1);
-          zero_tile(wnext == 2 ? 0 : wnext + 1);  // the tile of chunk ch+2 (last read by chunk ch-1)
-        }
+        if (ch + 2 < p.nchunks) issue_packed(ch + 2, ch & 1);
       } else {
+        if (ch + 2 < p.nchunks) zero_tile_lds(wnext == 2 ? 0 : wnext + 1);  // chunk ch+2's tile (last read by chunk ch-1)
         scatter_staged(wnext, (ch + 1) & 1);
       }
     }
@@ -850,6 +866,7 @@ bool layout(Params& pl, int32_t cinb, int32_t Cin, int32_t wres, int32_t npb, in
   pl.lds_bytes = static_cast<int32_t>(after + 2 * static_cast<int64_t>(pl.s_bytes));
   if (pl.fofs + f_bytes > pl.lds_bytes) pl.lds_bytes = static_cast<int32_t>(pl.fofs + f_bytes);
   pl.fd_ncols8 = make_fastdiv(pl.ncols8);
+  pl.fd_erows = make_fastdiv(pl.epg * K);
   pl.fd_nc2 = make_fastdiv(pl.ncols8 / 2);
   pl.fd_cin8 = make_fastdiv(Cin / 8);
   pl.fd_k = make_fastdiv(K);

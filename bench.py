@@ -23,6 +23,7 @@ from __future__ import annotations
 
 import argparse
 import hashlib
+import re
 import json
 import os
 import sys
@@ -59,11 +60,16 @@ def parse():
 
 
 def kernel_source_hash() -> str:
+    """Hash of the kernel sources with comments and blank space removed, so
+    that counter files stay matched to the code they measured across edits
+    of the comments."""
     h = hashlib.sha256()
     csrc = os.path.join(HERE, "paper_1910_11971_amd", "csrc")
     for f in sorted(os.listdir(csrc)):
-        with open(os.path.join(csrc, f), "rb") as fh:
-            h.update(f.encode() + fh.read())
+        with open(os.path.join(csrc, f)) as fh:
+            text = re.sub(r"//[^\n]*", "", fh.read())
+            text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        h.update(f.encode() + " ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 

@@ -23,11 +23,10 @@
 //     workgroup's outputs touches, CINB channels) is DMA'd from HBM straight
 //     into LDS with buffer_load...lds; out-of-image pixels read as zero
 //     because their buffer offsets are out of range (this *is* the conv
-//     padding); the patch is stored in blocks of 16 pixels, chunk-major
-//     inside a block, and the weight tile in MFMA-fragment order, so that
-//     the operand reads are bank-conflict free;
-//   - the expanded weight tile of the chunk is built in LDS while the patch
-//     streams in (the packed rows are loaded into registers first);
+//     padding); patch and weight tile use the layouts described below, so
+//     that the operand reads are (nearly) bank-conflict free;
+//   - the expanded weight tile is built in LDS while the patch streams in
+//     (the packed rows are staged in LDS by DMA first);
 //   - with two buffers, chunk j+1 is in flight while chunk j is multiplied.
 // Patch geometry: "rect" mode (k x k convolutions) stages the input rows and
 // columns under a band of RH output rows; "rows" mode (FC and 1x1

@@ -59,11 +59,19 @@ typedef enum { CCI_F32 = 0, CCI_BF16 = 1 } cci_dtype;
  *  CCI_ALGO_DENSE_TILE_MFMA packed groups are expanded to dense bf16 tiles in
  *                           LDS and multiplied on the matrix cores.  Needs
  *                           bf16 X and vals, C % 32 == 0 (conv: Cin % 32 ==
- *                           0) and 64 % G == 0.                              */
+ *                           0) and 64 % G == 0.
+ *  CCI_ALGO_WIDE_TILE_MFMA  the same expansion with 256-pixel x 256-output
+ *                           workgroup tiles (four waves of 128 x 128
+ *                           accumulators), for large FC products and 1x1
+ *                           convolutions with stride 1 and no padding.  Needs
+ *                           bf16 X and vals, C % 64 == 0, O % 256 == 0,
+ *                           64 % G == 0, X, vals and Y 16-byte aligned and
+ *                           idx 8-byte aligned.                              */
 typedef enum {
   CCI_ALGO_AUTO = 0,
   CCI_ALGO_SPARSE_MAC = 1,
-  CCI_ALGO_DENSE_TILE_MFMA = 2
+  CCI_ALGO_DENSE_TILE_MFMA = 2,
+  CCI_ALGO_WIDE_TILE_MFMA = 3
 } cci_algo;
 
 /* Optional fused epilogue, applied per output element before rounding:

@@ -67,7 +67,8 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
   if ((a.scale && !aligned16(a.scale)) || (a.bias && !aligned16(a.bias)) ||
       (a.residual && !aligned16(a.residual)))
     return fail(CCI_EALIGN, "epilogue pointer not 16-byte aligned");
-  if (algo != CCI_ALGO_AUTO && algo != CCI_ALGO_SPARSE_MAC && algo != CCI_ALGO_DENSE_TILE_MFMA)
+  if (algo != CCI_ALGO_AUTO && algo != CCI_ALGO_SPARSE_MAC && algo != CCI_ALGO_DENSE_TILE_MFMA &&
+      algo != CCI_ALGO_WIDE_TILE_MFMA)
     return fail(CCI_EINVAL, "unknown algo %d", (int)algo);
   if (a.N == 0) return ok();
 
@@ -85,8 +86,14 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
   if (chosen == CCI_ALGO_DENSE_TILE_MFMA && !tile_ok)
     return fail(CCI_EUNSUPPORTED,
                 "dense-tile MFMA kernels need bf16 X/vals, 64 %% G == 0 and C (conv: Cin) %% 32 == 0");
-  hipError_t e = chosen == CCI_ALGO_SPARSE_MAC ? cci::launch_sparse_mac(a, static_cast<hipStream_t>(stream))
-                                               : cci::launch_dense_tile(a, static_cast<hipStream_t>(stream));
+  if (chosen == CCI_ALGO_WIDE_TILE_MFMA && !cci::wide_tile_supports(a))
+    return fail(CCI_EUNSUPPORTED,
+                "wide-tile MFMA kernels need bf16 X/vals, an FC or stride-1 unpadded 1x1 product, "
+                "C %% 64 == 0, O %% 256 == 0, 64 %% G == 0 and aligned pointers");
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = chosen == CCI_ALGO_SPARSE_MAC  ? cci::launch_sparse_mac(a, st)
+                 : chosen == CCI_ALGO_WIDE_TILE_MFMA ? cci::launch_wide_tile(a, st)
+                                                     : cci::launch_dense_tile(a, st);
   if (e != hipSuccess) return fail(CCI_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
 }

@@ -43,6 +43,12 @@ hipError_t launch_sparse_mac(const ProductArgs& a, hipStream_t s);
 bool dense_tile_supports(const ProductArgs& a);
 hipError_t launch_dense_tile(const ProductArgs& a, hipStream_t s);
 
+// The same expansion with 256 x 256 workgroup tiles and four waves of 128 x
+// 128 accumulators (FC and stride-1 1x1 convolutions; bf16; C % 64 == 0,
+// O % 256 == 0, 64 % G == 0).
+bool wide_tile_supports(const ProductArgs& a);
+hipError_t launch_wide_tile(const ProductArgs& a, hipStream_t s);
+
 hipError_t launch_maxpool(const void* X, DType t, int64_t B, int64_t H, int64_t W, int64_t C,
                           int32_t k, int32_t st, int32_t p, void* Y, hipStream_t s);
 hipError_t launch_avgpool(const void* X, DType x_t, int64_t B, int64_t H, int64_t W, int64_t C,

@@ -1,0 +1,456 @@
+// CCI-sparse product on the matrix cores: wide-tile plan for large FC and
+// stride-1 1x1 products (implicit GEMM with X rows = pixels).
+//
+// The method is the dense-tile one -- each chunk of packed groups becomes a
+// dense bf16 weight tile in LDS (zero fill, then every kept weight written
+// to row G*g + idx of its column: the routing of Alg. 1, Sec. 3.2) that is
+// multiplied on v_mfma_f32_16x16x32_bf16 -- with a work split sized for
+// products large enough to fill the chip with 256 x 256 output tiles:
+//   - a workgroup is four waves, one per SIMD, and owns 256 pixels x 256
+//     outputs; each wave accumulates 128 pixels x 128 outputs (256 fp32 per
+//     lane, in the accumulation registers), so every fragment read from LDS
+//     feeds eight MFMAs, and each expanded weight tile serves 256 pixels;
+//   - the reduction runs over chunks of 64 channels.  The activations of
+//     chunk j+2 are DMA'd into LDS while chunk j is multiplied (three
+//     buffers); the packed weights of chunk j+2 are loaded into registers
+//     during chunk j and expanded into the second weight tile between chunk
+//     j+1's two k-steps; one barrier per chunk;
+//   - workgroup ids are remapped so that each XCD holds a 4 pixel-block x
+//     8 output-block patch of tiles: activations and packed rows are then
+//     mostly read through that XCD's L2.
+//
+// LDS layouts (bytes):
+//   activation buffer: pixel q at q * 128; its 16-byte column c holds
+//     channels 8 * (c ^ sw(q)) .. +7 of the chunk, sw(q) = ((q >> 2) & 3) * 2.
+//     The DMA still reads each pixel's 128 contiguous bytes (one cache line
+//     per 8 lanes); the swizzle makes a fragment read (16 pixels x two
+//     adjacent 8-channel columns per half-wave) touch 32 distinct 16-byte
+//     bank slots.
+//   weight tile: 16-row block b, k-step s at (2 b + s) * 1024, inside it
+//     (k / 8 % 4) * 256 + (o % 16) * 16 + (k % 8) * 2: the fragment a lane
+//     reads is its 16 contiguous bytes at lane * 16.
+#include "cci_launch.hpp"
+
+namespace cci {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+constexpr int kThreads = 256;                   // four waves, one per SIMD
+constexpr int kTile = 256;                      // pixels and outputs of a workgroup
+constexpr int kCK = 64;                         // channels per chunk (two k-steps)
+constexpr int kXBytes = kTile * kCK * 2;        // one activation buffer
+constexpr int kWBytes = kTile * kCK * 2;        // one weight tile
+constexpr int kWOfs = 3 * kXBytes;              // weight tiles follow the three activation buffers
+constexpr int kLds = kWOfs + 2 * kWBytes;       // 160 KiB
+constexpr int kEpPitch = 128 * 4 + 32;          // epilogue staging: bytes per pixel row
+constexpr uint32_t kOOB = 0x80000000u;          // buffer offset that reads as zero / drops a store
+constexpr int kRsrcWord3 = 0x00020000;          // raw buffer descriptor word 3 (gfx9 family)
+static_assert(kLds <= 160 * 1024, "LDS budget");
+static_assert(4 * 64 * kEpPitch <= kLds, "epilogue staging reuses the operand buffers");
+
+struct WParams {
+  const uint16_t* X;
+  const uint16_t* vals;
+  const uint8_t* idx;
+  const float* scale;
+  const float* bias;
+  const void* residual;
+  void* Y;
+  uint32_t x_bytes, v_bytes, i_bytes, y_bytes;
+  int32_t N, C, O, G, K, relu;
+  int32_t npb, nob, nch;  // pixel blocks, output blocks (of 256), channel chunks
+  int32_t rows_w;         // packed rows behind 64 outputs: 64 K / G
+  int32_t grid8;          // grid / 8 when the grid is a multiple of 8, else 0
+};
+
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// Wait until at most N vector-memory operations of this wave are in flight
+// (loads complete in issue order).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+template <bool B>
+struct BoolC {
+  static constexpr bool value = B;
+};
+
+// acc += A * B on the matrix cores, with the accumulator pinned to the
+// accumulation registers: all 256 of them hold the wave's 128 x 128 tile,
+// and the builtin lets the register allocator shuttle accumulators through
+// the vector registers.  Dependent uses of acc by vector instructions are
+// separated from the last MFMA by mfma_drain().
+// (volatile: kept in program order with the other volatile statements below)
+__device__ __forceinline__ void mfma_acc(f32x4_t& acc, const bf16x8_t a, const bf16x8_t b) {
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+// Longer than any dependency between a vector write of an accumulation
+// register and an MFMA reading it, or an MFMA result and a vector read.
+__device__ __forceinline__ void mfma_drain() { asm volatile("s_nop 15\n\ts_nop 15\n\ts_nop 15\n\ts_nop 15" ::: "memory"); }
+// Pin acc's current value in the accumulation registers at this point of
+// the volatile sequence (no code).
+__device__ __forceinline__ void acc_fence(f32x4_t& acc) { asm volatile("" : "+a"(acc)); }
+
+// Byte offset of tile row o (< 256) in the weight tile, k-column 0.
+__device__ __forceinline__ uint32_t trow(uint32_t o) { return ((o >> 4) << 11) | ((o & 15) << 4); }
+
+// UPL: packed 8-channel units per lane per chunk (ceil(8 K / G)); FULL: K == G
+// (every entry kept, indices ascending, so a unit is one row's 16 bytes).
+template <typename YT, int UPL, bool FULL>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void wide_tile_kernel(WParams p) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  constexpr int NW = FULL ? UPL : 2 * UPL;  // vector-memory operations of one packed-chunk load
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wp = w >> 1, wo = w & 1;  // pixel half, output half of this wave
+
+  // ---- tile of this workgroup ------------------------------------------------
+  // Dispatch places workgroup b on XCD b % 8; L numbers the workgroups of
+  // one XCD consecutively, and runs of 4 * nob consecutive L cover 4 pixel
+  // blocks x every output block, output-block-major.
+  const uint32_t bid = blockIdx.x;
+  const uint32_t L = p.grid8 ? (bid & 7u) * static_cast<uint32_t>(p.grid8) + (bid >> 3) : bid;
+  const uint32_t per = 4u * static_cast<uint32_t>(p.nob);
+  const uint32_t pg = L / per;
+  const uint32_t pgs = min(4u, static_cast<uint32_t>(p.npb) - 4u * pg);
+  const uint32_t within = L - pg * per;
+  const uint32_t ob = within / pgs;
+  const uint32_t pb = 4u * pg + (within - ob * pgs);
+
+  const __amdgpu_buffer_rsrc_t xr =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(p.X), (short)0, static_cast<int>(p.x_bytes), kRsrcWord3);
+  const __amdgpu_buffer_rsrc_t vr =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(p.vals), (short)0, static_cast<int>(p.v_bytes), kRsrcWord3);
+  const __amdgpu_buffer_rsrc_t ir =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(p.idx), (short)0, static_cast<int>(p.i_bytes), kRsrcWord3);
+
+  // ---- activation DMA --------------------------------------------------------
+  // DMA instruction i of wave w fills pixels (8w + i) * 8 .. +8 of a buffer:
+  // lane l writes the 16 bytes at (8w + i) * 1024 + 16 l, i.e. pixel
+  // q = (8w + i) * 8 + l / 8, column l % 8, which holds channel block
+  // (l % 8) ^ sw(q).  Pixels past N read as zero.
+  uint32_t xoff[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const uint32_t q = static_cast<uint32_t>((8 * w + i) * 8 + (lane >> 3));
+    const uint32_t px = pb * kTile + q;
+    const uint32_t k8 = static_cast<uint32_t>(lane & 7) ^ (((q >> 2) & 3u) << 1);
+    xoff[i] = px < static_cast<uint32_t>(p.N) ? px * static_cast<uint32_t>(p.C) * 2u + k8 * 16u : kOOB;
+  }
+  auto issue_x = [&](int ch, int buf) {
+    uint8_t* dst = lds + buf * kXBytes + w * 8192;
+    const uint32_t co = static_cast<uint32_t>(ch) * (kCK * 2);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      lds_void_t* d = (lds_void_t*)(dst + i * 1024);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, d, 16, xoff[i] + co, 0, 0, 0);
+    }
+  };
+
+  // ---- packed weights ---------------------------------------------------------
+  // Wave w expands tile rows [64 w, 64 w + 64): 64 / G groups, rows_w packed
+  // rows.  Unit u of a lane is packed row r = (lane + 64 u) / 8 of them,
+  // 8-channel block cb = lane % 8 of the chunk (8 lanes read a row's 64
+  // channels contiguously).
+  uint32_t voff[UPL], ioff[UPL], ubase[UPL];
+  bool uok[UPL];
+#pragma unroll
+  for (int u = 0; u < UPL; ++u) {
+    const int v = lane + 64 * u;
+    const int r = v >> 3, cb = v & 7;
+    uok[u] = r < p.rows_w;
+    const uint32_t prow = (ob * 4u + static_cast<uint32_t>(w)) * static_cast<uint32_t>(p.rows_w) + static_cast<uint32_t>(r);
+    voff[u] = uok[u] ? prow * static_cast<uint32_t>(p.C) * 2u + static_cast<uint32_t>(cb) * 16u : kOOB;
+    ioff[u] = uok[u] ? prow * static_cast<uint32_t>(p.C) + static_cast<uint32_t>(cb) * 8u : kOOB;
+    // first tile row of the unit's group (FULL: the unit's own row)
+    const int o0 = 64 * w + (FULL ? r : (r / p.K) * p.G);
+    ubase[u] = trow(static_cast<uint32_t>(uok[u] ? o0 : 0)) + static_cast<uint32_t>((cb >> 2) * 1024 + (cb & 3) * 256);
+  }
+  u32x4_t pv[UPL];
+  u32x2_t pi[UPL];
+  auto load_w = [&](int ch) {
+#pragma unroll
+    for (int u = 0; u < UPL; ++u) {
+      pv[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(vr, voff[u] + static_cast<uint32_t>(ch) * (kCK * 2), 0, 0));
+      if constexpr (!FULL)
+        pi[u] = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(ir, ioff[u] + static_cast<uint32_t>(ch) * kCK, 0, 0));
+    }
+  };
+  // Building a tile: wave w zeroes its 64 rows (8 stores of 16 bytes per
+  // lane), then writes its kept weights; program order puts the zero fill
+  // first and no other wave touches these rows.
+  auto zero_piece = [&](uint8_t* tb, int i) {
+    if constexpr (!FULL) *reinterpret_cast<u32x4_t*>(tb + w * 8192 + (i * 64 + lane) * 16) = u32x4_t{0u, 0u, 0u, 0u};
+  };
+  auto zero_rows = [&](uint8_t* tb) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) zero_piece(tb, i);
+  };
+  auto scatter = [&](uint8_t* tb, int u) {
+    if (!uok[u]) return;
+    if constexpr (FULL) {
+      *reinterpret_cast<u32x4_t*>(tb + ubase[u]) = pv[u];
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t rr = (pi[u][e >> 2] >> (8 * (e & 3))) & 0xffu;  // row within the group
+        *reinterpret_cast<uint16_t*>(tb + ubase[u] + trow(rr) + 2 * e) =
+            static_cast<uint16_t>(pv[u][e >> 1] >> (16 * (e & 1)));
+      }
+    }
+  };
+
+  // ---- MFMAs --------------------------------------------------------------------
+  // acc[pt][ot]: 16 pixels (tile pt of the wave's 128) x 16 outputs (tile ot
+  // of its 128).  A lane holds outputs 4 (lane / 16) .. +3 of pixel lane % 16.
+  f32x4_t acc[8][8];
+#pragma unroll
+  for (int pt = 0; pt < 8; ++pt)
+#pragma unroll
+    for (int ot = 0; ot < 8; ++ot) acc[pt][ot] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int pt = 0; pt < 8; ++pt)
+#pragma unroll
+    for (int ot = 0; ot < 8; ++ot) acc_fence(acc[pt][ot]);
+  mfma_drain();  // the zero writes land before the first MFMA reads them
+  // B fragment (activations): pixel lane % 16, channels 8 * (4 s + lane / 16) ..
+  const uint32_t xl = static_cast<uint32_t>(lane & 15), xk = static_cast<uint32_t>(lane >> 4);
+  const uint32_t sw = ((xl >> 2) & 3u) << 1;
+  const uint32_t boff0 = xl * 128u + ((xk ^ sw) << 4);
+  const uint32_t boff1 = xl * 128u + (((4u + xk) ^ sw) << 4);
+  auto ld = [](const uint8_t* q) { return *reinterpret_cast<const bf16x8_t*>(q); };
+
+  // ---- pipeline -------------------------------------------------------------------
+  // Issue order of a wave's vector-memory operations: X(0) W(0) X(1) W(1),
+  // then per chunk j: X(j+2) at its start, W(j+2) once W(j+1) is scattered.
+  const int nch = p.nch;
+  issue_x(0, 0);
+  load_w(0);
+  if (nch > 1) {
+    issue_x(1, 1);
+    wait_vm<8>();  // W(0)
+  } else {
+    wait_vm<0>();
+  }
+  zero_rows(lds + kWOfs);
+#pragma unroll
+  for (int u = 0; u < UPL; ++u) scatter(lds + kWOfs, u);
+  if (nch > 1) {
+    load_w(1);
+    wait_vm<8 + NW>();  // X(0)
+  } else {
+    wait_vm<0>();
+  }
+  lds_barrier();
+
+  // Chunk j as 16 groups of 8 MFMAs (k-step g / 8, output tile g % 8).  The
+  // instruction order is fixed (scheduling barriers): ahead of group g the
+  // wave reads the weight fragment of group g + 1, one activation fragment of
+  // the second k-step and does one piece of building tile j+1 (a zero-fill
+  // store in groups 0-7, a packed unit in groups 8 ..), so those LDS
+  // latencies and the expansion hide behind MFMAs.  M1 / M2: chunks j+1 /
+  // j+2 exist (compile-time, so the steady-state body has no branches).
+  auto chunk = [&](int j, auto m1, auto m2) {
+    constexpr bool more1 = decltype(m1)::value, more2 = decltype(m2)::value;
+    const int xbuf = j % 3;
+    const uint8_t* xb = lds + xbuf * kXBytes + wp * 16384;
+    const uint8_t* wb = lds + kWOfs + (j & 1) * kWBytes + wo * 16384 + lane * 16;
+    uint8_t* tb = lds + kWOfs + ((j + 1) & 1) * kWBytes;
+    if constexpr (more2) issue_x(j + 2, xbuf == 0 ? 2 : xbuf - 1);  // the buffer chunk j-1 used
+    bf16x8_t b0[8], b1[8], af[2];
+#pragma unroll
+    for (int pt = 0; pt < 8; ++pt) b0[pt] = ld(xb + pt * 2048 + boff0);
+    af[0] = ld(wb);
+#pragma unroll
+    for (int g = 0; g < 16; ++g) {
+      const int s = g >> 3, ot = g & 7;
+      if (g + 1 < 16) af[(g + 1) & 1] = ld(wb + ((((g + 1) & 7) * 2 + ((g + 1) >> 3)) * 1024));
+      if (g < 8) b1[g] = ld(xb + g * 2048 + boff1);
+      if constexpr (more1) {
+        if (g < 8) zero_piece(tb, g);
+        if (g == 8) {
+          if constexpr (more2) wait_vm<8>(); else wait_vm<0>();  // W(j+1)
+        }
+        if (g >= 8 && g - 8 < UPL) scatter(tb, g - 8);
+        if constexpr (more2) {
+          if (g == 8 + UPL - 1) load_w(j + 2);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int pt = 0; pt < 8; ++pt) mfma_acc(acc[pt][ot], af[g & 1], s ? b1[pt] : b0[pt]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if constexpr (more1) {
+      if constexpr (more2) wait_vm<8 + NW>(); else wait_vm<0>();  // X(j+1)
+      lds_barrier();
+    }
+  };
+  int j = 0;
+#pragma unroll 1
+  for (; j + 2 < nch; ++j) chunk(j, BoolC<true>{}, BoolC<true>{});
+  if (j + 1 < nch) {
+    chunk(j, BoolC<true>{}, BoolC<false>{});
+    ++j;
+  }
+  chunk(j, BoolC<false>{}, BoolC<false>{});
+
+  // ---- fused epilogue -----------------------------------------------------------
+  // Each wave parks 64 pixels x 128 outputs (fp32) at a time in its own LDS
+  // region and reads them back by pixel rows: a lane then owns 4 consecutive
+  // outputs of one pixel (32 lanes cover the wave's 128), applies
+  // scale / bias / residual / ReLU in fp32, rounds once and stores.
+  mfma_drain();    // the last MFMAs have written acc
+#pragma unroll
+  for (int pt = 0; pt < 8; ++pt)
+#pragma unroll
+    for (int ot = 0; ot < 8; ++ot) acc_fence(acc[pt][ot]);
+  lds_barrier();  // every wave is done with the operand buffers
+  constexpr uint32_t ysz = sizeof(YT);
+  const __amdgpu_buffer_rsrc_t yr =
+      __builtin_amdgcn_make_buffer_rsrc(p.Y, (short)0, static_cast<int>(p.y_bytes), kRsrcWord3);
+  const __amdgpu_buffer_rsrc_t rsr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(p.residual), (short)0, p.residual ? static_cast<int>(p.y_bytes) : 0, kRsrcWord3);
+  const uint32_t o = ob * kTile + static_cast<uint32_t>(wo * 128 + 4 * (lane & 31));
+  f32x4_t sc{1.f, 1.f, 1.f, 1.f}, bi{0.f, 0.f, 0.f, 0.f};
+  if (p.scale) sc = *reinterpret_cast<const f32x4_t*>(p.scale + o);
+  if (p.bias) bi = *reinterpret_cast<const f32x4_t*>(p.bias + o);
+  uint8_t* stg = lds + w * 64 * kEpPitch;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+#pragma unroll
+    for (int pt = 0; pt < 4; ++pt)
+#pragma unroll
+      for (int ot = 0; ot < 8; ++ot)
+        *reinterpret_cast<f32x4_t*>(stg + (pt * 16 + (lane & 15)) * kEpPitch + (ot * 16 + 4 * (lane >> 4)) * 4) =
+            acc[4 * h + pt][ot];
+#pragma unroll 4
+    for (int rr = 0; rr < 32; ++rr) {
+      const int row = 2 * rr + (lane >> 5);
+      f32x4_t y = *reinterpret_cast<const f32x4_t*>(stg + row * kEpPitch + (lane & 31) * 16);
+      const uint32_t px = pb * kTile + static_cast<uint32_t>(wp * 128 + h * 64 + row);
+      const uint32_t off = px < static_cast<uint32_t>(p.N) ? (px * static_cast<uint32_t>(p.O) + o) * ysz : kOOB;
+      y = y * sc + bi;
+      if (p.residual) {
+        if constexpr (ysz == 2) {
+          const u32x2_t r = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(rsr, off, 0, 0));
+          y[0] += __uint_as_float(r[0] << 16);
+          y[1] += __uint_as_float(r[0] & 0xffff0000u);
+          y[2] += __uint_as_float(r[1] << 16);
+          y[3] += __uint_as_float(r[1] & 0xffff0000u);
+        } else {
+          y += __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rsr, off, 0, 0));
+        }
+      }
+      if (p.relu) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) y[e] = y[e] > 0.0f ? y[e] : (y[e] != y[e] ? y[e] : 0.0f);
+      }
+      if constexpr (ysz == 2) {
+        // v_cvt_pk_bf16_f32: round to nearest even
+        const u32x2_t pk = {__builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{y[0], y[1]}), bf16x2_t)),
+                            __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{y[2], y[3]}), bf16x2_t))};
+        __builtin_amdgcn_raw_buffer_store_b64(
+            __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b64(yr, 0, 0, 0)), pk), yr, off, 0, 0);
+      } else {
+        __builtin_amdgcn_raw_buffer_store_b128(
+            __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b128(yr, 0, 0, 0)), y), yr, off, 0, 0);
+      }
+    }
+  }
+}
+
+// Rows of X are pixels: FC, or a 1x1 convolution with unit stride and no
+// padding over NHWC activations.
+bool plain_rows(const ProductArgs& a) {
+  if (!a.conv) return true;
+  const ConvGeom& g = a.geom;
+  return g.KH == 1 && g.KW == 1 && g.sh == 1 && g.sw == 1 && g.ph == 0 && g.pw == 0;
+}
+
+int units_per_lane(int G, int K) { return (8 * K + G - 1) / G; }
+
+template <typename YT, int UPL, bool FULL>
+hipError_t launch_wu(const WParams& p, uint32_t grid, hipStream_t s) {
+  static const hipError_t attr = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(&wide_tile_kernel<YT, UPL, FULL>), hipFuncAttributeMaxDynamicSharedMemorySize, kLds);
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL((wide_tile_kernel<YT, UPL, FULL>), dim3(grid), dim3(kThreads), kLds, s, p);
+  return hipGetLastError();
+}
+
+template <typename YT>
+hipError_t launch_wy(const WParams& p, uint32_t grid, hipStream_t s) {
+  if (p.K == p.G) return launch_wu<YT, 8, true>(p, grid, s);
+  switch (units_per_lane(p.G, p.K)) {
+    case 1: return launch_wu<YT, 1, false>(p, grid, s);
+    case 2: return launch_wu<YT, 2, false>(p, grid, s);
+    case 3:
+    case 4: return launch_wu<YT, 4, false>(p, grid, s);
+    default: return launch_wu<YT, 8, false>(p, grid, s);
+  }
+}
+
+}  // namespace
+
+bool wide_tile_supports(const ProductArgs& a) {
+  if (a.x_t != DType::BF16 || a.val_t != DType::BF16) return false;
+  if (!plain_rows(a)) return false;
+  if (a.G < 1 || a.G > 64 || 64 % a.G != 0 || a.K < 1 || a.K > a.G) return false;
+  if (a.C % kCK != 0 || a.O % kTile != 0 || a.N < 1) return false;
+  const auto al = [](const void* q, uintptr_t m) { return (reinterpret_cast<uintptr_t>(q) & (m - 1)) == 0; };
+  if (!al(a.X, 16) || !al(a.vals, 16) || !al(a.idx, 8) || !al(a.Y, 16)) return false;
+  if ((a.scale && !al(a.scale, 16)) || (a.bias && !al(a.bias, 16)) || (a.residual && !al(a.residual, 16)))
+    return false;
+  // every buffer offset is 32-bit and stays below the out-of-range marker
+  const int64_t lim = static_cast<int64_t>(kOOB);
+  const int64_t packed = (a.O / a.G) * a.K * a.C;
+  if (a.N * a.C * 2 >= lim || packed * 2 >= lim || a.N * a.O * (a.y_t == DType::F32 ? 4 : 2) >= lim) return false;
+  return true;
+}
+
+hipError_t launch_wide_tile(const ProductArgs& a, hipStream_t s) {
+  if (!wide_tile_supports(a)) return hipErrorInvalidConfiguration;
+  WParams p{};
+  p.X = static_cast<const uint16_t*>(a.X);
+  p.vals = static_cast<const uint16_t*>(a.vals);
+  p.idx = a.idx;
+  p.scale = a.scale;
+  p.bias = a.bias;
+  p.residual = a.residual;
+  p.Y = a.Y;
+  const int64_t ysz = a.y_t == DType::F32 ? 4 : 2;
+  const int64_t packed = (a.O / a.G) * a.K * a.C;
+  p.x_bytes = static_cast<uint32_t>(a.N * a.C * 2);
+  p.v_bytes = static_cast<uint32_t>(packed * 2);
+  p.i_bytes = static_cast<uint32_t>(packed);
+  p.y_bytes = static_cast<uint32_t>(a.N * a.O * ysz);
+  p.N = static_cast<int32_t>(a.N);
+  p.C = static_cast<int32_t>(a.C);
+  p.O = static_cast<int32_t>(a.O);
+  p.G = a.G;
+  p.K = a.K;
+  p.relu = a.relu;
+  p.npb = static_cast<int32_t>((a.N + kTile - 1) / kTile);
+  p.nob = static_cast<int32_t>(a.O / kTile);
+  p.nch = static_cast<int32_t>(a.C / kCK);
+  p.rows_w = 64 * a.K / a.G;
+  const int64_t grid = static_cast<int64_t>(p.npb) * p.nob;
+  if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
+  p.grid8 = grid % 8 == 0 ? static_cast<int32_t>(grid / 8) : 0;
+  const uint32_t g = static_cast<uint32_t>(grid);
+  return a.y_t == DType::BF16 ? launch_wy<bf16_t>(p, g, s) : launch_wy<float>(p, g, s);
+}
+
+}  // namespace cci

@@ -74,6 +74,19 @@ def test_explicit_algo_requirements():
                         cci.BF16, cci.ALGO_SPARSE_MAC, None) == cci.EUNSUPPORTED
     assert lib.cci_spmm(FAKE, cci.BF16, 4, 64, FAKE, cci.BF16, FAKE, 16, 8, 2, None, FAKE,
                         cci.BF16, 9, None) == cci.EINVAL
+    # wide-tile MFMA: O % 256, C % 64, 64 % G, bf16 only; strided / padded / k x k convs refused
+    W = cci.ALGO_WIDE_TILE_MFMA
+    assert lib.cci_spmm(FAKE, cci.BF16, 4, 64, FAKE, cci.BF16, FAKE, 128, 8, 2, None, FAKE,
+                        cci.BF16, W, None) == cci.EUNSUPPORTED
+    assert lib.cci_spmm(FAKE, cci.BF16, 4, 96, FAKE, cci.BF16, FAKE, 256, 8, 2, None, FAKE,
+                        cci.BF16, W, None) == cci.EUNSUPPORTED
+    assert lib.cci_spmm(FAKE, cci.F32, 4, 64, FAKE, cci.F32, FAKE, 256, 8, 2, None, FAKE,
+                        cci.F32, W, None) == cci.EUNSUPPORTED
+    assert lib.cci_spmm(FAKE, cci.BF16, 4, 64, FAKE, cci.BF16, FAKE, 256, 128, 2, None, FAKE,
+                        cci.BF16, W, None) == cci.EUNSUPPORTED
+    for KH, sh, ph in [(3, 1, 1), (1, 2, 0), (1, 1, 1)]:
+        assert lib.cci_conv_im2col(FAKE, cci.BF16, 1, 8, 8, 64, KH, KH, sh, sh, ph, ph, FAKE, cci.BF16,
+                                   FAKE, 256, 8, 2, None, FAKE, cci.BF16, W, None) == cci.EUNSUPPORTED
 
 
 def test_empty_is_a_noop():

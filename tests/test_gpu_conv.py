@@ -70,6 +70,15 @@ def test_conv_bf16(B, H, W, Cin, O, k, stride, pad, G, K, algo):
     run_conv(X, rand_w(O, k * k * Cin, O + k), G, K, k, stride, pad, torch.bfloat16, algo)
 
 
+@pytest.mark.parametrize("B,H,W,Cin,O,G,K", [(2, 14, 14, 128, 256, 16, 4), (3, 9, 13, 64, 512, 8, 2)])
+def test_conv1x1_wide_tile(B, H, W, Cin, O, G, K):
+    """Stride-1 unpadded 1x1 convolution on the wide-tile kernels (pixels are X rows)."""
+    need_gpu()
+    X = rand_x((B, H, W, Cin), torch.bfloat16, B * H + Cin)
+    ep = rand_epilogue(O, B * H * W, torch.bfloat16, 8, residual=True, relu=True)
+    run_conv(X, rand_w(O, Cin, O + 1), G, K, 1, 1, 0, torch.bfloat16, "wide_tile_mfma", ep=ep)
+
+
 @pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma"])
 def test_conv_epilogue_residual_relu(algo):
     need_gpu()

@@ -62,18 +62,43 @@ def test_spmm_bf16(N, C, O, G, K, algo):
     run_case(rand_x(N, C, torch.bfloat16, N + C), rand_w(O, C, O + G), G, K, torch.bfloat16, algo)
 
 
-@pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma"])
+WIDE_CASES = [  # N, C, O, G, K: chunks 1..5, ragged pixel blocks, every unit count, K == G
+    (600, 256, 512, 8, 2), (300, 128, 256, 16, 1), (257, 64, 256, 16, 4), (1000, 320, 256, 4, 3),
+    (512, 192, 768, 16, 16), (100, 256, 256, 64, 7), (2065, 128, 256, 2, 1), (1024, 128, 1024, 8, 2),
+    (2048, 64, 256, 32, 9),
+]
+
+
+@pytest.mark.parametrize("N,C,O,G,K", WIDE_CASES)
+def test_spmm_bf16_wide_tile(N, C, O, G, K):
+    need_gpu()
+    run_case(rand_x(N, C, torch.bfloat16, N + C), rand_w(O, C, O + G), G, K, torch.bfloat16, "wide_tile_mfma")
+
+
+def test_spmm_wide_tile_repeat_is_identical():
+    """Two launches on the same inputs give the same bytes (no state carried between launches)."""
+    need_gpu()
+    from paper_1910_11971_amd import cci
+    X = rand_x(700, 256, torch.bfloat16, 3).to(DEV)
+    vals, idx = cci.pack(torch.from_numpy(rand_w(512, 256, 4)).to(DEV), 8, 2, torch.bfloat16)
+    Y1 = cci.spmm(X, vals, idx, 8, algo="wide_tile_mfma")
+    Y2 = cci.spmm(X, vals, idx, 8, algo="wide_tile_mfma")
+    torch.cuda.synchronize()
+    assert torch.equal(Y1.view(torch.int16), Y2.view(torch.int16))
+
+
+@pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma", "wide_tile_mfma"])
 def test_spmm_bf16_in_f32_out_with_epilogue(algo):
     need_gpu()
-    N, C, O, G, K = 777, 128, 128, 8, 2
+    N, C, O, G, K = 777, 128, 256, 8, 2
     ep = rand_epilogue(O, N, torch.float32, 3, residual=True, relu=True)
     run_case(rand_x(N, C, torch.bfloat16, 1), rand_w(O, C, 2), G, K, torch.float32, algo, ep=ep)
 
 
-@pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma"])
+@pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma", "wide_tile_mfma"])
 def test_spmm_bf16_epilogue_bf16_residual(algo):
     need_gpu()
-    N, C, O, G, K = 300, 64, 64, 16, 4
+    N, C, O, G, K = 300, 64, 256, 16, 4
     ep = rand_epilogue(O, N, torch.bfloat16, 4, residual=True, relu=True)
     run_case(rand_x(N, C, torch.bfloat16, 5), rand_w(O, C, 6), G, K, torch.bfloat16, algo, ep=ep)
 
@@ -103,7 +128,7 @@ def sample_rows(N, n, seed):
     return np.unique(np.concatenate([[0, 1, N // 2, N - 2, N - 1], rng.integers(0, N, n)]))
 
 
-@pytest.mark.parametrize("algo", ["auto", "sparse_mac"])
+@pytest.mark.parametrize("algo", ["auto", "sparse_mac", "dense_tile_mfma", "wide_tile_mfma"])
 @pytest.mark.parametrize("K", [1, 2, 4, 8, 16])
 def test_spmm_fc4096_full_size_sampled(K, algo):
     """FC sweep at full size (4096^3, G=16), sampled rows vs the oracle."""

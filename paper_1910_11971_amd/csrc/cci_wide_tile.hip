@@ -49,7 +49,7 @@ constexpr int kXBytes = kTile * kCK * 2;        // one activation buffer
 constexpr int kWBytes = kTile * kCK * 2;        // one weight tile
 constexpr int kWOfs = 3 * kXBytes;              // weight tiles follow the three activation buffers
 constexpr int kLds = kWOfs + 2 * kWBytes;       // 160 KiB
-constexpr int kEpPitch = 128 * 4 + 32;          // epilogue staging: bytes per pixel row
+constexpr int kEpPitch = 128 * 4 + 16;          // epilogue staging: bytes per pixel row
 constexpr uint32_t kOOB = 0x80000000u;          // buffer offset that reads as zero / drops a store
 constexpr int kRsrcWord3 = 0x00020000;          // raw buffer descriptor word 3 (gfx9 family)
 static_assert(kLds <= 160 * 1024, "LDS budget");
@@ -148,6 +148,10 @@ void wide_tile_kernel(WParams p) {
     const uint32_t k8 = static_cast<uint32_t>(lane & 7) ^ (((q >> 2) & 3u) << 1);
     xoff[i] = px < static_cast<uint32_t>(p.N) ? px * static_cast<uint32_t>(p.C) * 2u + k8 * 16u : kOOB;
   }
+  auto issue_x_one = [&](int ch, int buf, int i) {
+    lds_void_t* d = (lds_void_t*)(lds + buf * kXBytes + w * 8192 + i * 1024);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, d, 16, xoff[i] + static_cast<uint32_t>(ch) * (kCK * 2), 0, 0, 0);
+  };
   auto issue_x = [&](int ch, int buf) {
     uint8_t* dst = lds + buf * kXBytes + w * 8192;
     const uint32_t co = static_cast<uint32_t>(ch) * (kCK * 2);
@@ -187,15 +191,45 @@ void wide_tile_kernel(WParams p) {
         pi[u] = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(ir, ioff[u] + static_cast<uint32_t>(ch) * kCK, 0, 0));
     }
   };
-  // Building a tile: wave w zeroes its 64 rows (8 stores of 16 bytes per
-  // lane), then writes its kept weights; program order puts the zero fill
-  // first and no other wave touches these rows.
+  // Building a tile.  The two tiles are zeroed once.  K == G: a build
+  // overwrites every entry.  K <= G / 4 (UNSC): a build first clears only
+  // the entries the build two chunks earlier (same tile) wrote, then writes
+  // its own.  Otherwise it zeroes its rows, then writes.  All clears of a
+  // build are issued before its writes, so across lanes a clear never lands
+  // after a write.  Wave w owns tile rows [64 w, 64 w + 64) in every step.
+  constexpr bool UNSC = !FULL && UPL <= 2;
+  u32x2_t pold1[UPL], pold2[UPL];  // indices of the last two builds (UNSC)
+#pragma unroll
+  for (int u = 0; u < UPL; ++u) pold1[u] = pold2[u] = u32x2_t{0u, 0u};
   auto zero_piece = [&](uint8_t* tb, int i) {
-    if constexpr (!FULL) *reinterpret_cast<u32x4_t*>(tb + w * 8192 + (i * 64 + lane) * 16) = u32x4_t{0u, 0u, 0u, 0u};
+    *reinterpret_cast<u32x4_t*>(tb + w * 8192 + (i * 64 + lane) * 16) = u32x4_t{0u, 0u, 0u, 0u};
   };
   auto zero_rows = [&](uint8_t* tb) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) zero_piece(tb, i);
+  };
+  auto unscatter = [&](uint8_t* tb, int u) {  // clear what pold2[u] (two builds ago) wrote
+    if constexpr (UNSC) {
+      if (!uok[u]) return;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t rr = (pold2[u][e >> 2] >> (8 * (e & 3))) & 0xffu;
+        *reinterpret_cast<uint16_t*>(tb + ubase[u] + trow(rr) + 2 * e) = 0;
+      }
+    }
+  };
+  auto unscatter_e = [&](uint8_t* tb, int u, int e) {  // element e of unscatter(tb, u)
+    if (!uok[u]) return;
+    const uint32_t rr = (pold2[u][e >> 2] >> (8 * (e & 3))) & 0xffu;
+    *reinterpret_cast<uint16_t*>(tb + ubase[u] + trow(rr) + 2 * e) = 0;
+  };
+  auto scatter_e = [&](uint8_t* tb, int u, int e) {  // element e of scatter(tb, u), K < G
+    if (!uok[u]) return;
+    const uint32_t rr = (pi[u][e >> 2] >> (8 * (e & 3))) & 0xffu;
+    *reinterpret_cast<uint16_t*>(tb + ubase[u] + trow(rr) + 2 * e) = static_cast<uint16_t>(pv[u][e >> 1] >> (16 * (e & 1)));
+  };
+  auto scatter_full = [&](uint8_t* tb, int u) {  // K == G: the unit's 16 bytes
+    if (uok[u]) *reinterpret_cast<u32x4_t*>(tb + ubase[u]) = pv[u];
   };
   auto scatter = [&](uint8_t* tb, int u) {
     if (!uok[u]) return;
@@ -207,6 +241,15 @@ void wide_tile_kernel(WParams p) {
         const uint32_t rr = (pi[u][e >> 2] >> (8 * (e & 3))) & 0xffu;  // row within the group
         *reinterpret_cast<uint16_t*>(tb + ubase[u] + trow(rr) + 2 * e) =
             static_cast<uint16_t>(pv[u][e >> 1] >> (16 * (e & 1)));
+      }
+    }
+  };
+  auto rotate_idx = [&]() {
+    if constexpr (UNSC) {
+#pragma unroll
+      for (int u = 0; u < UPL; ++u) {
+        pold2[u] = pold1[u];
+        pold1[u] = pi[u];
       }
     }
   };
@@ -232,85 +275,141 @@ void wide_tile_kernel(WParams p) {
   auto ld = [](const uint8_t* q) { return *reinterpret_cast<const bf16x8_t*>(q); };
 
   // ---- pipeline -------------------------------------------------------------------
-  // Issue order of a wave's vector-memory operations: X(0) W(0) X(1) W(1),
-  // then per chunk j: X(j+2) at its start, W(j+2) once W(j+1) is scattered.
+  // A wave's vector-memory operations are issued in the order X(0) W(0) X(1)
+  // W(1) X(2), then per chunk j: W(j+2) (group 7) and X(j+3) (groups 8-11,
+  // into the buffer chunk j has just released).  Loads complete in issue
+  // order, so "X(c) has landed" is "at most <ops issued after it> in flight".
   const int nch = p.nch;
   issue_x(0, 0);
   load_w(0);
-  if (nch > 1) {
-    issue_x(1, 1);
-    wait_vm<8>();  // W(0)
-  } else {
-    wait_vm<0>();
-  }
+  if (nch > 1) issue_x(1, 1);
+  if (nch > 1) wait_vm<8>(); else wait_vm<0>();  // W(0)
   zero_rows(lds + kWOfs);
+  zero_rows(lds + kWOfs + kWBytes);
 #pragma unroll
   for (int u = 0; u < UPL; ++u) scatter(lds + kWOfs, u);
-  if (nch > 1) {
-    load_w(1);
-    wait_vm<8 + NW>();  // X(0)
-  } else {
-    wait_vm<0>();
-  }
+  rotate_idx();
+  if (nch > 1) load_w(1);
+  if (nch > 2) issue_x(2, 2);
+  if (nch > 2) wait_vm<16 + NW>(); else if (nch > 1) wait_vm<8 + NW>(); else wait_vm<0>();  // X(0)
   lds_barrier();
 
-  // Chunk j as 16 groups of 8 MFMAs (k-step g / 8, output tile g % 8).  The
-  // instruction order is fixed (scheduling barriers): ahead of group g the
-  // wave reads the weight fragment of group g + 1, one activation fragment of
-  // the second k-step and does one piece of building tile j+1 (a zero-fill
-  // store in groups 0-7, a packed unit in groups 8 ..), so those LDS
-  // latencies and the expansion hide behind MFMAs.  M1 / M2: chunks j+1 /
-  // j+2 exist (compile-time, so the steady-state body has no branches).
-  auto chunk = [&](int j, auto m1, auto m2) {
-    constexpr bool more1 = decltype(m1)::value, more2 = decltype(m2)::value;
+  // Chunk j is 16 groups of 8 MFMAs: group g multiplies k-step g / 8 by
+  // output tile g % 8 against the wave's 8 pixel tiles.  Fragments sit in
+  // registers well before use: af[g] holds the weight fragment of group g,
+  // b0 / b1 the activation fragments of k-step 0 / 1.  The barrier of chunk
+  // j sits between groups 7 and 8; the instruction order is fixed with
+  // scheduling barriers:
+  //   groups 0-7: read b1[g] and af[g + 8] (the rest of chunk j, so after
+  //     the barrier no wave reads chunk j's buffers); build tile j+1: clear
+  //     (groups 0-3), write W(j+1) (groups 4-7); then load W(j+2);
+  //   barrier: X(j+1) has landed and tile j+1 is complete in every wave;
+  //   groups 8-15: DMA X(j+3) into chunk j's buffer (two per group, groups
+  //     8-11), read chunk j+1's b0 (two per group, groups 8-11) and
+  //     af[g - 8] from the new buffers.
+  // Every fragment read is issued at least four groups (~500 cycles of
+  // MFMAs) before its use.  M1 / M2 / M3: chunks j+1 / j+2 / j+3 exist
+  // (compile-time, so the steady-state body has no branches).
+  bf16x8_t b0[8], b1[8], af[16];
+  auto read_first = [&](int j) {  // chunk j's k-step-0 fragments
+    const uint8_t* xb = lds + (j % 3) * kXBytes + wp * 16384;
+    const uint8_t* wb = lds + kWOfs + (j & 1) * kWBytes + wo * 16384 + lane * 16;
+#pragma unroll
+    for (int pt = 0; pt < 8; ++pt) b0[pt] = ld(xb + pt * 2048 + boff0);
+#pragma unroll
+    for (int g = 0; g < 8; ++g) af[g] = ld(wb + g * 2048);
+  };
+  constexpr int kUPG = (UPL + 3) / 4;  // packed units per group (groups 0-3 clear, 4-7 write)
+  auto chunk = [&](int j, auto m1, auto m2, auto m3) {
+    constexpr bool more1 = decltype(m1)::value, more2 = decltype(m2)::value, more3 = decltype(m3)::value;
     const int xbuf = j % 3;
     const uint8_t* xb = lds + xbuf * kXBytes + wp * 16384;
     const uint8_t* wb = lds + kWOfs + (j & 1) * kWBytes + wo * 16384 + lane * 16;
-    uint8_t* tb = lds + kWOfs + ((j + 1) & 1) * kWBytes;
-    if constexpr (more2) issue_x(j + 2, xbuf == 0 ? 2 : xbuf - 1);  // the buffer chunk j-1 used
-    bf16x8_t b0[8], b1[8], af[2];
-#pragma unroll
-    for (int pt = 0; pt < 8; ++pt) b0[pt] = ld(xb + pt * 2048 + boff0);
-    af[0] = ld(wb);
+    const int xnb = xbuf == 2 ? 0 : xbuf + 1;
+    const uint8_t* xn = lds + xnb * kXBytes + wp * 16384;  // chunk j+1
+    const uint8_t* wn = lds + kWOfs + ((j + 1) & 1) * kWBytes + wo * 16384 + lane * 16;
+    uint8_t* tb = lds + kWOfs + ((j + 1) & 1) * kWBytes;  // tile j+1, built here
 #pragma unroll
     for (int g = 0; g < 16; ++g) {
-      const int s = g >> 3, ot = g & 7;
-      if (g + 1 < 16) af[(g + 1) & 1] = ld(wb + ((((g + 1) & 7) * 2 + ((g + 1) >> 3)) * 1024));
-      if (g < 8) b1[g] = ld(xb + g * 2048 + boff1);
       if constexpr (more1) {
-        if (g < 8) zero_piece(tb, g);
-        if (g == 8) {
+        if (g == 4) {
           if constexpr (more2) wait_vm<8>(); else wait_vm<0>();  // W(j+1)
         }
-        if (g >= 8 && g - 8 < UPL) scatter(tb, g - 8);
-        if constexpr (more2) {
-          if (g == 8 + UPL - 1) load_w(j + 2);
+        if (g == 8) {
+          if constexpr (more2) wait_vm<8 + 2 * NW>(); else wait_vm<0>();  // X(j+1)
+          lds_barrier();
         }
       }
-      __builtin_amdgcn_sched_barrier(0);
+      // One wave per SIMD issues in order, so other work overlaps an MFMA
+      // only when it sits between two of them: slot i follows MFMA i.
 #pragma unroll
-      for (int pt = 0; pt < 8; ++pt) mfma_acc(acc[pt][ot], af[g & 1], s ? b1[pt] : b0[pt]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    if constexpr (more1) {
-      if constexpr (more2) wait_vm<8 + NW>(); else wait_vm<0>();  // X(j+1)
-      lds_barrier();
+      for (int i = 0; i < 8; ++i) {
+        mfma_acc(acc[i][g & 7], af[g], g < 8 ? b0[i] : b1[i]);
+        __builtin_amdgcn_sched_barrier(0);
+        if (g < 8) {
+          if (i == 0) b1[g] = ld(xb + g * 2048 + boff1);
+          if (i == 1) af[g + 8] = ld(wb + (g * 2 + 1) * 1024);
+          if constexpr (more1) {
+            if constexpr (FULL) {
+              if (g >= 4 && i >= 2 && i < 2 + kUPG) scatter_full(tb, (g - 4) * kUPG + (i - 2));
+            } else {
+              if constexpr (!UNSC) {
+                if (g < 4 && (i == 2 || i == 3)) zero_piece(tb, 2 * g + (i - 2));
+              }
+#pragma unroll
+              for (int k = 0; k < kUPG; ++k) {
+                const int u = (g & 3) * kUPG + k;
+                if (u < UPL) {
+                  if (g < 4) {
+                    if constexpr (UNSC) unscatter_e(tb, u, i);
+                  } else {
+                    scatter_e(tb, u, i);
+                  }
+                }
+              }
+            }
+            if (g == 7 && i == 7) {
+              rotate_idx();
+              if constexpr (more2) load_w(j + 2);
+            }
+          }
+        } else if constexpr (more1) {
+          if (g < 12) {
+            if constexpr (more3) {
+              if (i == 0) {
+                issue_x_one(j + 3, xbuf, 2 * (g - 8));
+                issue_x_one(j + 3, xbuf, 2 * (g - 8) + 1);
+              }
+            }
+            if (i == 1) b0[2 * (g - 8)] = ld(xn + (2 * (g - 8)) * 2048 + boff0);
+            if (i == 2) b0[2 * (g - 8) + 1] = ld(xn + (2 * (g - 8) + 1) * 2048 + boff0);
+          }
+          if (i == 3) af[g - 8] = ld(wn + (g - 8) * 2048);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
   };
+  read_first(0);
   int j = 0;
 #pragma unroll 1
-  for (; j + 2 < nch; ++j) chunk(j, BoolC<true>{}, BoolC<true>{});
-  if (j + 1 < nch) {
-    chunk(j, BoolC<true>{}, BoolC<false>{});
+  for (; j + 3 < nch; ++j) chunk(j, BoolC<true>{}, BoolC<true>{}, BoolC<true>{});
+  if (j + 2 < nch) {
+    chunk(j, BoolC<true>{}, BoolC<true>{}, BoolC<false>{});
     ++j;
   }
-  chunk(j, BoolC<false>{}, BoolC<false>{});
+  if (j + 1 < nch) {
+    chunk(j, BoolC<true>{}, BoolC<false>{}, BoolC<false>{});
+    ++j;
+  }
+  chunk(j, BoolC<false>{}, BoolC<false>{}, BoolC<false>{});
 
   // ---- fused epilogue -----------------------------------------------------------
   // Each wave parks 64 pixels x 128 outputs (fp32) at a time in its own LDS
-  // region and reads them back by pixel rows: a lane then owns 4 consecutive
-  // outputs of one pixel (32 lanes cover the wave's 128), applies
-  // scale / bias / residual / ReLU in fp32, rounds once and stores.
+  // region (pitch 528 bytes: the read-back below is conflict-free) and
+  // reads them back by pixel rows: a lane then owns 8 consecutive outputs
+  // of one pixel (16 lanes cover the wave's 128), applies scale / bias /
+  // residual / ReLU in fp32, rounds once and stores 16 (bf16) or 32 bytes.
   mfma_drain();    // the last MFMAs have written acc
 #pragma unroll
   for (int pt = 0; pt < 8; ++pt)
@@ -322,10 +421,17 @@ void wide_tile_kernel(WParams p) {
       __builtin_amdgcn_make_buffer_rsrc(p.Y, (short)0, static_cast<int>(p.y_bytes), kRsrcWord3);
   const __amdgpu_buffer_rsrc_t rsr = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<void*>(p.residual), (short)0, p.residual ? static_cast<int>(p.y_bytes) : 0, kRsrcWord3);
-  const uint32_t o = ob * kTile + static_cast<uint32_t>(wo * 128 + 4 * (lane & 31));
-  f32x4_t sc{1.f, 1.f, 1.f, 1.f}, bi{0.f, 0.f, 0.f, 0.f};
-  if (p.scale) sc = *reinterpret_cast<const f32x4_t*>(p.scale + o);
-  if (p.bias) bi = *reinterpret_cast<const f32x4_t*>(p.bias + o);
+  const int c8 = lane & 15;  // 8-output block of the wave's 128
+  const uint32_t o = ob * kTile + static_cast<uint32_t>(wo * 128 + 8 * c8);
+  f32x4_t sc0{1.f, 1.f, 1.f, 1.f}, sc1{1.f, 1.f, 1.f, 1.f}, bi0{0.f, 0.f, 0.f, 0.f}, bi1{0.f, 0.f, 0.f, 0.f};
+  if (p.scale) {
+    sc0 = *reinterpret_cast<const f32x4_t*>(p.scale + o);
+    sc1 = *reinterpret_cast<const f32x4_t*>(p.scale + o + 4);
+  }
+  if (p.bias) {
+    bi0 = *reinterpret_cast<const f32x4_t*>(p.bias + o);
+    bi1 = *reinterpret_cast<const f32x4_t*>(p.bias + o + 4);
+  }
   uint8_t* stg = lds + w * 64 * kEpPitch;
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
@@ -335,37 +441,52 @@ void wide_tile_kernel(WParams p) {
       for (int ot = 0; ot < 8; ++ot)
         *reinterpret_cast<f32x4_t*>(stg + (pt * 16 + (lane & 15)) * kEpPitch + (ot * 16 + 4 * (lane >> 4)) * 4) =
             acc[4 * h + pt][ot];
-#pragma unroll 4
-    for (int rr = 0; rr < 32; ++rr) {
-      const int row = 2 * rr + (lane >> 5);
-      f32x4_t y = *reinterpret_cast<const f32x4_t*>(stg + row * kEpPitch + (lane & 31) * 16);
+#pragma unroll 2
+    for (int rr = 0; rr < 16; ++rr) {
+      const int row = 4 * rr + (lane >> 4);
+      const uint8_t* src = stg + row * kEpPitch + c8 * 32;
+      f32x4_t y0 = *reinterpret_cast<const f32x4_t*>(src);
+      f32x4_t y1 = *reinterpret_cast<const f32x4_t*>(src + 16);
       const uint32_t px = pb * kTile + static_cast<uint32_t>(wp * 128 + h * 64 + row);
       const uint32_t off = px < static_cast<uint32_t>(p.N) ? (px * static_cast<uint32_t>(p.O) + o) * ysz : kOOB;
-      y = y * sc + bi;
+      y0 = y0 * sc0 + bi0;
+      y1 = y1 * sc1 + bi1;
       if (p.residual) {
         if constexpr (ysz == 2) {
-          const u32x2_t r = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(rsr, off, 0, 0));
-          y[0] += __uint_as_float(r[0] << 16);
-          y[1] += __uint_as_float(r[0] & 0xffff0000u);
-          y[2] += __uint_as_float(r[1] << 16);
-          y[3] += __uint_as_float(r[1] & 0xffff0000u);
+          const u32x4_t r = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rsr, off, 0, 0));
+          y0[0] += __uint_as_float(r[0] << 16);
+          y0[1] += __uint_as_float(r[0] & 0xffff0000u);
+          y0[2] += __uint_as_float(r[1] << 16);
+          y0[3] += __uint_as_float(r[1] & 0xffff0000u);
+          y1[0] += __uint_as_float(r[2] << 16);
+          y1[1] += __uint_as_float(r[2] & 0xffff0000u);
+          y1[2] += __uint_as_float(r[3] << 16);
+          y1[3] += __uint_as_float(r[3] & 0xffff0000u);
         } else {
-          y += __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rsr, off, 0, 0));
+          y0 += __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rsr, off, 0, 0));
+          y1 += __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rsr, off + 16, 0, 0));
         }
       }
       if (p.relu) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) y[e] = y[e] > 0.0f ? y[e] : (y[e] != y[e] ? y[e] : 0.0f);
+        for (int e = 0; e < 4; ++e) {
+          y0[e] = y0[e] > 0.0f ? y0[e] : (y0[e] != y0[e] ? y0[e] : 0.0f);
+          y1[e] = y1[e] > 0.0f ? y1[e] : (y1[e] != y1[e] ? y1[e] : 0.0f);
+        }
       }
       if constexpr (ysz == 2) {
         // v_cvt_pk_bf16_f32: round to nearest even
-        const u32x2_t pk = {__builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{y[0], y[1]}), bf16x2_t)),
-                            __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{y[2], y[3]}), bf16x2_t))};
-        __builtin_amdgcn_raw_buffer_store_b64(
-            __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b64(yr, 0, 0, 0)), pk), yr, off, 0, 0);
+        const u32x4_t pk = {__builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{y0[0], y0[1]}), bf16x2_t)),
+                            __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{y0[2], y0[3]}), bf16x2_t)),
+                            __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{y1[0], y1[1]}), bf16x2_t)),
+                            __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{y1[2], y1[3]}), bf16x2_t))};
+        __builtin_amdgcn_raw_buffer_store_b128(
+            __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b128(yr, 0, 0, 0)), pk), yr, off, 0, 0);
       } else {
         __builtin_amdgcn_raw_buffer_store_b128(
-            __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b128(yr, 0, 0, 0)), y), yr, off, 0, 0);
+            __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b128(yr, 0, 0, 0)), y0), yr, off, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b128(
+            __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b128(yr, 0, 0, 0)), y1), yr, off + 16, 0, 0);
       }
     }
   }

@@ -21,11 +21,11 @@
 //
 // LDS layouts (bytes):
 //   activation buffer: pixel q at q * 128; its 16-byte column c holds
-//     channels 8 * (c ^ sw(q)) .. +7 of the chunk, sw(q) = ((q >> 2) & 3) * 2.
+//     channels 8 * (c ^ sw(q)) .. +7 of the chunk, sw(q) = (q >> 1) % 8.
 //     The DMA still reads each pixel's 128 contiguous bytes (one cache line
-//     per 8 lanes); the swizzle makes a fragment read (16 pixels x two
-//     adjacent 8-channel columns per half-wave) touch 32 distinct 16-byte
-//     bank slots.
+//     per 8 lanes); with the swizzle a fragment read (16 pixels, one or two
+//     8-channel columns per 16 / 32 lanes) touches distinct 16-byte bank
+//     slots within every 16 and every 32 lanes.
 //   weight tile: 16-row block b, k-step s at (2 b + s) * 1024, inside it
 //     (k / 8 % 4) * 256 + (o % 16) * 16 + (k % 8) * 2: the fragment a lane
 //     reads is its 16 contiguous bytes at lane * 16.
@@ -101,6 +101,27 @@ __device__ __forceinline__ void mfma_drain() { asm volatile("s_nop 15\n\ts_nop 1
 // the volatile sequence (no code).
 __device__ __forceinline__ void acc_fence(f32x4_t& acc) { asm volatile("" : "+a"(acc)); }
 
+// Packed-weight loads into registers, issued as plain instructions.  The
+// compiler does not track them as pending loads (it cannot count the LDS DMAs
+// issued after them and would wait for every outstanding load); the kernel
+// waits for them itself with wait_vm<> before any use.
+__device__ __forceinline__ u32x4_t sdesc(const void* base, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  const auto rfl = [](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(x))); };
+  return u32x4_t{rfl(static_cast<uint32_t>(a)), rfl(static_cast<uint32_t>(a >> 32) & 0xffffu), rfl(bytes),
+                 static_cast<uint32_t>(kRsrcWord3)};
+}
+__device__ __forceinline__ u32x4_t load_x4(const u32x4_t d, uint32_t off) {
+  u32x4_t v;
+  asm volatile("buffer_load_dwordx4 %0, %1, %2, 0 offen" : "=v"(v) : "v"(off), "s"(d) : "memory");
+  return v;
+}
+__device__ __forceinline__ u32x2_t load_x2(const u32x4_t d, uint32_t off) {
+  u32x2_t v;
+  asm volatile("buffer_load_dwordx2 %0, %1, %2, 0 offen" : "=v"(v) : "v"(off), "s"(d) : "memory");
+  return v;
+}
+
 // Byte offset of tile row o (< 256) in the weight tile, k-column 0.
 __device__ __forceinline__ uint32_t trow(uint32_t o) { return ((o >> 4) << 11) | ((o & 15) << 4); }
 
@@ -130,10 +151,7 @@ void wide_tile_kernel(WParams p) {
 
   const __amdgpu_buffer_rsrc_t xr =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(p.X), (short)0, static_cast<int>(p.x_bytes), kRsrcWord3);
-  const __amdgpu_buffer_rsrc_t vr =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(p.vals), (short)0, static_cast<int>(p.v_bytes), kRsrcWord3);
-  const __amdgpu_buffer_rsrc_t ir =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(p.idx), (short)0, static_cast<int>(p.i_bytes), kRsrcWord3);
+  const u32x4_t vd = sdesc(p.vals, p.v_bytes), id = sdesc(p.idx, p.i_bytes);
 
   // ---- activation DMA --------------------------------------------------------
   // DMA instruction i of wave w fills pixels (8w + i) * 8 .. +8 of a buffer:
@@ -145,7 +163,7 @@ void wide_tile_kernel(WParams p) {
   for (int i = 0; i < 8; ++i) {
     const uint32_t q = static_cast<uint32_t>((8 * w + i) * 8 + (lane >> 3));
     const uint32_t px = pb * kTile + q;
-    const uint32_t k8 = static_cast<uint32_t>(lane & 7) ^ (((q >> 2) & 3u) << 1);
+    const uint32_t k8 = static_cast<uint32_t>(lane & 7) ^ ((q >> 1) & 7u);
     xoff[i] = px < static_cast<uint32_t>(p.N) ? px * static_cast<uint32_t>(p.C) * 2u + k8 * 16u : kOOB;
   }
   auto issue_x_one = [&](int ch, int buf, int i) {
@@ -186,9 +204,8 @@ void wide_tile_kernel(WParams p) {
   auto load_w = [&](int ch) {
 #pragma unroll
     for (int u = 0; u < UPL; ++u) {
-      pv[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(vr, voff[u] + static_cast<uint32_t>(ch) * (kCK * 2), 0, 0));
-      if constexpr (!FULL)
-        pi[u] = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(ir, ioff[u] + static_cast<uint32_t>(ch) * kCK, 0, 0));
+      pv[u] = load_x4(vd, voff[u] + static_cast<uint32_t>(ch) * (kCK * 2));
+      if constexpr (!FULL) pi[u] = load_x2(id, ioff[u] + static_cast<uint32_t>(ch) * kCK);
     }
   };
   // Building a tile.  The two tiles are zeroed once.  K == G: a build
@@ -201,6 +218,13 @@ void wide_tile_kernel(WParams p) {
   u32x2_t pold1[UPL], pold2[UPL];  // indices of the last two builds (UNSC)
 #pragma unroll
   for (int u = 0; u < UPL; ++u) pold1[u] = pold2[u] = u32x2_t{0u, 0u};
+  auto w_fence = [&]() {  // the loaded values are used only after this point
+#pragma unroll
+    for (int u = 0; u < UPL; ++u) {
+      asm volatile("" : "+v"(pv[u]));
+      if constexpr (!FULL) asm volatile("" : "+v"(pi[u]));
+    }
+  };
   auto zero_piece = [&](uint8_t* tb, int i) {
     *reinterpret_cast<u32x4_t*>(tb + w * 8192 + (i * 64 + lane) * 16) = u32x4_t{0u, 0u, 0u, 0u};
   };
@@ -269,7 +293,7 @@ void wide_tile_kernel(WParams p) {
   mfma_drain();  // the zero writes land before the first MFMA reads them
   // B fragment (activations): pixel lane % 16, channels 8 * (4 s + lane / 16) ..
   const uint32_t xl = static_cast<uint32_t>(lane & 15), xk = static_cast<uint32_t>(lane >> 4);
-  const uint32_t sw = ((xl >> 2) & 3u) << 1;
+  const uint32_t sw = (xl >> 1) & 7u;
   const uint32_t boff0 = xl * 128u + ((xk ^ sw) << 4);
   const uint32_t boff1 = xl * 128u + (((4u + xk) ^ sw) << 4);
   auto ld = [](const uint8_t* q) { return *reinterpret_cast<const bf16x8_t*>(q); };
@@ -284,6 +308,7 @@ void wide_tile_kernel(WParams p) {
   load_w(0);
   if (nch > 1) issue_x(1, 1);
   if (nch > 1) wait_vm<8>(); else wait_vm<0>();  // W(0)
+  w_fence();
   zero_rows(lds + kWOfs);
   zero_rows(lds + kWOfs + kWBytes);
 #pragma unroll
@@ -291,7 +316,8 @@ void wide_tile_kernel(WParams p) {
   rotate_idx();
   if (nch > 1) load_w(1);
   if (nch > 2) issue_x(2, 2);
-  if (nch > 2) wait_vm<16 + NW>(); else if (nch > 1) wait_vm<8 + NW>(); else wait_vm<0>();  // X(0)
+  if (nch > 2) wait_vm<8>(); else wait_vm<0>();  // X(0), X(1), W(1)
+  w_fence();
   lds_barrier();
 
   // Chunk j is 16 groups of 8 MFMAs: group g multiplies k-step g / 8 by
@@ -332,9 +358,6 @@ void wide_tile_kernel(WParams p) {
 #pragma unroll
     for (int g = 0; g < 16; ++g) {
       if constexpr (more1) {
-        if (g == 4) {
-          if constexpr (more2) wait_vm<8>(); else wait_vm<0>();  // W(j+1)
-        }
         if (g == 8) {
           if constexpr (more2) wait_vm<8 + 2 * NW>(); else wait_vm<0>();  // X(j+1)
           lds_barrier();
@@ -388,6 +411,12 @@ void wide_tile_kernel(WParams p) {
         }
         __builtin_amdgcn_sched_barrier(0);
       }
+    }
+    // W(j+2) is in registers before the loop carries it on (copies of it
+    // may be made at the loop head)
+    if constexpr (more2) {
+      if constexpr (more3) wait_vm<8>(); else wait_vm<0>();
+      w_fence();
     }
   };
   read_first(0);

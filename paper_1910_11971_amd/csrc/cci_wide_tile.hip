@@ -29,6 +29,8 @@
 //   weight tile: 16-row block b, k-step s at (2 b + s) * 1024, inside it
 //     (k / 8 % 4) * 256 + (o % 16) * 16 + (k % 8) * 2: the fragment a lane
 //     reads is its 16 contiguous bytes at lane * 16.
+#include <type_traits>
+
 #include "cci_launch.hpp"
 
 namespace cci {
@@ -121,13 +123,24 @@ __device__ __forceinline__ u32x2_t load_x2(const u32x4_t d, uint32_t off) {
   asm volatile("buffer_load_dwordx2 %0, %1, %2, 0 offen" : "=v"(v) : "v"(off), "s"(d) : "memory");
   return v;
 }
+__device__ __forceinline__ uint32_t load_x1(const u32x4_t d, uint32_t off) {
+  uint32_t v;
+  asm volatile("buffer_load_dword %0, %1, %2, 0 offen" : "=v"(v) : "v"(off), "s"(d) : "memory");
+  return v;
+}
+
+// Word k of a unit's packed indices.
+__device__ __forceinline__ uint32_t iword(const u32x2_t v, int k) { return v[k]; }
+__device__ __forceinline__ uint32_t iword(uint32_t v, int) { return v; }
 
 // Byte offset of tile row o (< 256) in the weight tile, k-column 0.
 __device__ __forceinline__ uint32_t trow(uint32_t o) { return ((o >> 4) << 11) | ((o & 15) << 4); }
 
-// UPL: packed 8-channel units per lane per chunk (ceil(8 K / G)); FULL: K == G
-// (every entry kept, indices ascending, so a unit is one row's 16 bytes).
-template <typename YT, int UPL, bool FULL>
+// A unit is UE (8 or 4) consecutive channels of one packed row; UPL units
+// per lane per chunk.  FULL: K == G (every entry kept, indices ascending, so
+// a unit is one row's 16 bytes).  BIGG: G > 16 (a group spans 16-row
+// blocks of the tile).
+template <typename YT, int UPL, int UE, bool FULL, bool BIGG>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void wide_tile_kernel(WParams p) {
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
@@ -182,42 +195,56 @@ void wide_tile_kernel(WParams p) {
 
   // ---- packed weights ---------------------------------------------------------
   // Wave w expands tile rows [64 w, 64 w + 64): 64 / G groups, rows_w packed
-  // rows.  Unit u of a lane is packed row r = (lane + 64 u) / 8 of them,
-  // 8-channel block cb = lane % 8 of the chunk (8 lanes read a row's 64
-  // channels contiguously).
+  // rows.  Unit u of a lane is packed row r = (lane + 64 u) * UE / 64 of
+  // them, channels c .. c + UE - 1 of the chunk, c = (lane * UE) % 64 (the
+  // lanes of a row read its 64 channels contiguously).
   uint32_t voff[UPL], ioff[UPL], ubase[UPL];
   bool uok[UPL];
 #pragma unroll
   for (int u = 0; u < UPL; ++u) {
     const int v = lane + 64 * u;
-    const int r = v >> 3, cb = v & 7;
+    const int r = UE == 8 ? v >> 3 : v >> 4;
+    const int c = UE == 8 ? (v & 7) * 8 : (v & 15) * 4;
     uok[u] = r < p.rows_w;
     const uint32_t prow = (ob * 4u + static_cast<uint32_t>(w)) * static_cast<uint32_t>(p.rows_w) + static_cast<uint32_t>(r);
-    voff[u] = uok[u] ? prow * static_cast<uint32_t>(p.C) * 2u + static_cast<uint32_t>(cb) * 16u : kOOB;
-    ioff[u] = uok[u] ? prow * static_cast<uint32_t>(p.C) + static_cast<uint32_t>(cb) * 8u : kOOB;
+    voff[u] = uok[u] ? (prow * static_cast<uint32_t>(p.C) + static_cast<uint32_t>(c)) * 2u : kOOB;
+    ioff[u] = uok[u] ? prow * static_cast<uint32_t>(p.C) + static_cast<uint32_t>(c) : kOOB;
     // first tile row of the unit's group (FULL: the unit's own row)
     const int o0 = 64 * w + (FULL ? r : (r / p.K) * p.G);
-    ubase[u] = trow(static_cast<uint32_t>(uok[u] ? o0 : 0)) + static_cast<uint32_t>((cb >> 2) * 1024 + (cb & 3) * 256);
+    const int cb = c >> 3;
+    ubase[u] = trow(static_cast<uint32_t>(uok[u] ? o0 : 0)) +
+               static_cast<uint32_t>((cb >> 2) * 1024 + (cb & 3) * 256 + (c & 7) * 2);
   }
-  u32x4_t pv[UPL];
-  u32x2_t pi[UPL];
+  // a unit's values and indices, in registers of exactly their size (an
+  // asm load result is never copied before its wait)
+  using PV = std::conditional_t<UE == 8, u32x4_t, u32x2_t>;
+  using PI = std::conditional_t<UE == 8, u32x2_t, uint32_t>;
+  PV pv[UPL];
+  PI pi[UPL];
   auto load_w = [&](int ch) {
 #pragma unroll
     for (int u = 0; u < UPL; ++u) {
-      pv[u] = load_x4(vd, voff[u] + static_cast<uint32_t>(ch) * (kCK * 2));
-      if constexpr (!FULL) pi[u] = load_x2(id, ioff[u] + static_cast<uint32_t>(ch) * kCK);
+      if constexpr (UE == 8) {
+        pv[u] = load_x4(vd, voff[u] + static_cast<uint32_t>(ch) * (kCK * 2));
+        if constexpr (!FULL) pi[u] = load_x2(id, ioff[u] + static_cast<uint32_t>(ch) * kCK);
+      } else {
+        pv[u] = load_x2(vd, voff[u] + static_cast<uint32_t>(ch) * (kCK * 2));
+        pi[u] = load_x1(id, ioff[u] + static_cast<uint32_t>(ch) * kCK);
+      }
     }
   };
+  // tile offset of row rr of a group, relative to its first row
+  auto grow = [](uint32_t rr) { return BIGG ? trow(rr) : rr << 4; };
   // Building a tile.  The two tiles are zeroed once.  K == G: a build
   // overwrites every entry.  K <= G / 4 (UNSC): a build first clears only
   // the entries the build two chunks earlier (same tile) wrote, then writes
   // its own.  Otherwise it zeroes its rows, then writes.  All clears of a
   // build are issued before its writes, so across lanes a clear never lands
   // after a write.  Wave w owns tile rows [64 w, 64 w + 64) in every step.
-  constexpr bool UNSC = !FULL && UPL <= 2;
-  u32x2_t pold1[UPL], pold2[UPL];  // indices of the last two builds (UNSC)
+  constexpr bool UNSC = !FULL && UPL * UE <= 16;
+  PI pold1[UPL], pold2[UPL];  // indices of the last two builds (UNSC)
 #pragma unroll
-  for (int u = 0; u < UPL; ++u) pold1[u] = pold2[u] = u32x2_t{0u, 0u};
+  for (int u = 0; u < UPL; ++u) pold1[u] = pold2[u] = PI{};
   auto w_fence = [&]() {  // the loaded values are used only after this point
 #pragma unroll
     for (int u = 0; u < UPL; ++u) {
@@ -232,38 +259,30 @@ void wide_tile_kernel(WParams p) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) zero_piece(tb, i);
   };
-  auto unscatter = [&](uint8_t* tb, int u) {  // clear what pold2[u] (two builds ago) wrote
-    if constexpr (UNSC) {
-      if (!uok[u]) return;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const uint32_t rr = (pold2[u][e >> 2] >> (8 * (e & 3))) & 0xffu;
-        *reinterpret_cast<uint16_t*>(tb + ubase[u] + trow(rr) + 2 * e) = 0;
-      }
-    }
-  };
   auto unscatter_e = [&](uint8_t* tb, int u, int e) {  // element e of unscatter(tb, u)
     if (!uok[u]) return;
-    const uint32_t rr = (pold2[u][e >> 2] >> (8 * (e & 3))) & 0xffu;
-    *reinterpret_cast<uint16_t*>(tb + ubase[u] + trow(rr) + 2 * e) = 0;
+    const uint32_t rr = (iword(pold2[u], e >> 2) >> (8 * (e & 3))) & 0xffu;
+    *reinterpret_cast<uint16_t*>(tb + ubase[u] + grow(rr) + 2 * e) = 0;
   };
   auto scatter_e = [&](uint8_t* tb, int u, int e) {  // element e of scatter(tb, u), K < G
     if (!uok[u]) return;
-    const uint32_t rr = (pi[u][e >> 2] >> (8 * (e & 3))) & 0xffu;
-    *reinterpret_cast<uint16_t*>(tb + ubase[u] + trow(rr) + 2 * e) = static_cast<uint16_t>(pv[u][e >> 1] >> (16 * (e & 1)));
+    const uint32_t rr = (iword(pi[u], e >> 2) >> (8 * (e & 3))) & 0xffu;
+    *reinterpret_cast<uint16_t*>(tb + ubase[u] + grow(rr) + 2 * e) = static_cast<uint16_t>(pv[u][e >> 1] >> (16 * (e & 1)));
   };
   auto scatter_full = [&](uint8_t* tb, int u) {  // K == G: the unit's 16 bytes
-    if (uok[u]) *reinterpret_cast<u32x4_t*>(tb + ubase[u]) = pv[u];
+    if constexpr (UE == 8) {
+      if (uok[u]) *reinterpret_cast<u32x4_t*>(tb + ubase[u]) = pv[u];
+    }
   };
   auto scatter = [&](uint8_t* tb, int u) {
     if (!uok[u]) return;
-    if constexpr (FULL) {
+    if constexpr (FULL && UE == 8) {
       *reinterpret_cast<u32x4_t*>(tb + ubase[u]) = pv[u];
     } else {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const uint32_t rr = (pi[u][e >> 2] >> (8 * (e & 3))) & 0xffu;  // row within the group
-        *reinterpret_cast<uint16_t*>(tb + ubase[u] + trow(rr) + 2 * e) =
+      for (int e = 0; e < UE; ++e) {
+        const uint32_t rr = (iword(pi[u], e >> 2) >> (8 * (e & 3))) & 0xffu;  // row within the group
+        *reinterpret_cast<uint16_t*>(tb + ubase[u] + grow(rr) + 2 * e) =
             static_cast<uint16_t>(pv[u][e >> 1] >> (16 * (e & 1)));
       }
     }
@@ -382,7 +401,7 @@ void wide_tile_kernel(WParams p) {
 #pragma unroll
               for (int k = 0; k < kUPG; ++k) {
                 const int u = (g & 3) * kUPG + k;
-                if (u < UPL) {
+                if (u < UPL && i < UE) {
                   if (g < 4) {
                     if constexpr (UNSC) unscatter_e(tb, u, i);
                   } else {
@@ -529,27 +548,30 @@ bool plain_rows(const ProductArgs& a) {
   return g.KH == 1 && g.KW == 1 && g.sh == 1 && g.sw == 1 && g.ph == 0 && g.pw == 0;
 }
 
-int units_per_lane(int G, int K) { return (8 * K + G - 1) / G; }
-
-template <typename YT, int UPL, bool FULL>
+template <typename YT, int UPL, int UE, bool FULL, bool BIGG>
 hipError_t launch_wu(const WParams& p, uint32_t grid, hipStream_t s) {
-  static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(&wide_tile_kernel<YT, UPL, FULL>), hipFuncAttributeMaxDynamicSharedMemorySize, kLds);
+  static const hipError_t attr =
+      hipFuncSetAttribute(reinterpret_cast<const void*>(&wide_tile_kernel<YT, UPL, UE, FULL, BIGG>),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, kLds);
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((wide_tile_kernel<YT, UPL, FULL>), dim3(grid), dim3(kThreads), kLds, s, p);
+  hipLaunchKernelGGL((wide_tile_kernel<YT, UPL, UE, FULL, BIGG>), dim3(grid), dim3(kThreads), kLds, s, p);
   return hipGetLastError();
+}
+
+template <typename YT, bool BIGG>
+hipError_t launch_wg(const WParams& p, uint32_t grid, hipStream_t s) {
+  // packed elements per lane per chunk: rows_w (= 64 K / G)
+  if (p.rows_w == 4) return launch_wu<YT, 1, 4, false, BIGG>(p, grid, s);
+  if (p.rows_w <= 8) return launch_wu<YT, 1, 8, false, BIGG>(p, grid, s);
+  if (p.rows_w <= 16) return launch_wu<YT, 2, 8, false, BIGG>(p, grid, s);
+  if (p.rows_w <= 32) return launch_wu<YT, 4, 8, false, BIGG>(p, grid, s);
+  return launch_wu<YT, 8, 8, false, BIGG>(p, grid, s);
 }
 
 template <typename YT>
 hipError_t launch_wy(const WParams& p, uint32_t grid, hipStream_t s) {
-  if (p.K == p.G) return launch_wu<YT, 8, true>(p, grid, s);
-  switch (units_per_lane(p.G, p.K)) {
-    case 1: return launch_wu<YT, 1, false>(p, grid, s);
-    case 2: return launch_wu<YT, 2, false>(p, grid, s);
-    case 3:
-    case 4: return launch_wu<YT, 4, false>(p, grid, s);
-    default: return launch_wu<YT, 8, false>(p, grid, s);
-  }
+  if (p.K == p.G) return launch_wu<YT, 8, 8, true, false>(p, grid, s);
+  return p.G > 16 ? launch_wg<YT, true>(p, grid, s) : launch_wg<YT, false>(p, grid, s);
 }
 
 }  // namespace

@@ -65,7 +65,7 @@ def test_spmm_bf16(N, C, O, G, K, algo):
 WIDE_CASES = [  # N, C, O, G, K: chunks 1..5, ragged pixel blocks, every unit count, K == G
     (600, 256, 512, 8, 2), (300, 128, 256, 16, 1), (257, 64, 256, 16, 4), (1000, 320, 256, 4, 3),
     (512, 192, 768, 16, 16), (100, 256, 256, 64, 7), (2065, 128, 256, 2, 1), (1024, 128, 1024, 8, 2),
-    (2048, 64, 256, 32, 9),
+    (2048, 64, 256, 32, 9), (520, 128, 256, 32, 2), (300, 192, 512, 64, 4),
 ]
 
 

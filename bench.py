@@ -41,7 +41,7 @@ def parse():
     p.add_argument("--steps", type=int, default=200)
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--workload", default="conv3x3")
-    p.add_argument("--algo", default="auto", choices=["auto", "sparse_mac", "dense_tile_mfma"])
+    p.add_argument("--algo", default="auto", choices=["auto", "sparse_mac", "dense_tile_mfma", "wide_tile_mfma"])
     p.add_argument("--rotate-mb", type=float, default=600.0,
                    help="total size of rotated X/Y copies (0: no rotation)")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target wall time of the CPU oracle sample")
@@ -59,17 +59,20 @@ def parse():
     return p.parse_args()
 
 
-def kernel_source_hash() -> str:
-    """Hash of the kernel sources with comments and blank space removed, so
-    that counter files stay matched to the code they measured across edits
-    of the comments."""
+KERNEL_SOURCES = {"cci_dense_tile": "cci_dense_tile.hip", "cci_wide_tile": "cci_wide_tile.hip",
+                  "cci_sparse_mac": "cci_sparse_mac.hip"}
+
+
+def kernel_source_hash(kernel: str = "cci_dense_tile") -> str:
+    """Hash of one kernel's source file with comments and blank space
+    removed, so that counter files stay matched to the code they measured
+    across edits of comments or of other kernels."""
     h = hashlib.sha256()
-    csrc = os.path.join(HERE, "paper_1910_11971_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
-        with open(os.path.join(csrc, f)) as fh:
-            text = re.sub(r"//[^\n]*", "", fh.read())
-            text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-        h.update(f.encode() + " ".join(text.split()).encode())
+    f = KERNEL_SOURCES[kernel]
+    with open(os.path.join(HERE, "paper_1910_11971_amd", "csrc", f)) as fh:
+        text = re.sub(r"//[^\n]*", "", fh.read())
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    h.update(f.encode() + " ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 
@@ -213,9 +216,9 @@ def main():
     val_b = 2 if vdt == torch.bfloat16 else 4
     alg_bytes = x_bytes + wl.nnz * (val_b + 1) + y_bytes
     dense_flop = 2.0 * wl.N * wl.C * wl.O
-    src_hash = kernel_source_hash()
-    kname = "cci_dense_tile" if algo == "dense_tile_mfma" else "cci_sparse_mac"
-    if algo == "dense_tile_mfma":
+    kname = kernel_name(algo)
+    src_hash = kernel_source_hash(kname)
+    if algo in ("dense_tile_mfma", "wide_tile_mfma"):
         t_hbm = alg_bytes / (PEAK["hbm_GBps"] * 1e9)
         t_mfma = dense_flop / (PEAK["mfma_bf16_TFLOPs"] * 1e12)
         if t_hbm >= t_mfma:
@@ -223,7 +226,7 @@ def main():
             roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK["hbm_GBps"], "unit": "GB/s",
                     "frac": round(ach / PEAK["hbm_GBps"], 4)}
         else:
-            ach = flop / (conv_avg * 1e-3) / 1e12
+            ach = dense_flop / (conv_avg * 1e-3) / 1e12  # the expanded product the matrix cores run
             roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK["mfma_bf16_TFLOPs"],
                     "unit": "TFLOP/s", "frac": round(ach / PEAK["mfma_bf16_TFLOPs"], 4)}
     else:
@@ -373,8 +376,13 @@ def _eager_time(fn, n, stream):
     return a.elapsed_time(b) / n
 
 
+def kernel_name(algo):
+    return {"dense_tile_mfma": "cci_dense_tile", "wide_tile_mfma": "cci_wide_tile"}.get(algo, "cci_sparse_mac")
+
+
 def _roof(kname, flop, dense_flop, alg_bytes, t_ms):
-    if kname == "cci_dense_tile":
+    # the matrix-core kernels execute the expanded (dense) product
+    if kname in ("cci_dense_tile", "cci_wide_tile"):
         t_hbm = alg_bytes / (PEAK["hbm_GBps"] * 1e9)
         t_mfma = dense_flop / (PEAK["mfma_bf16_TFLOPs"] * 1e12)
         if t_hbm >= t_mfma:
@@ -414,7 +422,7 @@ def sweep(args):
         W = torch.from_numpy(W_np).to(dev)
         vals, idx = cci.pack(W, wl.G, wl.K, xdt)
         algo = cci.auto_algo(xdt, xdt, wl.N, wl.C, wl.Cin, wl.O, wl.G, wl.K)
-        kname = "cci_dense_tile" if algo == "dense_tile_mfma" else "cci_sparse_mac"
+        kname = kernel_name(algo)
         if wl.conv:
             f = lambda i: cci.conv_im2col(Xs[i % ncopy], vals, idx, wl.G, wl.KH, wl.KW, (wl.stride,) * 2,
                                           (wl.pad,) * 2, out_dtype=ydt, out=Ys[i % ncopy])

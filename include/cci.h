@@ -135,7 +135,9 @@ cci_status cci_conv_im2col(const void *X, cci_dtype x_t, int64_t B, int64_t H,
                            cci_algo algo, void *stream);
 
 /* Which family CCI_ALGO_AUTO picks for a product of N x C x O (conv: pass
- * N = B*Ho*Wo, C = KH*KW*Cin and cin = Cin; FC: cin = C).  Host-only. */
+ * N = B*Ho*Wo, C = KH*KW*Cin and cin = Cin; FC: cin = C).  Host-only.  A
+ * 1x1 convolution reported as CCI_ALGO_WIDE_TILE_MFMA runs on the dense-tile
+ * kernels when its stride or padding rules the wide-tile ones out. */
 cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C,
                        int64_t cin, int64_t O, int32_t G, int32_t K);
 

@@ -112,8 +112,13 @@ def test_conv_geometry_errors():
 def test_auto_algo_cost_model():
     # bf16, tile-friendly: expanded MFMA work wins while K/G > 1/32
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 100352, 576, 64, 64, 8, 2) == "dense_tile_mfma"
-    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 4096, 4096, 4096, 4096, 16, 1) == "dense_tile_mfma"
-    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 4096, 4096, 4096, 4096, 64, 1) == "sparse_mac"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 4096, 4096, 4096, 512, 16, 1) == "dense_tile_mfma"
+    # large FC / 1x1 products (>= 128 tiles of 256 x 256): wide-tile MFMA, any K
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 4096, 4096, 4096, 4096, 16, 1) == "wide_tile_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 4096, 4096, 4096, 4096, 64, 1) == "wide_tile_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 12544, 1024, 1024, 256, 16, 4) == "dense_tile_mfma"
+    # G the vector kernels do not support: the tile path even at K/G < 1/32
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 4096, 4096, 4096, 512, 64, 1) == "dense_tile_mfma"
     # fp32, or a reduction the tile path cannot step through: sparse-MAC
     assert cci.auto_algo(torch.float32, torch.float32, 64, 256, 256, 256, 8, 4) == "sparse_mac"
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 1000, 147, 3, 64, 8, 8) == "sparse_mac"

@@ -115,8 +115,6 @@ def main():
         return sweep(args)
 
     wl = workloads.WORKLOADS[args.workload]
-    if not wl.conv:
-        raise SystemExit("bench.py times the convolution workloads (conv3x3, conv1x1_k4, conv1x1_k2)")
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     X_cpu, W_np = workloads.draw(wl)
@@ -131,7 +129,8 @@ def main():
     ncopy = 1 if args.rotate_mb <= 0 else max(1, int(np.ceil(args.rotate_mb * 1e6 / (x_bytes + y_bytes))))
     X0 = X_cpu.to(dev)
     Xs = [X0] + [X0.clone() for _ in range(ncopy - 1)]
-    Ys = [torch.empty((wl.B, wl.Ho, wl.Wo, wl.O), dtype=ydt, device=dev) for _ in range(ncopy)]
+    yshape = (wl.B, wl.Ho, wl.Wo, wl.O) if wl.conv else (wl.N, wl.O)
+    Ys = [torch.empty(yshape, dtype=ydt, device=dev) for _ in range(ncopy)]
     W = torch.from_numpy(W_np).to(dev)
     vals = torch.empty((wl.O // wl.G, wl.K, wl.C), dtype=vdt, device=dev)
     idx = torch.empty((wl.O // wl.G, wl.K, wl.C), dtype=torch.uint8, device=dev)
@@ -139,14 +138,16 @@ def main():
     stream = torch.cuda.Stream(device=dev)  # default priority
     algo = args.algo if args.algo != "auto" else cci.auto_algo(xdt, vdt, wl.N, wl.C, wl.Cin, wl.O, wl.G, wl.K)
 
+    def conv_only(i):  # the product (a convolution, or an FC layer via cci_spmm)
+        if wl.conv:
+            cci.conv_im2col(Xs[i % ncopy], vals, idx, wl.G, wl.KH, wl.KW, stride, pad, out_dtype=ydt, algo=algo,
+                            out=Ys[i % ncopy])
+        else:
+            cci.spmm(Xs[i % ncopy], vals, idx, wl.G, out_dtype=ydt, algo=algo, out=Ys[i % ncopy])
+
     def step(i):
         cci.pack(W, wl.G, wl.K, vdt, out=(vals, idx))
-        cci.conv_im2col(Xs[i % ncopy], vals, idx, wl.G, wl.KH, wl.KW, stride, pad, out_dtype=ydt, algo=algo,
-                        out=Ys[i % ncopy])
-
-    def conv_only(i):
-        cci.conv_im2col(Xs[i % ncopy], vals, idx, wl.G, wl.KH, wl.KW, stride, pad, out_dtype=ydt, algo=algo,
-                        out=Ys[i % ncopy])
+        conv_only(i)
 
     def pack_only(i):
         cci.pack(W, wl.G, wl.K, vdt, out=(vals, idx))
@@ -244,28 +245,37 @@ def main():
     if not args.no_dense and xdt == torch.bfloat16:
         with torch.cuda.stream(stream):
             Wd = W.to(torch.bfloat16)                                  # [O, C] dense
-            if wl.KH == 1 and wl.stride == 1 and wl.pad == 0:
-                A = Xs[0].reshape(wl.N, wl.Cin)
-            else:
-                A = torch.nn.functional.unfold(Xs[0].permute(0, 3, 1, 2).float(), (wl.KH, wl.KW),
-                                               padding=wl.pad, stride=wl.stride)   # [B, Cin*k*k, L]
-                A = A.reshape(wl.B, wl.Cin, wl.KH, wl.KW, -1).permute(0, 4, 2, 3, 1).reshape(wl.N, wl.C)
-                A = A.to(torch.bfloat16).contiguous()
             Bt = Wd.t().contiguous()
-            Wc = W.reshape(wl.O, wl.KH, wl.KW, wl.Cin).permute(0, 3, 1, 2).to(torch.bfloat16).contiguous(
-                memory_format=torch.channels_last)
-
-            Xn = [x.permute(0, 3, 1, 2) for x in Xs]                   # channels_last views, rotated
-            for i in range(5):                                         # library heuristics / autotuning
-                torch.matmul(A, Bt)
-                torch.nn.functional.conv2d(Xn[i % ncopy], Wc, stride=wl.stride, padding=wl.pad)
-            gemm_ms = timed(lambda i: torch.matmul(A, Bt), 50)
-            conv_ms_d = timed(lambda i: torch.nn.functional.conv2d(Xn[i % ncopy], Wc, stride=wl.stride,
-                                                                  padding=wl.pad), 50)
-        dense = {"gemm_explicit_im2col_ms": round(gemm_ms, 5), "miopen_conv2d_ms": round(conv_ms_d, 5),
-                 "speedup_vs_gemm": round(gemm_ms / conv_avg, 3), "speedup_vs_conv2d": round(conv_ms_d / conv_avg, 3),
-                 "note": "conv2d rotates X like the CCI kernel; the GEMM reads one 115 MB im2col matrix (warm in MALL)"}
-        del A
+            if not wl.conv:
+                # FC: the GEMM reads the same rotated activations as the CCI kernel
+                for i in range(5):
+                    torch.matmul(Xs[i % ncopy], Bt)
+                gemm_ms = timed(lambda i: torch.matmul(Xs[i % ncopy], Bt), 50)
+                dense = {"gemm_ms": round(gemm_ms, 5), "speedup_vs_gemm": round(gemm_ms / conv_avg, 3),
+                         "note": "hipBLASLt bf16 GEMM of the dense weights, X rotated like the CCI kernel"}
+            else:
+                if wl.KH == 1 and wl.stride == 1 and wl.pad == 0:
+                    A = Xs[0].reshape(wl.N, wl.Cin)
+                else:
+                    A = torch.nn.functional.unfold(Xs[0].permute(0, 3, 1, 2).float(), (wl.KH, wl.KW),
+                                                   padding=wl.pad, stride=wl.stride)   # [B, Cin*k*k, L]
+                    A = A.reshape(wl.B, wl.Cin, wl.KH, wl.KW, -1).permute(0, 4, 2, 3, 1).reshape(wl.N, wl.C)
+                    A = A.to(torch.bfloat16).contiguous()
+                Wc = W.reshape(wl.O, wl.KH, wl.KW, wl.Cin).permute(0, 3, 1, 2).to(torch.bfloat16).contiguous(
+                    memory_format=torch.channels_last)
+                Xn = [x.permute(0, 3, 1, 2) for x in Xs]                   # channels_last views, rotated
+                for i in range(5):                                         # library heuristics / autotuning
+                    torch.matmul(A, Bt)
+                    torch.nn.functional.conv2d(Xn[i % ncopy], Wc, stride=wl.stride, padding=wl.pad)
+                gemm_ms = timed(lambda i: torch.matmul(A, Bt), 50)
+                conv_ms_d = timed(lambda i: torch.nn.functional.conv2d(Xn[i % ncopy], Wc, stride=wl.stride,
+                                                                      padding=wl.pad), 50)
+                dense = {"gemm_explicit_im2col_ms": round(gemm_ms, 5), "miopen_conv2d_ms": round(conv_ms_d, 5),
+                         "speedup_vs_gemm": round(gemm_ms / conv_avg, 3),
+                         "speedup_vs_conv2d": round(conv_ms_d / conv_avg, 3),
+                         "note": "conv2d rotates X like the CCI kernel; the GEMM reads one im2col matrix "
+                                 "(warm in MALL)"}
+                del A
 
     # ---- CPU oracle baseline (rank 0, N=1 only) ---------------------------------
     cpu = None
@@ -276,13 +286,19 @@ def main():
         v32, ix = oracle.pack(W_np, wl.G, wl.K)
         vb = oracle.bf16_bits_to_f32(oracle.bf16_rne(v32)) if vdt == torch.bfloat16 else v32
         Wm = oracle.unpack(vb, ix, wl.G).reshape(wl.O, wl.KH, wl.KW, wl.Cin)
+
+        def oracle_rows(pix):  # the product for a sample of output pixels / rows
+            if wl.conv:
+                return oracle.conv2d_nhwc(Xf, Wm, stride, pad, pixels=pix)
+            return oracle.spmm_rows(Xf, vb, ix, wl.G, rows=pix)
+
         t_pack = time.perf_counter() - t
         rng = np.random.default_rng(0)
         n = 256
         while True:
             pix = np.sort(rng.choice(wl.N, size=min(n, wl.N), replace=False))
             t = time.perf_counter()
-            oracle.conv2d_nhwc(Xf, Wm, stride, pad, pixels=pix)
+            oracle_rows(pix)
             dt = time.perf_counter() - t
             if dt >= args.cpu_seconds or n >= wl.N:
                 break
@@ -294,7 +310,7 @@ def main():
             ts = [dt]
             for _ in range(reps - 1):
                 t = time.perf_counter()
-                oracle.conv2d_nhwc(Xf, Wm, stride, pad, pixels=pix)
+                oracle_rows(pix)
                 ts.append(time.perf_counter() - t)
             dt = float(np.median(ts))
         per_pix = dt / len(pix)
@@ -307,8 +323,8 @@ def main():
             pass
         cpu = {"value": round(flop / t_step / 1e12, 6), "unit": "TFLOP/s", "cores": oracle.num_threads(),
                "kind": "oracle",
-               "sample": f"oracle pack of all {wl.O}x{wl.C} weights ({t_pack:.3f}s) + direct conv of "
-                         f"{len(pix)} of {wl.N} output pixels ({dt:.2f}s, median of {reps}, double precision), "
+               "sample": f"oracle pack of all {wl.O}x{wl.C} weights ({t_pack:.3f}s) + the product for "
+                         f"{len(pix)} of {wl.N} {'output pixels' if wl.conv else 'rows'} ({dt:.2f}s, median of {reps}, double precision), "
                          f"scaled to the full step",
                "cpu_model": cpu_model, "omp_num_threads": os.environ.get("OMP_NUM_THREADS")}
 
@@ -317,8 +333,11 @@ def main():
         "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_step, 6), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": f"{wl.name}: conv {wl.KH}x{wl.KW} s{wl.stride} p{wl.pad}, batch {wl.B}, "
-                               f"{wl.H}x{wl.W}, {wl.Cin}->{wl.O}, G={wl.G}, K={wl.K}, bf16 in/out, fp32 acc",
+        "config": {"workload": (f"{wl.name}: conv {wl.KH}x{wl.KW} s{wl.stride} p{wl.pad}, batch {wl.B}, "
+                                f"{wl.H}x{wl.W}, {wl.Cin}->{wl.O}, G={wl.G}, K={wl.K}, bf16 in/out, fp32 acc"
+                                if wl.conv else
+                                f"{wl.name}: FC, X [{wl.N},{wl.C}], W [{wl.O},{wl.C}], G={wl.G}, K={wl.K}, "
+                                f"bf16 in/out, fp32 acc"),
                    "N": wl.N, "C": wl.C, "O": wl.O, "G": wl.G, "K": wl.K, "nnz": wl.nnz, "algo": algo,
                    "rotated_copies": ncopy},
         "kernels_us": {"cci_pack": round(pack_avg * 1e3, 3), kname: round(conv_avg * 1e3, 3),

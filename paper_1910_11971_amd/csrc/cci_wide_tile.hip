@@ -11,13 +11,18 @@
 //     lane, in the accumulation registers), so every fragment read from LDS
 //     feeds eight MFMAs, and each expanded weight tile serves 256 pixels;
 //   - the reduction runs over chunks of 64 channels.  The activations of
-//     chunk j+2 are DMA'd into LDS while chunk j is multiplied (three
-//     buffers); the packed weights of chunk j+2 are loaded into registers
-//     during chunk j and expanded into the second weight tile between chunk
-//     j+1's two k-steps; one barrier per chunk;
+//     chunk j+3 are DMA'd into LDS during chunk j (three buffers, each
+//     refilled as soon as the chunk that used it is done); the packed
+//     weights of chunk j+2 are loaded into registers during chunk j and
+//     written into the second weight tile during chunk j+1; the barrier of
+//     a chunk sits in its middle, after which no wave reads that chunk's
+//     buffers (every fragment is already in registers), so the next chunk's
+//     fragments stream in behind the remaining MFMAs;
+//   - one wave per SIMD issues in order, so the loads and tile writes are
+//     placed between single MFMAs;
 //   - workgroup ids are remapped so that each XCD holds a 4 pixel-block x
-//     8 output-block patch of tiles: activations and packed rows are then
-//     mostly read through that XCD's L2.
+//     8 output-block patch of tiles (tiles that share activations or packed
+//     rows sit behind one L2).
 //
 // LDS layouts (bytes):
 //   activation buffer: pixel q at q * 128; its 16-byte column c holds

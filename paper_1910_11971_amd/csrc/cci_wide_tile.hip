@@ -241,12 +241,13 @@ void wide_tile_kernel(WParams p) {
   // tile offset of row rr of a group, relative to its first row
   auto grow = [](uint32_t rr) { return BIGG ? trow(rr) : rr << 4; };
   // Building a tile.  The two tiles are zeroed once.  K == G: a build
-  // overwrites every entry.  K <= G / 4 (UNSC): a build first clears only
-  // the entries the build two chunks earlier (same tile) wrote, then writes
-  // its own.  Otherwise it zeroes its rows, then writes.  All clears of a
+  // overwrites every entry.  Four entries per lane (UNSC): a build first
+  // clears only the entries the build two chunks earlier (same tile) wrote,
+  // then writes its own.  Otherwise it zeroes its rows (cheaper from eight
+  // entries per lane up), then writes.  All clears of a
   // build are issued before its writes, so across lanes a clear never lands
   // after a write.  Wave w owns tile rows [64 w, 64 w + 64) in every step.
-  constexpr bool UNSC = !FULL && UPL * UE <= 16;
+  constexpr bool UNSC = !FULL && UPL * UE <= 4;
   PI pold1[UPL], pold2[UPL];  // indices of the last two builds (UNSC)
 #pragma unroll
   for (int u = 0; u < UPL; ++u) pold1[u] = pold2[u] = PI{};

@@ -134,6 +134,16 @@ __device__ __forceinline__ uint32_t load_x1(const u32x4_t d, uint32_t off) {
   return v;
 }
 
+// Geometry of a workgroup tile of PT 16-pixel tiles per wave (namespace
+// scope: the kernel's lambdas must not capture constants of the template).
+template <int PT>
+struct Geo {
+  static constexpr int TP = PT * 32;        // pixels of the workgroup's tile
+  static constexpr int XB = TP * kCK * 2;   // one activation buffer
+  static constexpr int WOFS = 3 * XB;       // weight tiles follow the three activation buffers
+  static constexpr int WPX = PT * 2048;     // bytes of one wave's pixel half of a buffer
+};
+
 // Word k of a unit's packed indices.
 __device__ __forceinline__ uint32_t iword(const u32x2_t v, int k) { return v[k]; }
 __device__ __forceinline__ uint32_t iword(uint32_t v, int) { return v; }
@@ -145,10 +155,8 @@ __device__ __forceinline__ uint32_t trow(uint32_t o) { return ((o >> 4) << 11) |
 // per lane per chunk.  FULL: K == G (every entry kept, indices ascending, so
 // a unit is one row's 16 bytes).  BIGG: G > 16 (a group spans 16-row
 // blocks of the tile).
-template <typename YT, int UPL, int UE, bool FULL, bool BIGG>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void wide_tile_kernel(WParams p) {
-  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+template <typename YT, int PT, int UPL, int UE, bool FULL, bool BIGG>
+__device__ __forceinline__ void wide_tile_body(const WParams& p, uint8_t* lds) {
   constexpr int NW = FULL ? UPL : 2 * UPL;  // vector-memory operations of one packed-chunk load
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -176,23 +184,23 @@ void wide_tile_kernel(WParams p) {
   // lane l writes the 16 bytes at (8w + i) * 1024 + 16 l, i.e. pixel
   // q = (8w + i) * 8 + l / 8, column l % 8, which holds channel block
   // (l % 8) ^ sw(q).  Pixels past N read as zero.
-  uint32_t xoff[8];
+  uint32_t xoff[PT];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const uint32_t q = static_cast<uint32_t>((8 * w + i) * 8 + (lane >> 3));
-    const uint32_t px = pb * kTile + q;
+  for (int i = 0; i < PT; ++i) {
+    const uint32_t q = static_cast<uint32_t>((PT * w + i) * 8 + (lane >> 3));
+    const uint32_t px = pb * Geo<PT>::TP + q;
     const uint32_t k8 = static_cast<uint32_t>(lane & 7) ^ ((q >> 1) & 7u);
     xoff[i] = px < static_cast<uint32_t>(p.N) ? px * static_cast<uint32_t>(p.C) * 2u + k8 * 16u : kOOB;
   }
   auto issue_x_one = [&](int ch, int buf, int i) {
-    lds_void_t* d = (lds_void_t*)(lds + buf * kXBytes + w * 8192 + i * 1024);
+    lds_void_t* d = (lds_void_t*)(lds + buf * Geo<PT>::XB + w * (PT * 1024) + i * 1024);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, d, 16, xoff[i] + static_cast<uint32_t>(ch) * (kCK * 2), 0, 0, 0);
   };
   auto issue_x = [&](int ch, int buf) {
-    uint8_t* dst = lds + buf * kXBytes + w * 8192;
+    uint8_t* dst = lds + buf * Geo<PT>::XB + w * (PT * 1024);
     const uint32_t co = static_cast<uint32_t>(ch) * (kCK * 2);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < PT; ++i) {
       lds_void_t* d = (lds_void_t*)(dst + i * 1024);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, d, 16, xoff[i] + co, 0, 0, 0);
     }
@@ -306,13 +314,13 @@ void wide_tile_kernel(WParams p) {
   // ---- MFMAs --------------------------------------------------------------------
   // acc[pt][ot]: 16 pixels (tile pt of the wave's 128) x 16 outputs (tile ot
   // of its 128).  A lane holds outputs 4 (lane / 16) .. +3 of pixel lane % 16.
-  f32x4_t acc[8][8];
+  f32x4_t acc[PT][8];
 #pragma unroll
-  for (int pt = 0; pt < 8; ++pt)
+  for (int pt = 0; pt < PT; ++pt)
 #pragma unroll
     for (int ot = 0; ot < 8; ++ot) acc[pt][ot] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int pt = 0; pt < 8; ++pt)
+  for (int pt = 0; pt < PT; ++pt)
 #pragma unroll
     for (int ot = 0; ot < 8; ++ot) acc_fence(acc[pt][ot]);
   mfma_drain();  // the zero writes land before the first MFMA reads them
@@ -332,16 +340,16 @@ void wide_tile_kernel(WParams p) {
   issue_x(0, 0);
   load_w(0);
   if (nch > 1) issue_x(1, 1);
-  if (nch > 1) wait_vm<8>(); else wait_vm<0>();  // W(0)
+  if (nch > 1) wait_vm<PT>(); else wait_vm<0>();  // W(0)
   w_fence();
-  zero_rows(lds + kWOfs);
-  zero_rows(lds + kWOfs + kWBytes);
+  zero_rows(lds + Geo<PT>::WOFS);
+  zero_rows(lds + Geo<PT>::WOFS + kWBytes);
 #pragma unroll
-  for (int u = 0; u < UPL; ++u) scatter(lds + kWOfs, u);
+  for (int u = 0; u < UPL; ++u) scatter(lds + Geo<PT>::WOFS, u);
   rotate_idx();
   if (nch > 1) load_w(1);
   if (nch > 2) issue_x(2, 2);
-  if (nch > 2) wait_vm<8>(); else wait_vm<0>();  // X(0), X(1), W(1)
+  if (nch > 2) wait_vm<PT>(); else wait_vm<0>();  // X(0), X(1), W(1)
   w_fence();
   lds_barrier();
 
@@ -361,12 +369,12 @@ void wide_tile_kernel(WParams p) {
   // Every fragment read is issued at least four groups (~500 cycles of
   // MFMAs) before its use.  M1 / M2 / M3: chunks j+1 / j+2 / j+3 exist
   // (compile-time, so the steady-state body has no branches).
-  bf16x8_t b0[8], b1[8], af[16];
+  bf16x8_t b0[PT], b1[PT], af[16];
   auto read_first = [&](int j) {  // chunk j's k-step-0 fragments
-    const uint8_t* xb = lds + (j % 3) * kXBytes + wp * 16384;
-    const uint8_t* wb = lds + kWOfs + (j & 1) * kWBytes + wo * 16384 + lane * 16;
+    const uint8_t* xb = lds + (j % 3) * Geo<PT>::XB + wp * Geo<PT>::WPX;
+    const uint8_t* wb = lds + Geo<PT>::WOFS + (j & 1) * kWBytes + wo * 16384 + lane * 16;
 #pragma unroll
-    for (int pt = 0; pt < 8; ++pt) b0[pt] = ld(xb + pt * 2048 + boff0);
+    for (int pt = 0; pt < PT; ++pt) b0[pt] = ld(xb + pt * 2048 + boff0);
 #pragma unroll
     for (int g = 0; g < 8; ++g) af[g] = ld(wb + g * 2048);
   };
@@ -374,28 +382,28 @@ void wide_tile_kernel(WParams p) {
   auto chunk = [&](int j, auto m1, auto m2, auto m3) {
     constexpr bool more1 = decltype(m1)::value, more2 = decltype(m2)::value, more3 = decltype(m3)::value;
     const int xbuf = j % 3;
-    const uint8_t* xb = lds + xbuf * kXBytes + wp * 16384;
-    const uint8_t* wb = lds + kWOfs + (j & 1) * kWBytes + wo * 16384 + lane * 16;
+    const uint8_t* xb = lds + xbuf * Geo<PT>::XB + wp * Geo<PT>::WPX;
+    const uint8_t* wb = lds + Geo<PT>::WOFS + (j & 1) * kWBytes + wo * 16384 + lane * 16;
     const int xnb = xbuf == 2 ? 0 : xbuf + 1;
-    const uint8_t* xn = lds + xnb * kXBytes + wp * 16384;  // chunk j+1
-    const uint8_t* wn = lds + kWOfs + ((j + 1) & 1) * kWBytes + wo * 16384 + lane * 16;
-    uint8_t* tb = lds + kWOfs + ((j + 1) & 1) * kWBytes;  // tile j+1, built here
+    const uint8_t* xn = lds + xnb * Geo<PT>::XB + wp * Geo<PT>::WPX;  // chunk j+1
+    const uint8_t* wn = lds + Geo<PT>::WOFS + ((j + 1) & 1) * kWBytes + wo * 16384 + lane * 16;
+    uint8_t* tb = lds + Geo<PT>::WOFS + ((j + 1) & 1) * kWBytes;  // tile j+1, built here
 #pragma unroll
     for (int g = 0; g < 16; ++g) {
       if constexpr (more1) {
         if (g == 8) {
-          if constexpr (more2) wait_vm<8 + 2 * NW>(); else wait_vm<0>();  // X(j+1)
+          if constexpr (more2) wait_vm<PT + 2 * NW>(); else wait_vm<0>();  // X(j+1)
           lds_barrier();
         }
       }
       // One wave per SIMD issues in order, so other work overlaps an MFMA
       // only when it sits between two of them: slot i follows MFMA i.
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
+      for (int i = 0; i < PT; ++i) {
         mfma_acc(acc[i][g & 7], af[g], g < 8 ? b0[i] : b1[i]);
         __builtin_amdgcn_sched_barrier(0);
         if (g < 8) {
-          if (i == 0) b1[g] = ld(xb + g * 2048 + boff1);
+          if (i == 0 && g < PT) b1[g % PT] = ld(xb + g * 2048 + boff1);
           if (i == 1) af[g + 8] = ld(wb + (g * 2 + 1) * 1024);
           if constexpr (more1) {
             if constexpr (FULL) {
@@ -407,30 +415,33 @@ void wide_tile_kernel(WParams p) {
 #pragma unroll
               for (int k = 0; k < kUPG; ++k) {
                 const int u = (g & 3) * kUPG + k;
-                if (u < UPL && i < UE) {
-                  if (g < 4) {
-                    if constexpr (UNSC) unscatter_e(tb, u, i);
-                  } else {
-                    scatter_e(tb, u, i);
+#pragma unroll
+                for (int e = i; e < UE; e += PT) {  // element e of unit u, at slot e % PT
+                  if (u < UPL) {
+                    if (g < 4) {
+                      if constexpr (UNSC) unscatter_e(tb, u, e);
+                    } else {
+                      scatter_e(tb, u, e);
+                    }
                   }
                 }
               }
             }
-            if (g == 7 && i == 7) {
+            if (g == 7 && i == PT - 1) {
               rotate_idx();
               if constexpr (more2) load_w(j + 2);
             }
           }
         } else if constexpr (more1) {
-          if (g < 12) {
+          if (g < 8 + PT / 2) {
             if constexpr (more3) {
               if (i == 0) {
                 issue_x_one(j + 3, xbuf, 2 * (g - 8));
                 issue_x_one(j + 3, xbuf, 2 * (g - 8) + 1);
               }
             }
-            if (i == 1) b0[2 * (g - 8)] = ld(xn + (2 * (g - 8)) * 2048 + boff0);
-            if (i == 2) b0[2 * (g - 8) + 1] = ld(xn + (2 * (g - 8) + 1) * 2048 + boff0);
+            if (i == 1) b0[(2 * (g - 8)) % PT] = ld(xn + (2 * (g - 8)) * 2048 + boff0);
+            if (i == 2) b0[(2 * (g - 8) + 1) % PT] = ld(xn + (2 * (g - 8) + 1) * 2048 + boff0);
           }
           if (i == 3) af[g - 8] = ld(wn + (g - 8) * 2048);
         }
@@ -440,7 +451,7 @@ void wide_tile_kernel(WParams p) {
     // W(j+2) is in registers before the loop carries it on (copies of it
     // may be made at the loop head)
     if constexpr (more2) {
-      if constexpr (more3) wait_vm<8>(); else wait_vm<0>();
+      if constexpr (more3) wait_vm<PT>(); else wait_vm<0>();
       w_fence();
     }
   };
@@ -466,7 +477,7 @@ void wide_tile_kernel(WParams p) {
   // residual / ReLU in fp32, rounds once and stores 16 (bf16) or 32 bytes.
   mfma_drain();    // the last MFMAs have written acc
 #pragma unroll
-  for (int pt = 0; pt < 8; ++pt)
+  for (int pt = 0; pt < PT; ++pt)
 #pragma unroll
     for (int ot = 0; ot < 8; ++ot) acc_fence(acc[pt][ot]);
   lds_barrier();  // every wave is done with the operand buffers
@@ -488,7 +499,7 @@ void wide_tile_kernel(WParams p) {
   }
   uint8_t* stg = lds + w * 64 * kEpPitch;
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
+  for (int h = 0; h < PT / 4; ++h) {
 #pragma unroll
     for (int pt = 0; pt < 4; ++pt)
 #pragma unroll
@@ -501,7 +512,7 @@ void wide_tile_kernel(WParams p) {
       const uint8_t* src = stg + row * kEpPitch + c8 * 32;
       f32x4_t y0 = *reinterpret_cast<const f32x4_t*>(src);
       f32x4_t y1 = *reinterpret_cast<const f32x4_t*>(src + 16);
-      const uint32_t px = pb * kTile + static_cast<uint32_t>(wp * 128 + h * 64 + row);
+      const uint32_t px = pb * Geo<PT>::TP + static_cast<uint32_t>(wp * (PT * 16) + h * 64 + row);
       const uint32_t off = px < static_cast<uint32_t>(p.N) ? (px * static_cast<uint32_t>(p.O) + o) * ysz : kOOB;
       y0 = y0 * sc0 + bi0;
       y1 = y1 * sc1 + bi1;
@@ -546,6 +557,15 @@ void wide_tile_kernel(WParams p) {
   }
 }
 
+// (The body is a device function: with it inside the kernel template, the
+// host pass of this compiler emitted no launch stubs for the kernels.)
+template <typename YT, int PT, int UPL, int UE, bool FULL, bool BIGG>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void wide_tile_kernel(WParams p) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  wide_tile_body<YT, PT, UPL, UE, FULL, BIGG>(p, lds);
+}
+
 // Rows of X are pixels: FC, or a 1x1 convolution with unit stride and no
 // padding over NHWC activations.
 bool plain_rows(const ProductArgs& a) {
@@ -554,31 +574,35 @@ bool plain_rows(const ProductArgs& a) {
   return g.KH == 1 && g.KW == 1 && g.sh == 1 && g.sw == 1 && g.ph == 0 && g.pw == 0;
 }
 
-template <typename YT, int UPL, int UE, bool FULL, bool BIGG>
+template <typename YT, int PT, int UPL, int UE, bool FULL, bool BIGG>
 hipError_t launch_wu(const WParams& p, uint32_t grid, hipStream_t s) {
   static const hipError_t attr =
-      hipFuncSetAttribute(reinterpret_cast<const void*>(&wide_tile_kernel<YT, UPL, UE, FULL, BIGG>),
+      hipFuncSetAttribute(reinterpret_cast<const void*>(&wide_tile_kernel<YT, PT, UPL, UE, FULL, BIGG>),
                           hipFuncAttributeMaxDynamicSharedMemorySize, kLds);
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((wide_tile_kernel<YT, UPL, UE, FULL, BIGG>), dim3(grid), dim3(kThreads), kLds, s, p);
+  hipLaunchKernelGGL((wide_tile_kernel<YT, PT, UPL, UE, FULL, BIGG>), dim3(grid), dim3(kThreads), kLds, s, p);
   return hipGetLastError();
 }
 
-template <typename YT, bool BIGG>
+template <typename YT, int PT, bool BIGG>
 hipError_t launch_wg(const WParams& p, uint32_t grid, hipStream_t s) {
   // packed elements per lane per chunk: rows_w (= 64 K / G)
-  if (p.rows_w == 4) return launch_wu<YT, 1, 4, false, BIGG>(p, grid, s);
-  if (p.rows_w <= 8) return launch_wu<YT, 1, 8, false, BIGG>(p, grid, s);
-  if (p.rows_w <= 16) return launch_wu<YT, 2, 8, false, BIGG>(p, grid, s);
-  if (p.rows_w <= 32) return launch_wu<YT, 4, 8, false, BIGG>(p, grid, s);
-  return launch_wu<YT, 8, 8, false, BIGG>(p, grid, s);
+  if (p.rows_w == 4) return launch_wu<YT, PT, 1, 4, false, BIGG>(p, grid, s);
+  if (p.rows_w <= 8) return launch_wu<YT, PT, 1, 8, false, BIGG>(p, grid, s);
+  if (p.rows_w <= 16) return launch_wu<YT, PT, 2, 8, false, BIGG>(p, grid, s);
+  if (p.rows_w <= 32) return launch_wu<YT, PT, 4, 8, false, BIGG>(p, grid, s);
+  return launch_wu<YT, PT, 8, 8, false, BIGG>(p, grid, s);
 }
 
-template <typename YT>
-hipError_t launch_wy(const WParams& p, uint32_t grid, hipStream_t s) {
-  if (p.K == p.G) return launch_wu<YT, 8, 8, true, false>(p, grid, s);
-  return p.G > 16 ? launch_wg<YT, true>(p, grid, s) : launch_wg<YT, false>(p, grid, s);
+template <typename YT, int PT>
+hipError_t launch_wp(const WParams& p, uint32_t grid, hipStream_t s) {
+  if (p.K == p.G) return launch_wu<YT, PT, 8, 8, true, false>(p, grid, s);
+  return p.G > 16 ? launch_wg<YT, PT, true>(p, grid, s) : launch_wg<YT, PT, false>(p, grid, s);
 }
+
+// Pixels per workgroup tile: 256, or 128 when 256-pixel tiles would leave
+// more than half of the CUs idle.
+int tile_pixels(int64_t N, int64_t O) { return (N + 255) / 256 * (O / kTile) >= 128 ? 256 : 128; }
 
 }  // namespace
 
@@ -620,7 +644,8 @@ hipError_t launch_wide_tile(const ProductArgs& a, hipStream_t s) {
   p.G = a.G;
   p.K = a.K;
   p.relu = a.relu;
-  p.npb = static_cast<int32_t>((a.N + kTile - 1) / kTile);
+  const int tp = tile_pixels(a.N, a.O);
+  p.npb = static_cast<int32_t>((a.N + tp - 1) / tp);
   p.nob = static_cast<int32_t>(a.O / kTile);
   p.nch = static_cast<int32_t>(a.C / kCK);
   p.rows_w = 64 * a.K / a.G;
@@ -628,7 +653,8 @@ hipError_t launch_wide_tile(const ProductArgs& a, hipStream_t s) {
   if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
   p.grid8 = grid % 8 == 0 ? static_cast<int32_t>(grid / 8) : 0;
   const uint32_t g = static_cast<uint32_t>(grid);
-  return a.y_t == DType::BF16 ? launch_wy<bf16_t>(p, g, s) : launch_wy<float>(p, g, s);
+  if (tp == 256) return a.y_t == DType::BF16 ? launch_wp<bf16_t, 8>(p, g, s) : launch_wp<float, 8>(p, g, s);
+  return a.y_t == DType::BF16 ? launch_wp<bf16_t, 4>(p, g, s) : launch_wp<float, 4>(p, g, s);
 }
 
 }  // namespace cci

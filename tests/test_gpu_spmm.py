@@ -66,6 +66,8 @@ WIDE_CASES = [  # N, C, O, G, K: chunks 1..5, ragged pixel blocks, every unit co
     (600, 256, 512, 8, 2), (300, 128, 256, 16, 1), (257, 64, 256, 16, 4), (1000, 320, 256, 4, 3),
     (512, 192, 768, 16, 16), (100, 256, 256, 64, 7), (2065, 128, 256, 2, 1), (1024, 128, 1024, 8, 2),
     (2048, 64, 256, 32, 9), (520, 128, 256, 32, 2), (300, 192, 512, 64, 4),
+    # >= 128 tiles of 256 pixels: the 256-pixel plan (the rest run 128-pixel tiles)
+    (32768, 64, 256, 64, 7), (32768, 128, 256, 4, 3), (33000, 64, 256, 32, 2), (32768, 192, 256, 16, 16),
 ]
 
 

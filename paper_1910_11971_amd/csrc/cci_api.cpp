@@ -150,15 +150,16 @@ cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C, int
   // the vector ALUs multiply only kept weights at 78.6 fp32 TFLOP/s (no
   // packed fp32).  Expanded work is G/K times the kept work, so the tile
   // path wins whenever K/G > 78.6/2516.6 (about 1/32).  The wide-tile plan
-  // (256 x 256 workgroup tiles) is measured faster than the dense-tile one
-  // once the product has at least 128 such tiles (half the CUs) and a
-  // reduction of at least 8 of its 64-channel chunks to pipeline: 2.2-2.4x
-  // on 4096^3 FC products, 0.8x on a 12544 x 1024 x 256 one (49 tiles),
-  // slower on the short reductions of ResNet-50's 1x1 layers.
+  // (256-output workgroup tiles of 256 pixels, or of 128 when the product is
+  // smaller) is measured faster than the dense-tile one once there are
+  // at least 96 tiles of 128 pixels and a reduction of at least 8 of its
+  // 64-channel chunks to pipeline: 2.2-2.4x on 4096^3 FC products, 1.15x on
+  // a 12544 x 1024 x 256 one (98 tiles of 128 pixels), slower on the short
+  // reductions of ResNet-50's other 1x1 layers.
   const bool bf = x_t == CCI_BF16 && val_t == CCI_BF16 && G >= 1 && 64 % G == 0;
   const bool mac_g = G == 2 || G == 4 || G == 8 || G == 16 || G == 32;
-  const int64_t tiles = (N + 255) / 256 * (O / 256);
-  if (bf && C == cin && C % 64 == 0 && C >= 512 && O % 256 == 0 && tiles >= 128) return CCI_ALGO_WIDE_TILE_MFMA;
+  const int64_t tiles = (N + 127) / 128 * (O / 256);
+  if (bf && C == cin && C % 64 == 0 && C >= 512 && O % 256 == 0 && tiles >= 96) return CCI_ALGO_WIDE_TILE_MFMA;
   const bool tile_shape = bf && cin % 32 == 0;
   if (tile_shape && (32 * static_cast<int64_t>(K) > G || !mac_g)) return CCI_ALGO_DENSE_TILE_MFMA;
   return CCI_ALGO_SPARSE_MAC;

@@ -116,7 +116,9 @@ def test_auto_algo_cost_model():
     # large FC / 1x1 products (>= 128 tiles of 256 x 256): wide-tile MFMA, any K
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 4096, 4096, 4096, 4096, 16, 1) == "wide_tile_mfma"
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 4096, 4096, 4096, 4096, 64, 1) == "wide_tile_mfma"
-    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 12544, 1024, 1024, 256, 16, 4) == "dense_tile_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 12544, 1024, 1024, 256, 16, 4) == "wide_tile_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 12544, 256, 256, 1024, 16, 4) == "dense_tile_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 6000, 1024, 1024, 256, 16, 4) == "dense_tile_mfma"
     # G the vector kernels do not support: the tile path even at K/G < 1/32
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 4096, 4096, 4096, 512, 64, 1) == "dense_tile_mfma"
     # fp32, or a reduction the tile path cannot step through: sparse-MAC

@@ -278,10 +278,33 @@ __device__ __forceinline__ void wide_tile_body(const WParams& p, uint8_t* lds) {
     const uint32_t rr = (iword(pold2[u], e >> 2) >> (8 * (e & 3))) & 0xffu;
     *reinterpret_cast<uint16_t*>(tb + ubase[u] + grow(rr) + 2 * e) = 0;
   };
+  // Element order of the in-loop writes of 8-channel units (PERM): lane l
+  // writes element e ^ 2 m2 at step e, m2 = (l / 2) % 4.  Lanes of one
+  // half-wave hit random rows of the same 16-byte column, so in plain order
+  // they collide on the same banks; XOR-ing the column per lane spreads them
+  // over 4x as many.  permute_unit reorders a unit's registers once so that
+  // step e reads its value and index at fixed positions.
+  constexpr bool PERM = UE == 8 && !FULL && !UNSC;
+  const uint32_t m2 = (static_cast<uint32_t>(lane) >> 1) & 3u;
+  uint32_t eoff[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) eoff[e] = PERM ? 2u * (static_cast<uint32_t>(e) ^ (2u * m2)) : 2u * e;
+  auto permute_unit = [&](int u) {
+    if constexpr (PERM) {
+      const bool s1 = (m2 & 1u) != 0, s2 = (m2 & 2u) != 0;
+      const u32x4_t v = pv[u];
+      const u32x4_t t = s1 ? u32x4_t{v[1], v[0], v[3], v[2]} : v;  // element XOR 2: dwords XOR 1
+      pv[u] = s2 ? u32x4_t{t[2], t[3], t[0], t[1]} : t;              // element XOR 4: dwords XOR 2
+      const u32x2_t x = pi[u];
+      const u32x2_t y = s2 ? u32x2_t{x[1], x[0]} : x;               // index bytes XOR 4: dword swap
+      const uint32_t hs = 16u * (m2 & 1u);                           // index bytes XOR 2: half swap
+      pi[u] = u32x2_t{__builtin_amdgcn_alignbit(y[0], y[0], hs), __builtin_amdgcn_alignbit(y[1], y[1], hs)};
+    }
+  };
   auto scatter_e = [&](uint8_t* tb, int u, int e) {  // element e of scatter(tb, u), K < G
     if (!uok[u]) return;
     const uint32_t rr = (iword(pi[u], e >> 2) >> (8 * (e & 3))) & 0xffu;
-    *reinterpret_cast<uint16_t*>(tb + ubase[u] + grow(rr) + 2 * e) = static_cast<uint16_t>(pv[u][e >> 1] >> (16 * (e & 1)));
+    *reinterpret_cast<uint16_t*>(tb + ubase[u] + grow(rr) + eoff[e]) = static_cast<uint16_t>(pv[u][e >> 1] >> (16 * (e & 1)));
   };
   auto scatter_full = [&](uint8_t* tb, int u) {  // K == G: the unit's 16 bytes
     if constexpr (UE == 8) {
@@ -406,6 +429,11 @@ __device__ __forceinline__ void wide_tile_body(const WParams& p, uint8_t* lds) {
           if (i == 0 && g < PT) b1[g % PT] = ld(xb + g * 2048 + boff1);
           if (i == 1) af[g + 8] = ld(wb + (g * 2 + 1) * 1024);
           if constexpr (more1) {
+            if constexpr (PERM) {
+#pragma unroll
+              for (int u = i; u < UPL; u += PT)
+                if (g == 3) permute_unit(u);  // W(j+1) is in registers since chunk j-1 ended
+            }
             if constexpr (FULL) {
               if (g >= 4 && i >= 2 && i < 2 + kUPG) scatter_full(tb, (g - 4) * kUPG + (i - 2));
             } else {

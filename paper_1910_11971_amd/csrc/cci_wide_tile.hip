@@ -152,10 +152,11 @@ __device__ __forceinline__ uint32_t iword(uint32_t v, int) { return v; }
 __device__ __forceinline__ uint32_t trow(uint32_t o) { return ((o >> 4) << 11) | ((o & 15) << 4); }
 
 // A unit is UE (8 or 4) consecutive channels of one packed row; UPL units
-// per lane per chunk.  FULL: K == G (every entry kept, indices ascending, so
+// per lane per chunk; MASK: the units outnumber the packed rows' (some lanes
+// idle), else every lane's units exist and the checks compile away.  FULL: K == G (every entry kept, indices ascending, so
 // a unit is one row's 16 bytes).  BIGG: G > 16 (a group spans 16-row
 // blocks of the tile).
-template <typename YT, int PT, int UPL, int UE, bool FULL, bool BIGG>
+template <typename YT, int PT, int UPL, int UE, bool FULL, bool BIGG, bool MASK>
 __device__ __forceinline__ void wide_tile_body(const WParams& p, uint8_t* lds) {
   constexpr int NW = FULL ? UPL : 2 * UPL;  // vector-memory operations of one packed-chunk load
   const int lane = threadIdx.x & 63;
@@ -218,7 +219,7 @@ __device__ __forceinline__ void wide_tile_body(const WParams& p, uint8_t* lds) {
     const int v = lane + 64 * u;
     const int r = UE == 8 ? v >> 3 : v >> 4;
     const int c = UE == 8 ? (v & 7) * 8 : (v & 15) * 4;
-    uok[u] = r < p.rows_w;
+    uok[u] = !MASK || r < p.rows_w;  // (MASK: some lanes have no unit)
     const uint32_t prow = (ob * 4u + static_cast<uint32_t>(w)) * static_cast<uint32_t>(p.rows_w) + static_cast<uint32_t>(r);
     voff[u] = uok[u] ? (prow * static_cast<uint32_t>(p.C) + static_cast<uint32_t>(c)) * 2u : kOOB;
     ioff[u] = uok[u] ? prow * static_cast<uint32_t>(p.C) + static_cast<uint32_t>(c) : kOOB;
@@ -587,11 +588,11 @@ __device__ __forceinline__ void wide_tile_body(const WParams& p, uint8_t* lds) {
 
 // (The body is a device function: with it inside the kernel template, the
 // host pass of this compiler emitted no launch stubs for the kernels.)
-template <typename YT, int PT, int UPL, int UE, bool FULL, bool BIGG>
+template <typename YT, int PT, int UPL, int UE, bool FULL, bool BIGG, bool MASK>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void wide_tile_kernel(WParams p) {
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
-  wide_tile_body<YT, PT, UPL, UE, FULL, BIGG>(p, lds);
+  wide_tile_body<YT, PT, UPL, UE, FULL, BIGG, MASK>(p, lds);
 }
 
 // Rows of X are pixels: FC, or a 1x1 convolution with unit stride and no
@@ -602,29 +603,35 @@ bool plain_rows(const ProductArgs& a) {
   return g.KH == 1 && g.KW == 1 && g.sh == 1 && g.sw == 1 && g.ph == 0 && g.pw == 0;
 }
 
-template <typename YT, int PT, int UPL, int UE, bool FULL, bool BIGG>
+template <typename YT, int PT, int UPL, int UE, bool FULL, bool BIGG, bool MASK>
 hipError_t launch_wu(const WParams& p, uint32_t grid, hipStream_t s) {
   static const hipError_t attr =
-      hipFuncSetAttribute(reinterpret_cast<const void*>(&wide_tile_kernel<YT, PT, UPL, UE, FULL, BIGG>),
+      hipFuncSetAttribute(reinterpret_cast<const void*>(&wide_tile_kernel<YT, PT, UPL, UE, FULL, BIGG, MASK>),
                           hipFuncAttributeMaxDynamicSharedMemorySize, kLds);
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((wide_tile_kernel<YT, PT, UPL, UE, FULL, BIGG>), dim3(grid), dim3(kThreads), kLds, s, p);
+  hipLaunchKernelGGL((wide_tile_kernel<YT, PT, UPL, UE, FULL, BIGG, MASK>), dim3(grid), dim3(kThreads), kLds, s, p);
   return hipGetLastError();
+}
+
+template <typename YT, int PT, bool BIGG, int UPL>
+hipError_t launch_wm(const WParams& p, uint32_t grid, hipStream_t s) {
+  return p.rows_w == 8 * UPL ? launch_wu<YT, PT, UPL, 8, false, BIGG, false>(p, grid, s)
+                             : launch_wu<YT, PT, UPL, 8, false, BIGG, true>(p, grid, s);
 }
 
 template <typename YT, int PT, bool BIGG>
 hipError_t launch_wg(const WParams& p, uint32_t grid, hipStream_t s) {
   // packed elements per lane per chunk: rows_w (= 64 K / G)
-  if (p.rows_w == 4) return launch_wu<YT, PT, 1, 4, false, BIGG>(p, grid, s);
-  if (p.rows_w <= 8) return launch_wu<YT, PT, 1, 8, false, BIGG>(p, grid, s);
-  if (p.rows_w <= 16) return launch_wu<YT, PT, 2, 8, false, BIGG>(p, grid, s);
-  if (p.rows_w <= 32) return launch_wu<YT, PT, 4, 8, false, BIGG>(p, grid, s);
-  return launch_wu<YT, PT, 8, 8, false, BIGG>(p, grid, s);
+  if (p.rows_w == 4) return launch_wu<YT, PT, 1, 4, false, BIGG, false>(p, grid, s);
+  if (p.rows_w <= 8) return launch_wm<YT, PT, BIGG, 1>(p, grid, s);
+  if (p.rows_w <= 16) return launch_wm<YT, PT, BIGG, 2>(p, grid, s);
+  if (p.rows_w <= 32) return launch_wm<YT, PT, BIGG, 4>(p, grid, s);
+  return launch_wu<YT, PT, 8, 8, false, BIGG, true>(p, grid, s);
 }
 
 template <typename YT, int PT>
 hipError_t launch_wp(const WParams& p, uint32_t grid, hipStream_t s) {
-  if (p.K == p.G) return launch_wu<YT, PT, 8, 8, true, false>(p, grid, s);
+  if (p.K == p.G) return launch_wu<YT, PT, 8, 8, true, false, false>(p, grid, s);
   return p.G > 16 ? launch_wg<YT, PT, true>(p, grid, s) : launch_wg<YT, PT, false>(p, grid, s);
 }
 

@@ -41,7 +41,7 @@ def parse():
     p.add_argument("--steps", type=int, default=200)
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--workload", default="conv3x3")
-    p.add_argument("--algo", default="auto", choices=["auto", "sparse_mac", "dense_tile_mfma", "wide_tile_mfma"])
+    p.add_argument("--algo", default="auto", choices=["auto", "sparse_mac", "dense_tile_mfma", "wide_tile_mfma", "narrow_mfma"])
     p.add_argument("--rotate-mb", type=float, default=600.0,
                    help="total size of rotated X/Y copies (0: no rotation)")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target wall time of the CPU oracle sample")
@@ -53,6 +53,8 @@ def parse():
     p.add_argument("--sweep", action="store_true",
                    help="instead of the headline line: one JSON line per configuration (FC, 1x1, 3x3, "
                         "FC K-sweep, ResNet-50 forward) with CCI and dense bf16 times")
+    p.add_argument("--sweep-only", default="",
+                   help="comma-separated subset of the sweep: config names, 'resnet50', 'mobilenetv2'")
     p.add_argument("--calibrate-copy-mb", type=float, default=0.0,
                    help="only run a plain device copy of this many MB (x5) and exit: the reference "
                         "kernel for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes")
@@ -60,7 +62,7 @@ def parse():
 
 
 KERNEL_SOURCES = {"cci_dense_tile": "cci_dense_tile.hip", "cci_wide_tile": "cci_wide_tile.hip",
-                  "cci_sparse_mac": "cci_sparse_mac.hip"}
+                  "cci_sparse_mac": "cci_sparse_mac.hip", "cci_narrow": "cci_narrow.hip"}
 
 
 def kernel_source_hash(kernel: str = "cci_dense_tile") -> str:
@@ -396,12 +398,13 @@ def _eager_time(fn, n, stream):
 
 
 def kernel_name(algo):
-    return {"dense_tile_mfma": "cci_dense_tile", "wide_tile_mfma": "cci_wide_tile"}.get(algo, "cci_sparse_mac")
+    return {"dense_tile_mfma": "cci_dense_tile", "wide_tile_mfma": "cci_wide_tile",
+            "narrow_mfma": "cci_narrow"}.get(algo, "cci_sparse_mac")
 
 
 def _roof(kname, flop, dense_flop, alg_bytes, t_ms):
     # the matrix-core kernels execute the expanded (dense) product
-    if kname in ("cci_dense_tile", "cci_wide_tile"):
+    if kname in ("cci_dense_tile", "cci_wide_tile", "cci_narrow"):
         t_hbm = alg_bytes / (PEAK["hbm_GBps"] * 1e9)
         t_mfma = dense_flop / (PEAK["mfma_bf16_TFLOPs"] * 1e12)
         if t_hbm >= t_mfma:
@@ -423,6 +426,9 @@ def sweep(args):
     torch.cuda.set_device(dev)
     stream = torch.cuda.Stream(device=dev)
     names = ["fc256", "conv3x3", "conv1x1_k4", "conv1x1_k2"] + [f"fc4096_k{k}" for k in (1, 2, 4, 8, 16)]
+    only = set(x for x in args.sweep_only.split(",") if x)
+    if only:
+        names = [n for n in names if n in only]
     for name in names:
         wl = workloads.WORKLOADS[name]
         X_cpu, W_np = workloads.draw(wl)
@@ -483,7 +489,11 @@ def sweep(args):
         print(json.dumps(out), flush=True)
         del Xs, Ys, W, vals, idx
         torch.cuda.empty_cache()
-    sweep_resnet50(stream)
+    if not only or "resnet50" in only:
+        sweep_resnet50(stream)
+    if not only or "mobilenetv2" in only:
+        for K in (1, 2, 3, 4):
+            sweep_mobilenetv2(stream, K)
 
 
 def sweep_resnet50(stream):
@@ -544,6 +554,85 @@ def sweep_resnet50(stream):
                       "dense_bf16_forward_ms": round(t_dense, 4),
                       "speedup_vs_dense": round(t_dense / t_cci, 3),
                       "images_per_s": round(net.B / (t_cci * 1e-3), 1)}), flush=True)
+
+
+def sweep_mobilenetv2(stream, K, B=64):
+    """The 32 CCI pointwise layers of MobileNetV2 (G = 8, s = K) at batch 64,
+    each on its own synthetic input, run back to back from one HIP graph,
+    against the same 32 products as dense bf16 GEMMs (hipBLASLt).  The
+    layers' operands total about 1 GB, so a replay finds little of a layer in
+    the caches.  Batch norm is folded into the epilogue's scale / bias, with
+    ReLU after the expanding layers (the network's ReLU6 clamp at 6 is not
+    part of the product).  Per-layer times come from graphs of 8 launches of
+    one layer."""
+    import numpy as np
+    import torch
+    from paper_1910_11971_amd import cci, workloads
+
+    dev = torch.device("cuda:0")
+    P = workloads.mobilenetv2_pointwise(B=B, K=K)
+    kinds = [l.kind for l in workloads.mobilenetv2_cci_layers()]
+    Xs, Ys, packs, Wd, As, eps = [], [], [], [], [], []
+    flop = dense_flop = alg_bytes = 0.0
+    for w in P:
+        X_cpu, W_np = workloads.draw(w)
+        Xs.append(X_cpu.to(dev))
+        Ys.append(torch.empty((w.B, w.Ho, w.Wo, w.O), dtype=torch.bfloat16, device=dev))
+        W = torch.from_numpy(W_np).to(dev)
+        packs.append(cci.pack(W, w.G, w.K, torch.bfloat16))
+        Wd.append(W.to(torch.bfloat16).t().contiguous())
+        As.append(Xs[-1].reshape(w.N, w.C))
+        sc, bi = workloads.bn_fold(w.O)  # batch norm folded into the epilogue
+        eps.append((torch.from_numpy(sc).to(dev), torch.from_numpy(bi).to(dev)))
+        flop += 2.0 * w.N * w.nnz
+        dense_flop += 2.0 * w.N * w.C * w.O
+        alg_bytes += 2.0 * w.N * (w.C + w.O) + 3.0 * w.nnz
+    algos = [cci.auto_algo(torch.bfloat16, torch.bfloat16, w.N, w.C, w.Cin, w.O, w.G, w.K) for w in P]
+
+    def layer(i, algo="auto"):
+        w = P[i]
+        vals, idx = packs[i]
+        cci.conv_im2col(Xs[i], vals, idx, w.G, 1, 1, (1, 1), (0, 0), scale=eps[i][0], bias=eps[i][1],
+                        relu=kinds[i] == "expand", out_dtype=torch.bfloat16, out=Ys[i], algo=algo)
+
+    def network(_i):
+        for i in range(len(P)):
+            layer(i)
+
+    def dense(_i):
+        for i in range(len(P)):
+            torch.matmul(As[i], Wd[i])
+
+    t_cci = _graph_time(network, 1, 20, stream)
+    t_dense = _eager_time(dense, 20, stream)
+    try:  # the GEMMs from a graph too (no host launch gaps between the small ones)
+        t_dense_graph = round(_graph_time(dense, 1, 20, stream), 4)
+    except RuntimeError as e:
+        t_dense_graph = f"capture failed: {str(e)[:80]}"
+    per_layer = []
+    for i, w in enumerate(P):
+        t = _graph_time(lambda _j, i=i: layer(i), 8, 5, stream)
+        row = [w.name[5:], w.N, w.C, w.O, algos[i], round(t * 1e3, 2)]
+        alt = {}
+        for a in ("narrow_mfma", "dense_tile_mfma"):  # the other MFMA kernels that take the shape
+            if a == algos[i]:
+                continue
+            try:
+                alt[a] = round(_graph_time(lambda _j, i=i, a=a: layer(i, a), 8, 5, stream) * 1e3, 2)
+            except cci.CCIError:
+                pass
+        per_layer.append(row + [alt])
+    t_hbm = alg_bytes / (PEAK["hbm_GBps"] * 1e9)
+    print(json.dumps({"workload": f"mobilenetv2_pw_k{K}", "B": B, "G": 8, "K": K, "layers": len(P),
+                      "cci_ms": round(t_cci, 4), "eff_TFLOPs": round(flop / (t_cci * 1e-3) / 1e12, 3),
+                      "alg_bytes_MB": round(alg_bytes / 1e6, 1),
+                      "roofline": {"bound": "hbm", "frac": round(t_hbm / (t_cci * 1e-3), 4)},
+                      "dense_gemm_ms_eager": round(t_dense, 4), "dense_gemm_ms_graph": t_dense_graph,
+                      "speedup_vs_dense_gemm": round(t_dense / t_cci, 3),
+                      "algos": {a: algos.count(a) for a in sorted(set(algos))},
+                      "per_layer_us": per_layer}), flush=True)
+    del Xs, Ys, packs, Wd, As, eps
+    torch.cuda.empty_cache()
 
 
 if __name__ == "__main__":

@@ -66,12 +66,22 @@ typedef enum { CCI_F32 = 0, CCI_BF16 = 1 } cci_dtype;
  *                           convolutions with stride 1 and no padding.  Needs
  *                           bf16 X and vals, C % 64 == 0, O % 256 == 0,
  *                           64 % G == 0, X, vals and Y 16-byte aligned and
- *                           idx 8-byte aligned.                              */
+ *                           idx 8-byte aligned.
+ *  CCI_ALGO_NARROW_MFMA     the same expansion for short reductions: a wave
+ *                           keeps the expanded weights of up to 80 outputs
+ *                           in registers and streams pixels through them
+ *                           (the 1x1 layers of narrow networks).  FC or 1x1
+ *                           convolutions with stride 1 and no padding; bf16
+ *                           X and vals, C <= 256, C % 8 == 0, O % 4 == 0,
+ *                           G <= 256; X and vals 16-byte aligned, idx
+ *                           8-byte aligned, Y (and residual) 8-byte aligned
+ *                           for bf16 and 16-byte aligned for fp32 output. */
 typedef enum {
   CCI_ALGO_AUTO = 0,
   CCI_ALGO_SPARSE_MAC = 1,
   CCI_ALGO_DENSE_TILE_MFMA = 2,
-  CCI_ALGO_WIDE_TILE_MFMA = 3
+  CCI_ALGO_WIDE_TILE_MFMA = 3,
+  CCI_ALGO_NARROW_MFMA = 4
 } cci_algo;
 
 /* Optional fused epilogue, applied per output element before rounding:
@@ -137,7 +147,9 @@ cci_status cci_conv_im2col(const void *X, cci_dtype x_t, int64_t B, int64_t H,
 /* Which family CCI_ALGO_AUTO picks for a product of N x C x O (conv: pass
  * N = B*Ho*Wo, C = KH*KW*Cin and cin = Cin; FC: cin = C).  Host-only.  A
  * 1x1 convolution reported as CCI_ALGO_WIDE_TILE_MFMA runs on the dense-tile
- * kernels when its stride or padding rules the wide-tile ones out. */
+ * kernels when its stride or padding rules the wide-tile ones out; one
+ * reported as CCI_ALGO_NARROW_MFMA then runs on the dense-tile kernels if
+ * they take its shape, else on the sparse-MAC ones. */
 cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C,
                        int64_t cin, int64_t O, int32_t G, int32_t K);
 

@@ -68,7 +68,7 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
       (a.residual && !aligned16(a.residual)))
     return fail(CCI_EALIGN, "epilogue pointer not 16-byte aligned");
   if (algo != CCI_ALGO_AUTO && algo != CCI_ALGO_SPARSE_MAC && algo != CCI_ALGO_DENSE_TILE_MFMA &&
-      algo != CCI_ALGO_WIDE_TILE_MFMA)
+      algo != CCI_ALGO_WIDE_TILE_MFMA && algo != CCI_ALGO_NARROW_MFMA)
     return fail(CCI_EINVAL, "unknown algo %d", (int)algo);
   if (a.N == 0) return ok();
 
@@ -84,6 +84,8 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
   // (the shape-only choice cannot see stride and padding)
   if (algo == CCI_ALGO_AUTO && chosen == CCI_ALGO_WIDE_TILE_MFMA && !cci::wide_tile_supports(a))
     chosen = CCI_ALGO_DENSE_TILE_MFMA;
+  if (algo == CCI_ALGO_AUTO && chosen == CCI_ALGO_NARROW_MFMA && !cci::narrow_supports(a))
+    chosen = tile_ok ? CCI_ALGO_DENSE_TILE_MFMA : CCI_ALGO_SPARSE_MAC;
   if (chosen == CCI_ALGO_SPARSE_MAC && !mac_ok)
     return fail(CCI_EUNSUPPORTED, "sparse-MAC kernels need G in {2,4,8,16,32} (G=%d)", a.G);
   if (chosen == CCI_ALGO_DENSE_TILE_MFMA && !tile_ok)
@@ -93,9 +95,14 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
     return fail(CCI_EUNSUPPORTED,
                 "wide-tile MFMA kernels need bf16 X/vals, an FC or stride-1 unpadded 1x1 product, "
                 "C %% 64 == 0, O %% 256 == 0, 64 %% G == 0 and aligned pointers");
+  if (chosen == CCI_ALGO_NARROW_MFMA && !cci::narrow_supports(a))
+    return fail(CCI_EUNSUPPORTED,
+                "narrow MFMA kernels need bf16 X/vals, an FC or stride-1 unpadded 1x1 product, "
+                "C <= 256, C %% 8 == 0, O %% 4 == 0, G <= 256 and aligned pointers");
   const hipStream_t st = static_cast<hipStream_t>(stream);
-  hipError_t e = chosen == CCI_ALGO_SPARSE_MAC  ? cci::launch_sparse_mac(a, st)
+  hipError_t e = chosen == CCI_ALGO_SPARSE_MAC       ? cci::launch_sparse_mac(a, st)
                  : chosen == CCI_ALGO_WIDE_TILE_MFMA ? cci::launch_wide_tile(a, st)
+                 : chosen == CCI_ALGO_NARROW_MFMA    ? cci::launch_narrow(a, st)
                                                      : cci::launch_dense_tile(a, st);
   if (e != hipSuccess) return fail(CCI_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
@@ -160,6 +167,11 @@ cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C, int
   const bool mac_g = G == 2 || G == 4 || G == 8 || G == 16 || G == 32;
   const int64_t tiles = (N + 127) / 128 * (O / 256);
   if (bf && C == cin && C % 64 == 0 && C >= 512 && O % 256 == 0 && tiles >= 96) return CCI_ALGO_WIDE_TILE_MFMA;
+  // Short reductions the tile kernels cannot take (Cin % 32 != 0) stream
+  // through register-resident weights.
+  if (x_t == CCI_BF16 && val_t == CCI_BF16 && C == cin && C <= 256 && C % 8 == 0 && cin % 32 != 0 &&
+      O % 4 == 0)
+    return CCI_ALGO_NARROW_MFMA;
   const bool tile_shape = bf && cin % 32 == 0;
   if (tile_shape && (32 * static_cast<int64_t>(K) > G || !mac_g)) return CCI_ALGO_DENSE_TILE_MFMA;
   return CCI_ALGO_SPARSE_MAC;

@@ -49,6 +49,12 @@ hipError_t launch_dense_tile(const ProductArgs& a, hipStream_t s);
 bool wide_tile_supports(const ProductArgs& a);
 hipError_t launch_wide_tile(const ProductArgs& a, hipStream_t s);
 
+// Short reductions (C <= 256, C % 8 == 0): expanded weights of up to 80
+// outputs per wave held in registers, pixels streamed through them (FC and
+// stride-1 1x1 convolutions; bf16; O % 4 == 0).
+bool narrow_supports(const ProductArgs& a);
+hipError_t launch_narrow(const ProductArgs& a, hipStream_t s);
+
 hipError_t launch_maxpool(const void* X, DType t, int64_t B, int64_t H, int64_t W, int64_t C,
                           int32_t k, int32_t st, int32_t p, void* Y, hipStream_t s);
 hipError_t launch_avgpool(const void* X, DType x_t, int64_t B, int64_t H, int64_t W, int64_t C,

@@ -1,0 +1,330 @@
+// CCI-sparse products with a short reduction (C <= 256): the 1x1 layers of
+// narrow networks (MobileNetV2's expanding and projecting convolutions,
+// Sec. 6) and small FC layers.
+//
+// The method is the one of the tile kernels (Alg. 1's row G g + idx[g][k][c]
+// receives vals[g][k][c]; the expanded product runs on the bf16 matrix
+// cores), with a split for reductions too short to fill a channel pipeline:
+//
+//   - a slice of up to TM output tiles (16 outputs each) belongs to one wave,
+//     which expands the packed groups of its slice once, straight from HBM
+//     into MFMA operand fragments held in registers for the wave's lifetime
+//     (output 16 t + lane % 16, channels 32 s + 8 (lane / 16) .. +7);
+//   - the wave then streams groups of P 16-pixel blocks through them: the
+//     activations of the next group are loaded (16 bytes per lane, rows
+//     zero-padded past C and N by the buffer's range check) while the MFMAs
+//     and the fused epilogue of the current one run;
+//   - the accumulators leave the matrix cores with 4 consecutive outputs of
+//     one pixel per lane; scale / bias (staged in LDS), residual and ReLU are
+//     applied in fp32 and each lane stores 8 (bf16) or 16 (fp32) bytes.
+//
+// Every activation is read from HBM once per slice (slices of one pixel
+// group run in the same workgroup), the packed weights once per wave, and
+// every output is written once.  The layers this serves are bound by HBM
+// bandwidth: their MFMA work is small next to their bytes.
+#include "cci_launch.hpp"
+
+namespace cci {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+constexpr int kThreads = 256;
+constexpr int kMaxC = 256;                // reduction length covered (8 k-steps of 32)
+constexpr int kSliceOut = 80;             // outputs of the largest slice (TM <= 5)
+constexpr int kWavesTarget = 3072;        // resident waves if the runtime cannot say
+constexpr uint32_t kOOB = 0x80000000u;    // buffer offset that reads as zero / drops a store
+constexpr int kRsrcWord3 = 0x00020000;    // raw buffer descriptor word 3 (gfx9 family)
+
+struct NParams {
+  const uint16_t* X;
+  const uint16_t* vals;
+  const uint8_t* idx;
+  const float* scale;
+  const float* bias;
+  const void* residual;
+  void* Y;
+  uint32_t x_bytes, y_bytes;
+  int32_t N, C, O, G, K, relu;
+  int32_t tpw;      // output tiles per slice
+  int32_t nslices;  // slices covering the O / 16 (rounded up) output tiles
+  int32_t npg;      // pixel groups of 16 P pixels
+  int32_t wps;      // waves per slice (set at launch)
+};
+
+// Per k-step count S (= ceil(C / 32)): P 16-pixel blocks per step, at most TM
+// output tiles per slice.  Registers: weights 4 TM S, accumulators 4 TM P,
+// activations 2 x 4 P S (current and next group).
+template <int S>
+struct Shape {
+  static constexpr int P = S == 1 ? 4 : (S == 2 ? 2 : 1);
+  static constexpr int TM = S == 1 ? 4 : (S <= 3 ? 5 : (S == 4 ? 4 : (S <= 6 ? 3 : 2)));
+  static_assert(16 * TM <= kSliceOut, "slice staging");
+};
+
+__device__ __forceinline__ float relu_f(float y) { return y > 0.0f ? y : (y != y ? y : 0.0f); }
+
+template <typename YT, int S>
+__device__ __forceinline__ void narrow_body(const NParams& p, float* sb) {
+  constexpr int P = Shape<S>::P, TM = Shape<S>::TM;
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int gw = static_cast<int>(blockIdx.x) * (kThreads / 64) + w;
+  if (gw >= p.nslices * p.wps) return;  // whole wave: no barriers below
+  const int slice = gw % p.nslices;
+  const int wv = gw / p.nslices;
+  const int t0 = slice * p.tpw;                           // first output tile of the slice
+  const int tw = min(p.tpw, (p.O + 15) / 16 - t0);        // tiles of this slice
+  const int ol = lane & 15, kq = lane >> 4;
+
+  // ---- scale / bias of the slice's outputs, staged in this wave's LDS ------
+  float* ss = sb + w * 2 * kSliceOut;
+  for (int i = lane; i < 16 * tw; i += 64) {
+    const int o = 16 * t0 + i;
+    ss[i] = (p.scale && o < p.O) ? p.scale[o] : 1.0f;
+    ss[kSliceOut + i] = (p.bias && o < p.O) ? p.bias[o] : 0.0f;
+  }
+
+  // ---- expanded weights: fragment (t, s) of output 16 (t0 + t) + ol --------
+  // Each (group, channel) keeps K entries with distinct rows, so at most one
+  // slot matches a row; slots and channels past the slice or C stay zero.
+  bf16x8_t wf[TM][S];
+#pragma unroll
+  for (int t = 0; t < TM; ++t) {
+    const int o = 16 * (t0 + t) + ol;
+    const bool orow = t < tw && o < p.O;
+    const int g = orow ? o / p.G : 0;
+    const uint32_t r = static_cast<uint32_t>(orow ? o - g * p.G : 0);
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+      const int c = 32 * s + 8 * kq;
+      u32x4_t acc{0u, 0u, 0u, 0u};
+      if (orow && c < p.C) {
+        for (int kk = 0; kk < p.K; ++kk) {
+          const int64_t e = (static_cast<int64_t>(g) * p.K + kk) * p.C + c;
+          const u32x4_t v = *reinterpret_cast<const u32x4_t*>(p.vals + e);
+          const u32x2_t ix = *reinterpret_cast<const u32x2_t*>(p.idx + e);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const uint32_t row = (ix[j >> 2] >> (8 * (j & 3))) & 0xffu;
+            const uint32_t half = (j & 1) ? 0xffff0000u : 0x0000ffffu;
+            acc[j >> 1] |= row == r ? (v[j >> 1] & half) : 0u;
+          }
+        }
+      }
+      wf[t][s] = __builtin_bit_cast(bf16x8_t, acc);
+    }
+  }
+
+  // ---- stream pixel groups --------------------------------------------------
+  const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(p.X), (short)0, static_cast<int>(p.x_bytes), kRsrcWord3);
+  const __amdgpu_buffer_rsrc_t yr =
+      __builtin_amdgcn_make_buffer_rsrc(p.Y, (short)0, static_cast<int>(p.y_bytes), kRsrcWord3);
+  const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(p.residual), (short)0, p.residual ? static_cast<int>(p.y_bytes) : 0, kRsrcWord3);
+  const uint32_t N = static_cast<uint32_t>(p.N), C = static_cast<uint32_t>(p.C), O = static_cast<uint32_t>(p.O);
+  // B fragment of block b, k-step s: pixel 16 b + ol of the group, channels
+  // 32 s + 8 kq .. +7 (zero past C or N)
+  auto load_group = [&](int pg, bf16x8_t (&xf)[P][S]) {
+#pragma unroll
+    for (int b = 0; b < P; ++b) {
+      const uint32_t n = static_cast<uint32_t>(pg) * (16u * P) + 16u * b + static_cast<uint32_t>(ol);
+#pragma unroll
+      for (int s = 0; s < S; ++s) {
+        const uint32_t c = 32u * s + 8u * static_cast<uint32_t>(kq);
+        const uint32_t off = (n < N && c < C) ? (n * C + c) * 2u : kOOB;
+        xf[b][s] = __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0));
+      }
+    }
+  };
+
+  int pg = wv;
+  if (pg >= p.npg) return;
+  bf16x8_t xc[P][S], xn[P][S];
+  load_group(pg, xc);
+  constexpr uint32_t ysz = sizeof(YT);
+  while (true) {
+    const int pn = pg + p.wps;
+    load_group(pn, xn);  // past the last group: every offset is out of range
+    f32x4_t acc[P][TM];
+#pragma unroll
+    for (int b = 0; b < P; ++b)
+#pragma unroll
+      for (int t = 0; t < TM; ++t) {
+        acc[b][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        if (t < tw) {
+#pragma unroll
+          for (int s = 0; s < S; ++s)
+            acc[b][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[t][s], xc[b][s], acc[b][t], 0, 0, 0);
+        }
+      }
+    // epilogue: lane holds outputs 16 (t0 + t) + 4 kq .. +3 of pixel 16 b + ol
+#pragma unroll
+    for (int b = 0; b < P; ++b) {
+      const uint32_t n = static_cast<uint32_t>(pg) * (16u * P) + 16u * b + static_cast<uint32_t>(ol);
+#pragma unroll
+      for (int t = 0; t < TM; ++t) {
+        if (t >= tw) continue;
+        const int oi = 16 * t + 4 * kq;  // within the slice
+        const uint32_t o = static_cast<uint32_t>(16 * t0 + oi);
+        const uint32_t off = (n < N && o < O) ? (n * O + o) * ysz : kOOB;
+        const f32x4_t sc = *reinterpret_cast<const f32x4_t*>(ss + oi);
+        const f32x4_t bi = *reinterpret_cast<const f32x4_t*>(ss + kSliceOut + oi);
+        f32x4_t y = acc[b][t] * sc + bi;
+        if (p.residual) {
+          if constexpr (ysz == 2) {
+            const u32x2_t q = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(rr, off, 0, 0));
+            y[0] += __uint_as_float(q[0] << 16);
+            y[1] += __uint_as_float(q[0] & 0xffff0000u);
+            y[2] += __uint_as_float(q[1] << 16);
+            y[3] += __uint_as_float(q[1] & 0xffff0000u);
+          } else {
+            y += __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rr, off, 0, 0));
+          }
+        }
+        if (p.relu) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) y[e] = relu_f(y[e]);
+        }
+        if constexpr (ysz == 2) {
+          // v_cvt_pk_bf16_f32: round to nearest even
+          const u32x2_t pk = {__builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{y[0], y[1]}), bf16x2_t)),
+                              __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{y[2], y[3]}), bf16x2_t))};
+          __builtin_amdgcn_raw_buffer_store_b64(
+              __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b64(yr, 0, 0, 0)), pk), yr, off, 0, 0);
+        } else {
+          __builtin_amdgcn_raw_buffer_store_b128(
+              __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b128(yr, 0, 0, 0)), y), yr, off, 0, 0);
+        }
+      }
+    }
+    if (pn >= p.npg) break;
+    pg = pn;
+#pragma unroll
+    for (int b = 0; b < P; ++b)
+#pragma unroll
+      for (int s = 0; s < S; ++s) xc[b][s] = xn[b][s];
+  }
+}
+
+// (The body is a device function: with it inside the kernel template, the
+// host pass of this compiler emitted no launch stubs for the kernels.)
+template <typename YT, int S>
+__global__ __launch_bounds__(kThreads) void narrow_kernel(NParams p) {
+  __shared__ __attribute__((aligned(16))) float sb[(kThreads / 64) * 2 * kSliceOut];
+  narrow_body<YT, S>(p, sb);
+}
+
+// Waves of narrow_kernel<YT, S> that fit on the device at once (queried once).
+template <typename YT, int S>
+int64_t resident_waves() {
+  static const int64_t waves = [] {
+    int dev = 0, cus = 0, blocks = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, reinterpret_cast<const void*>(&narrow_kernel<YT, S>),
+                                                     kThreads, 0) != hipSuccess ||
+        cus < 1 || blocks < 1)
+      return static_cast<int64_t>(kWavesTarget);
+    return static_cast<int64_t>(cus) * blocks * (kThreads / 64);
+  }();
+  return waves;
+}
+
+// One wave per (slice, pixel group) when that fits on the device at once;
+// otherwise as many waves as are resident, each streaming several groups.
+template <typename YT, int S>
+hipError_t launch_k(NParams p, hipStream_t s) {
+  const int64_t per_slice = std::max<int64_t>(1, resident_waves<YT, S>() / p.nslices);
+  p.wps = static_cast<int32_t>(std::min<int64_t>(p.npg, per_slice));
+  const int64_t waves = static_cast<int64_t>(p.nslices) * p.wps;
+  const uint32_t grid = static_cast<uint32_t>((waves + 3) / 4);
+  hipLaunchKernelGGL((narrow_kernel<YT, S>), dim3(grid), dim3(kThreads), 0, s, p);
+  return hipGetLastError();
+}
+
+template <typename YT>
+hipError_t launch_s(const NParams& p, int S, hipStream_t s) {
+  switch (S) {
+    case 1: return launch_k<YT, 1>(p, s);
+    case 2: return launch_k<YT, 2>(p, s);
+    case 3: return launch_k<YT, 3>(p, s);
+    case 4: return launch_k<YT, 4>(p, s);
+    case 5: return launch_k<YT, 5>(p, s);
+    case 6: return launch_k<YT, 6>(p, s);
+    case 7: return launch_k<YT, 7>(p, s);
+    case 8: return launch_k<YT, 8>(p, s);
+    default: return hipErrorInvalidConfiguration;
+  }
+}
+
+int max_tiles(int S) {
+  switch (S) {
+    case 1: return Shape<1>::TM;
+    case 2: return Shape<2>::TM;
+    case 3: return Shape<3>::TM;
+    case 4: return Shape<4>::TM;
+    case 5: return Shape<5>::TM;
+    case 6: return Shape<6>::TM;
+    case 7: return Shape<7>::TM;
+    default: return Shape<8>::TM;
+  }
+}
+int pixel_blocks(int S) { return S == 1 ? Shape<1>::P : (S == 2 ? Shape<2>::P : 1); }
+
+}  // namespace
+
+bool narrow_supports(const ProductArgs& a) {
+  if (a.x_t != DType::BF16 || a.val_t != DType::BF16) return false;
+  if (a.conv) {  // a 1x1 convolution with unit stride and no padding: rows are pixels
+    const ConvGeom& g = a.geom;
+    if (!(g.KH == 1 && g.KW == 1 && g.sh == 1 && g.sw == 1 && g.ph == 0 && g.pw == 0)) return false;
+  }
+  if (a.G < 1 || a.G > 256 || a.K < 1 || a.K > a.G || a.O % a.G != 0) return false;
+  if (a.C < 1 || a.C > kMaxC || a.C % 8 != 0 || a.O % 4 != 0 || a.N < 1) return false;
+  const auto al = [](const void* q, uintptr_t m) { return (reinterpret_cast<uintptr_t>(q) & (m - 1)) == 0; };
+  const uintptr_t ya = a.y_t == DType::F32 ? 16 : 8;
+  if (!al(a.X, 16) || !al(a.vals, 16) || !al(a.idx, 8) || !al(a.Y, ya)) return false;
+  if ((a.scale && !al(a.scale, 4)) || (a.bias && !al(a.bias, 4)) || (a.residual && !al(a.residual, ya)))
+    return false;
+  // every buffer offset is 32-bit and stays below the out-of-range marker
+  const int64_t lim = static_cast<int64_t>(kOOB);
+  if (a.N * a.C * 2 >= lim || a.N * a.O * (a.y_t == DType::F32 ? 4 : 2) >= lim) return false;
+  return true;
+}
+
+hipError_t launch_narrow(const ProductArgs& a, hipStream_t s) {
+  if (!narrow_supports(a)) return hipErrorInvalidConfiguration;
+  NParams p{};
+  p.X = static_cast<const uint16_t*>(a.X);
+  p.vals = static_cast<const uint16_t*>(a.vals);
+  p.idx = a.idx;
+  p.scale = a.scale;
+  p.bias = a.bias;
+  p.residual = a.residual;
+  p.Y = a.Y;
+  p.x_bytes = static_cast<uint32_t>(a.N * a.C * 2);
+  p.y_bytes = static_cast<uint32_t>(a.N * a.O * (a.y_t == DType::F32 ? 4 : 2));
+  p.N = static_cast<int32_t>(a.N);
+  p.C = static_cast<int32_t>(a.C);
+  p.O = static_cast<int32_t>(a.O);
+  p.G = a.G;
+  p.K = a.K;
+  p.relu = a.relu;
+  const int S = static_cast<int>((a.C + 31) / 32);
+  const int tiles = static_cast<int>((a.O + 15) / 16);
+  const int tm = max_tiles(S);
+  p.nslices = (tiles + tm - 1) / tm;
+  p.tpw = (tiles + p.nslices - 1) / p.nslices;  // balanced slices
+  p.nslices = (tiles + p.tpw - 1) / p.tpw;
+  const int64_t gp = 16 * static_cast<int64_t>(pixel_blocks(S));
+  p.npg = static_cast<int32_t>((a.N + gp - 1) / gp);
+  return a.y_t == DType::F32 ? launch_s<float>(p, S, s) : launch_s<uint16_t>(p, S, s);
+}
+
+}  // namespace cci

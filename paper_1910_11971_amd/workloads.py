@@ -26,6 +26,10 @@ The layer shapes stand in for the paper's ImageNet / CIFAR CNN layers
              dense (K=G), fp32 logits.  Draw order: images, then every conv in
              network order (stem, then per bottleneck c1, c2, c3, downsample),
              then the FC.
+  mobilenetv2 (pointwise)  the 32 sparse 1x1 convs of MobileNetV2 (width 1,
+             224x224) at batch 64, G=8, K in {1,2,3,4}, each an independent
+             layer: X bf16 ~ N(0,1) for expanding layers, ~ ReLU(N(0,1)) for
+             projecting ones; W ~ N(0, 2/Cin); layer i seeded with seed + i.
 """
 from __future__ import annotations
 
@@ -233,3 +237,109 @@ def bn_fold(C: int):
     into a per-channel scale and bias (fp32 numpy)."""
     scale = np.full(C, 1.0 / np.sqrt(1.0 + BN_EPS), np.float32)
     return scale, np.zeros(C, np.float32)
+
+
+# ---------------------------------------------------------------------------
+# MobileNetV2: the network the paper sparsifies on its pointwise layers only
+# (Sec. 6, G = 8, s = 1..4)
+
+# inverted-residual stages of MobileNetV2 (Sandler et al. 2018, Table 2):
+# (expansion t, output channels c, blocks n, stride of the first block s)
+MBV2_STAGES = ((1, 16, 1, 1), (6, 24, 2, 2), (6, 32, 3, 2), (6, 64, 4, 2),
+               (6, 96, 3, 1), (6, 160, 3, 2), (6, 320, 1, 1))
+
+
+def round_channels(v: float, d: int = 8) -> int:
+    """Channel count for a width multiplier: the nearest multiple of d (at
+    least d), raised by d when rounding lost more than 10%."""
+    n = max(d, int(v + d / 2) // d * d)
+    return n + d if n < 0.9 * v else n
+
+
+@dataclass(frozen=True)
+class NetLayer:
+    name: str
+    kind: str        # "stem" | "expand" | "depthwise" | "project" | "last" | "fc"
+    Cin: int
+    Cout: int
+    k: int
+    stride: int
+    H: int           # input height (= width)
+    residual: bool = False   # project layers: output added to the block input
+
+    @property
+    def Ho(self) -> int:
+        if self.kind == "fc":
+            return 1
+        return (self.H + 2 * (self.k // 2) - self.k) // self.stride + 1
+
+    @property
+    def weights(self) -> int:
+        """Weight (and, for the classifier, bias) parameters; batch norm not counted."""
+        if self.kind == "depthwise":
+            return self.k * self.k * self.Cout
+        if self.kind == "fc":
+            return self.Cin * self.Cout + self.Cout
+        return self.k * self.k * self.Cin * self.Cout
+
+    @property
+    def macs(self) -> int:
+        """Multiply-accumulates per image."""
+        if self.kind == "fc":
+            return self.Cin * self.Cout
+        per_px = self.k * self.k * (self.Cout if self.kind == "depthwise" else self.Cin * self.Cout)
+        return per_px * self.Ho * self.Ho
+
+
+def mobilenetv2_layers(width: float = 1.0, res: int = 224, classes: int = 1000) -> list[NetLayer]:
+    """Every weight layer of MobileNetV2 in network order: 3x3 stem (stride
+    2), then per block an expanding 1x1 conv (absent when t = 1), a 3x3
+    depthwise conv carrying the stride and a projecting 1x1 conv (residual
+    when the stride is 1 and the channel count is kept), then a 1x1 conv to
+    1280 channels, global pooling and the classifier."""
+    L = [NetLayer("stem", "stem", 3, round_channels(32 * width), 3, 2, res)]
+    h = L[0].Ho
+    cin = L[0].Cout
+    for si, (t, c, n, s) in enumerate(MBV2_STAGES):
+        cout = round_channels(c * width)
+        for bi in range(n):
+            st = s if bi == 0 else 1
+            hid = cin * t
+            pre = f"b{si + 1}.{bi}"
+            if t != 1:
+                L.append(NetLayer(f"{pre}.expand", "expand", cin, hid, 1, 1, h))
+            dw = NetLayer(f"{pre}.dw", "depthwise", hid, hid, 3, st, h)
+            L.append(dw)
+            h = dw.Ho
+            L.append(NetLayer(f"{pre}.project", "project", hid, cout, 1, 1, h,
+                              residual=(st == 1 and cin == cout)))
+            cin = cout
+    last = round_channels(1280 * max(1.0, width))
+    L.append(NetLayer("last", "last", cin, last, 1, 1, h))
+    L.append(NetLayer("fc", "fc", last, classes, 1, 1, 1))
+    return L
+
+
+def mobilenetv2_cci_layers(width: float = 1.0, res: int = 224) -> list[NetLayer]:
+    """The pointwise layers that carry CCI sparsity: every expanding and
+    projecting 1x1 conv of the inverted-residual blocks except the first
+    block's projection (32 -> 16 at 112x112).  With that reading (and the
+    1280-channel conv, the stem, the depthwise convs and the classifier
+    dense) the network's weight and MAC counts agree with the paper's table
+    of lightweight-architecture benchmarks (appendix) to 0.3%."""
+    return [l for l in mobilenetv2_layers(width, res)
+            if l.kind in ("expand", "project") and l.name != "b1.0.project"]
+
+
+def mobilenetv2_pointwise(B: int = 64, K: int = 2, G: int = 8, res: int = 224, seed: int = 0) -> list[Workload]:
+    """The CCI pointwise layers of MobileNetV2 at batch B as independent 1x1
+    conv workloads (G, K from the paper's sweep).  Inputs of expanding layers
+    are a projection's linear output ~ N(0,1); inputs of projecting layers
+    follow a ReLU6 ~ ReLU(N(0,1)).  W ~ N(0, 2/Cin).  Layer i draws with seed
+    + i."""
+    out = []
+    for i, l in enumerate(mobilenetv2_cci_layers(1.0, res)):
+        out.append(conv(f"mbv2.{l.name}", B, l.H, l.H, l.Cin, l.Cout, 1, 1, 0, G=G, K=K,
+                        x_dist="relu_normal" if l.kind == "project" else "normal",
+                        w_std=(2.0 / l.Cin) ** 0.5, seed=seed + i))
+    return out

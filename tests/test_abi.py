@@ -89,6 +89,22 @@ def test_explicit_algo_requirements():
                                    FAKE, 256, 8, 2, None, FAKE, cci.BF16, W, None) == cci.EUNSUPPORTED
 
 
+def test_narrow_algo_requirements():
+    # narrow MFMA: bf16, C <= 256, C % 8 == 0, O % 4 == 0; strided / padded / k x k convs refused
+    Nw = cci.ALGO_NARROW_MFMA
+    assert lib.cci_spmm(FAKE, cci.BF16, 4, 264, FAKE, cci.BF16, FAKE, 16, 8, 2, None, FAKE,
+                        cci.BF16, Nw, None) == cci.EUNSUPPORTED
+    assert lib.cci_spmm(FAKE, cci.BF16, 4, 20, FAKE, cci.BF16, FAKE, 16, 8, 2, None, FAKE,
+                        cci.BF16, Nw, None) == cci.EUNSUPPORTED
+    assert lib.cci_spmm(FAKE, cci.BF16, 4, 16, FAKE, cci.BF16, FAKE, 18, 2, 1, None, FAKE,
+                        cci.BF16, Nw, None) == cci.EUNSUPPORTED
+    assert lib.cci_spmm(FAKE, cci.F32, 4, 16, FAKE, cci.F32, FAKE, 16, 8, 2, None, FAKE,
+                        cci.F32, Nw, None) == cci.EUNSUPPORTED
+    for KH, sh, ph in [(3, 1, 1), (1, 2, 0), (1, 1, 1)]:
+        assert lib.cci_conv_im2col(FAKE, cci.BF16, 1, 8, 8, 24, KH, KH, sh, sh, ph, ph, FAKE, cci.BF16,
+                                   FAKE, 96, 8, 2, None, FAKE, cci.BF16, Nw, None) == cci.EUNSUPPORTED
+
+
 def test_empty_is_a_noop():
     # N == 0: nothing to do, no pointer is needed or touched
     assert lib.cci_spmm(None, cci.BF16, 0, 64, None, cci.BF16, None, 16, 8, 2, None, None,
@@ -124,6 +140,10 @@ def test_auto_algo_cost_model():
     # fp32, or a reduction the tile path cannot step through: sparse-MAC
     assert cci.auto_algo(torch.float32, torch.float32, 64, 256, 256, 256, 8, 4) == "sparse_mac"
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 1000, 147, 3, 64, 8, 8) == "sparse_mac"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 1000, 45, 45, 64, 8, 2) == "sparse_mac"
+    # short reductions the tile path cannot step through (MobileNetV2's 16 / 24 / 144 channels)
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 802816, 16, 16, 96, 8, 2) == "narrow_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 200704, 144, 144, 24, 8, 1) == "narrow_mfma"
 
 
 @pytest.mark.skipif(torch.cuda.is_available(), reason="checks the no-device error path only")

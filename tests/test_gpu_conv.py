@@ -79,6 +79,15 @@ def test_conv1x1_wide_tile(B, H, W, Cin, O, G, K):
     run_conv(X, rand_w(O, Cin, O + 1), G, K, 1, 1, 0, torch.bfloat16, "wide_tile_mfma", ep=ep)
 
 
+@pytest.mark.parametrize("B,H,W,Cin,O,G,K", [(2, 7, 9, 24, 144, 8, 3), (3, 11, 5, 144, 32, 8, 1),
+                                             (1, 28, 28, 16, 96, 8, 2)])
+def test_conv1x1_narrow(B, H, W, Cin, O, G, K):
+    need_gpu()
+    X = rand_x((B, H, W, Cin), torch.bfloat16, Cin + O)
+    ep = rand_epilogue(O, B * H * W, torch.bfloat16, 5, relu=True)
+    run_conv(X, rand_w(O, Cin, O), G, K, 1, 1, 0, torch.bfloat16, "narrow_mfma", ep=ep)
+
+
 @pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma"])
 def test_conv_epilogue_residual_relu(algo):
     need_gpu()

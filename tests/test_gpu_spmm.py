@@ -77,6 +77,22 @@ def test_spmm_bf16_wide_tile(N, C, O, G, K):
     run_case(rand_x(N, C, torch.bfloat16, N + C), rand_w(O, C, O + G), G, K, torch.bfloat16, "wide_tile_mfma")
 
 
+NARROW_CASES = [  # N, C, O, G, K: every k-step count 1..8, ragged N and O, one to 30 slices, G 2..256
+    (1, 8, 16, 8, 2), (37, 16, 96, 8, 2), (1000, 24, 144, 8, 3), (333, 40, 36, 4, 1),
+    (2049, 72, 100, 4, 4), (129, 104, 64, 16, 5), (700, 136, 24, 8, 1), (90, 168, 192, 32, 7),
+    (515, 200, 80, 16, 16), (300, 256, 960, 64, 9), (5000, 144, 32, 8, 2), (64, 32, 256, 256, 3),
+    (4500, 64, 8, 2, 1),
+    # waves that stream more than one pixel group
+    (3000, 256, 960, 64, 9), (70000, 136, 24, 8, 1),
+]
+
+
+@pytest.mark.parametrize("N,C,O,G,K", NARROW_CASES)
+def test_spmm_bf16_narrow(N, C, O, G, K):
+    need_gpu()
+    run_case(rand_x(N, C, torch.bfloat16, N + C), rand_w(O, C, O + G), G, K, torch.bfloat16, "narrow_mfma")
+
+
 def test_spmm_wide_tile_repeat_is_identical():
     """Two launches on the same inputs give the same bytes (no state carried between launches)."""
     need_gpu()
@@ -89,7 +105,7 @@ def test_spmm_wide_tile_repeat_is_identical():
     assert torch.equal(Y1.view(torch.int16), Y2.view(torch.int16))
 
 
-@pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma", "wide_tile_mfma"])
+@pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma", "wide_tile_mfma", "narrow_mfma"])
 def test_spmm_bf16_in_f32_out_with_epilogue(algo):
     need_gpu()
     N, C, O, G, K = 777, 128, 256, 8, 2
@@ -97,7 +113,7 @@ def test_spmm_bf16_in_f32_out_with_epilogue(algo):
     run_case(rand_x(N, C, torch.bfloat16, 1), rand_w(O, C, 2), G, K, torch.float32, algo, ep=ep)
 
 
-@pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma", "wide_tile_mfma"])
+@pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma", "wide_tile_mfma", "narrow_mfma"])
 def test_spmm_bf16_epilogue_bf16_residual(algo):
     need_gpu()
     N, C, O, G, K = 300, 64, 256, 16, 4

@@ -82,46 +82,8 @@ __device__ __forceinline__ void narrow_body(const NParams& p, float* sb) {
   const int tw = min(p.tpw, (p.O + 15) / 16 - t0);        // tiles of this slice
   const int ol = lane & 15, kq = lane >> 4;
 
-  // ---- scale / bias of the slice's outputs, staged in this wave's LDS ------
-  float* ss = sb + w * 2 * kSliceOut;
-  for (int i = lane; i < 16 * tw; i += 64) {
-    const int o = 16 * t0 + i;
-    ss[i] = (p.scale && o < p.O) ? p.scale[o] : 1.0f;
-    ss[kSliceOut + i] = (p.bias && o < p.O) ? p.bias[o] : 0.0f;
-  }
-
-  // ---- expanded weights: fragment (t, s) of output 16 (t0 + t) + ol --------
-  // Each (group, channel) keeps K entries with distinct rows, so at most one
-  // slot matches a row; slots and channels past the slice or C stay zero.
-  bf16x8_t wf[TM][S];
-#pragma unroll
-  for (int t = 0; t < TM; ++t) {
-    const int o = 16 * (t0 + t) + ol;
-    const bool orow = t < tw && o < p.O;
-    const int g = orow ? o / p.G : 0;
-    const uint32_t r = static_cast<uint32_t>(orow ? o - g * p.G : 0);
-#pragma unroll
-    for (int s = 0; s < S; ++s) {
-      const int c = 32 * s + 8 * kq;
-      u32x4_t acc{0u, 0u, 0u, 0u};
-      if (orow && c < p.C) {
-        for (int kk = 0; kk < p.K; ++kk) {
-          const int64_t e = (static_cast<int64_t>(g) * p.K + kk) * p.C + c;
-          const u32x4_t v = *reinterpret_cast<const u32x4_t*>(p.vals + e);
-          const u32x2_t ix = *reinterpret_cast<const u32x2_t*>(p.idx + e);
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const uint32_t row = (ix[j >> 2] >> (8 * (j & 3))) & 0xffu;
-            const uint32_t half = (j & 1) ? 0xffff0000u : 0x0000ffffu;
-            acc[j >> 1] |= row == r ? (v[j >> 1] & half) : 0u;
-          }
-        }
-      }
-      wf[t][s] = __builtin_bit_cast(bf16x8_t, acc);
-    }
-  }
-
-  // ---- stream pixel groups --------------------------------------------------
+  // ---- pixel groups: the first group's activations are loaded before the
+  // weights are expanded, so the two latencies overlap ----------------------
   const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(p.X), (short)0, static_cast<int>(p.x_bytes), kRsrcWord3);
   const __amdgpu_buffer_rsrc_t yr =
@@ -148,6 +110,74 @@ __device__ __forceinline__ void narrow_body(const NParams& p, float* sb) {
   if (pg >= p.npg) return;
   bf16x8_t xc[P][S], xn[P][S];
   load_group(pg, xc);
+
+  // ---- scale / bias of the slice's outputs, staged in this wave's LDS ------
+  float* ss = sb + w * 2 * kSliceOut;
+  for (int i = lane; i < 16 * tw; i += 64) {
+    const int o = 16 * t0 + i;
+    ss[i] = (p.scale && o < p.O) ? p.scale[o] : 1.0f;
+    ss[kSliceOut + i] = (p.bias && o < p.O) ? p.bias[o] : 0.0f;
+  }
+
+  // ---- expanded weights: fragment (t, s) of output 16 (t0 + t) + ol --------
+  // Each (group, channel) keeps K entries with distinct rows, so at most one
+  // slot matches a row; slots and channels past the slice or C stay zero.
+  // The loads of up to 8 fragments are issued together, slot by slot
+  // (ceil(TM / TC) K rounds of memory latency rather than TM S K, with a
+  // bounded number of registers in flight).
+  constexpr int TC = 8 / S >= TM ? TM : (8 / S < 1 ? 1 : 8 / S);
+  int64_t ebase[TM];
+  uint32_t rrow[TM];
+  bool tok[TM];
+#pragma unroll
+  for (int t = 0; t < TM; ++t) {
+    const int o = 16 * (t0 + t) + ol;
+    tok[t] = t < tw && o < p.O;
+    const int g = tok[t] ? o / p.G : 0;
+    rrow[t] = static_cast<uint32_t>(tok[t] ? o - g * p.G : 0);
+    ebase[t] = static_cast<int64_t>(g) * p.K * p.C;
+  }
+  u32x4_t wacc[TM][S];
+#pragma unroll
+  for (int t = 0; t < TM; ++t)
+#pragma unroll
+    for (int s = 0; s < S; ++s) wacc[t][s] = u32x4_t{0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int tc = 0; tc < TM; tc += TC) {
+    for (int kk = 0; kk < p.K; ++kk) {
+      u32x4_t v[TC][S];
+      u32x2_t ix[TC][S];
+#pragma unroll
+      for (int u = 0; u < TC; ++u)
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+          const int t = tc + u < TM ? tc + u : TM - 1;
+          const int c = 32 * s + 8 * kq;
+          const bool ok = tc + u < TM && tok[t] && c < p.C;
+          const int64_t e = ebase[t] + static_cast<int64_t>(kk) * p.C + c;
+          v[u][s] = ok ? *reinterpret_cast<const u32x4_t*>(p.vals + e) : u32x4_t{0u, 0u, 0u, 0u};
+          ix[u][s] = ok ? *reinterpret_cast<const u32x2_t*>(p.idx + e) : u32x2_t{0xffffffffu, 0xffffffffu};
+        }
+#pragma unroll
+      for (int u = 0; u < TC; ++u) {
+        if (tc + u >= TM) continue;
+#pragma unroll
+        for (int s = 0; s < S; ++s)
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const uint32_t row = (ix[u][s][j >> 2] >> (8 * (j & 3))) & 0xffu;
+            const uint32_t half = (j & 1) ? 0xffff0000u : 0x0000ffffu;
+            wacc[tc + u][s][j >> 1] |= row == rrow[tc + u] ? (v[u][s][j >> 1] & half) : 0u;
+          }
+      }
+    }
+  }
+  bf16x8_t wf[TM][S];
+#pragma unroll
+  for (int t = 0; t < TM; ++t)
+#pragma unroll
+    for (int s = 0; s < S; ++s) wf[t][s] = __builtin_bit_cast(bf16x8_t, wacc[t][s]);
+
   constexpr uint32_t ysz = sizeof(YT);
   while (true) {
     const int pn = pg + p.wps;

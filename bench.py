@@ -55,6 +55,7 @@ def parse():
                         "FC K-sweep, ResNet-50 forward) with CCI and dense bf16 times")
     p.add_argument("--sweep-only", default="",
                    help="comma-separated subset of the sweep: config names, 'resnet50', 'mobilenetv2'")
+    p.add_argument("--mbv2-k", default="1,2,3,4", help="kept weights per group of the MobileNetV2 sweep lines")
     p.add_argument("--calibrate-copy-mb", type=float, default=0.0,
                    help="only run a plain device copy of this many MB (x5) and exit: the reference "
                         "kernel for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes")
@@ -492,7 +493,7 @@ def sweep(args):
     if not only or "resnet50" in only:
         sweep_resnet50(stream)
     if not only or "mobilenetv2" in only:
-        for K in (1, 2, 3, 4):
+        for K in (int(k) for k in args.mbv2_k.split(",")):
             sweep_mobilenetv2(stream, K)
 
 

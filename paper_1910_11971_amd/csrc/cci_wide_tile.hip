@@ -403,15 +403,17 @@ __device__ __forceinline__ void wide_tile_body(const WParams& p, uint8_t* lds) {
     for (int g = 0; g < 8; ++g) af[g] = ld(wb + g * 2048);
   };
   constexpr int kUPG = (UPL + 3) / 4;  // packed units per group (groups 0-3 clear, 4-7 write)
-  auto chunk = [&](int j, auto m1, auto m2, auto m3) {
+  // xbuf = j % 3 and tbit = j % 2 select the buffers; the unrolled steady
+  // state passes them as literals, so every LDS address of a chunk (the DMA
+  // targets in M0 included) is a constant offset from the wave's base.
+  auto chunk = [&](int j, int xbuf, int tbit, auto m1, auto m2, auto m3) __attribute__((always_inline)) {
     constexpr bool more1 = decltype(m1)::value, more2 = decltype(m2)::value, more3 = decltype(m3)::value;
-    const int xbuf = j % 3;
     const uint8_t* xb = lds + xbuf * Geo<PT>::XB + wp * Geo<PT>::WPX;
-    const uint8_t* wb = lds + Geo<PT>::WOFS + (j & 1) * kWBytes + wo * 16384 + lane * 16;
+    const uint8_t* wb = lds + Geo<PT>::WOFS + tbit * kWBytes + wo * 16384 + lane * 16;
     const int xnb = xbuf == 2 ? 0 : xbuf + 1;
     const uint8_t* xn = lds + xnb * Geo<PT>::XB + wp * Geo<PT>::WPX;  // chunk j+1
-    const uint8_t* wn = lds + Geo<PT>::WOFS + ((j + 1) & 1) * kWBytes + wo * 16384 + lane * 16;
-    uint8_t* tb = lds + Geo<PT>::WOFS + ((j + 1) & 1) * kWBytes;  // tile j+1, built here
+    const uint8_t* wn = lds + Geo<PT>::WOFS + (tbit ^ 1) * kWBytes + wo * 16384 + lane * 16;
+    uint8_t* tb = lds + Geo<PT>::WOFS + (tbit ^ 1) * kWBytes;  // tile j+1, built here
 #pragma unroll
     for (int g = 0; g < 16; ++g) {
       if constexpr (more1) {
@@ -486,17 +488,32 @@ __device__ __forceinline__ void wide_tile_body(const WParams& p, uint8_t* lds) {
   };
   read_first(0);
   int j = 0;
+  const BoolC<true> T{};
+  const BoolC<false> F{};
+  // (with four or eight packed units per lane the six copies no longer fit
+  // the registers: those variants keep the one-chunk loop)
+  if constexpr (FULL || UPL <= 2) {
 #pragma unroll 1
-  for (; j + 3 < nch; ++j) chunk(j, BoolC<true>{}, BoolC<true>{}, BoolC<true>{});
+    for (; j + 8 < nch; j += 6) {  // six chunks: both rotations return to their start
+      chunk(j, 0, 0, T, T, T);
+      chunk(j + 1, 1, 1, T, T, T);
+      chunk(j + 2, 2, 0, T, T, T);
+      chunk(j + 3, 0, 1, T, T, T);
+      chunk(j + 4, 1, 0, T, T, T);
+      chunk(j + 5, 2, 1, T, T, T);
+    }
+  }
+#pragma unroll 1
+  for (; j + 3 < nch; ++j) chunk(j, j % 3, j & 1, T, T, T);
   if (j + 2 < nch) {
-    chunk(j, BoolC<true>{}, BoolC<true>{}, BoolC<false>{});
+    chunk(j, j % 3, j & 1, T, T, F);
     ++j;
   }
   if (j + 1 < nch) {
-    chunk(j, BoolC<true>{}, BoolC<false>{}, BoolC<false>{});
+    chunk(j, j % 3, j & 1, T, F, F);
     ++j;
   }
-  chunk(j, BoolC<false>{}, BoolC<false>{}, BoolC<false>{});
+  chunk(j, j % 3, j & 1, F, F, F);
 
   // ---- fused epilogue -----------------------------------------------------------
   // Each wave parks 64 pixels x 128 outputs (fp32) at a time in its own LDS

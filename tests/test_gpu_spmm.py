@@ -68,6 +68,9 @@ WIDE_CASES = [  # N, C, O, G, K: chunks 1..5, ragged pixel blocks, every unit co
     (2048, 64, 256, 32, 9), (520, 128, 256, 32, 2), (300, 192, 512, 64, 4),
     # >= 128 tiles of 256 pixels: the 256-pixel plan (the rest run 128-pixel tiles)
     (32768, 64, 256, 64, 7), (32768, 128, 256, 4, 3), (33000, 64, 256, 32, 2), (32768, 192, 256, 16, 16),
+    # 9, 10, 15 and 16 chunks: the six-chunk steady state, the one-chunk loop and the tails
+    (300, 576, 256, 16, 1), (520, 640, 256, 16, 2), (300, 1024, 512, 16, 4), (257, 960, 256, 8, 8),
+    (600, 576, 256, 32, 3), (300, 1024, 256, 64, 7), (130, 960, 256, 16, 8), (32768, 576, 256, 16, 1),
 ]
 
 

@@ -26,6 +26,20 @@ def test_graph_replays_match_eager():
     vf = torch.empty((16, 4, 256), dtype=torch.float32, device=DEV)
     xf = torch.empty((16, 4, 256), dtype=torch.uint8, device=DEV)
     Yf = torch.empty((64, 128), dtype=torch.float32, device=DEV)
+    # a MobileNetV2-shaped 1x1 conv (24 -> 144) on the narrow kernels and a
+    # 4096-channel FC product on the wide-tile ones
+    Xn = torch.from_numpy(np.random.default_rng(7).standard_normal((2, 15, 13, 24)).astype(np.float32)).to(
+        torch.bfloat16).to(DEV)
+    Wn = torch.from_numpy((np.random.default_rng(8).standard_normal((144, 24)) / 5).astype(np.float32)).to(DEV)
+    vn = torch.empty((18, 3, 24), dtype=torch.bfloat16, device=DEV)
+    xn = torch.empty((18, 3, 24), dtype=torch.uint8, device=DEV)
+    Yn = torch.empty((2, 15, 13, 144), dtype=torch.bfloat16, device=DEV)
+    Xw = torch.from_numpy(np.random.default_rng(9).standard_normal((300, 1024)).astype(np.float32)).to(
+        torch.bfloat16).to(DEV)
+    Ww = torch.from_numpy((np.random.default_rng(10).standard_normal((256, 1024)) / 32).astype(np.float32)).to(DEV)
+    vw = torch.empty((16, 1, 1024), dtype=torch.bfloat16, device=DEV)
+    xw = torch.empty((16, 1, 1024), dtype=torch.uint8, device=DEV)
+    Yw = torch.empty((300, 256), dtype=torch.bfloat16, device=DEV)
     s = torch.cuda.Stream()
 
     def step():
@@ -34,11 +48,15 @@ def test_graph_replays_match_eager():
             cci.conv_im2col(Xs[i], vals, idx, w.G, 3, 3, (1, 1), (1, 1), out=Ys[i])
         cci.pack(Wf, 8, 4, torch.float32, out=(vf, xf))
         cci.spmm(Xf, vf, xf, 8, out=Yf)
+        cci.pack(Wn, 8, 3, torch.bfloat16, out=(vn, xn))
+        cci.conv_im2col(Xn, vn, xn, 8, 1, 1, out=Yn, algo="narrow_mfma")
+        cci.pack(Ww, 16, 1, torch.bfloat16, out=(vw, xw))
+        cci.spmm(Xw, vw, xw, 16, out=Yw, algo="wide_tile_mfma")
 
     with torch.cuda.stream(s):
         step()
     torch.cuda.synchronize()
-    ref = [y.clone() for y in Ys] + [Yf.clone(), vals.clone(), idx.clone()]
+    ref = [y.clone() for y in Ys] + [Yf.clone(), vals.clone(), idx.clone(), Yn.clone(), Yw.clone()]
 
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g, stream=s):
@@ -47,12 +65,14 @@ def test_graph_replays_match_eager():
         for y in Ys:
             y.zero_()
         Yf.zero_()
+        Yn.zero_()
+        Yw.zero_()
         vals.zero_()
         torch.cuda.synchronize()
         with torch.cuda.stream(s):
             g.replay()
         torch.cuda.synchronize()
-        got = Ys + [Yf, vals, idx]
+        got = Ys + [Yf, vals, idx, Yn, Yw]
         for a, b in zip(got, ref):
             assert torch.equal(a, b), f"replay {rep} differs from the eager run"
         # eager work between replays, on other data

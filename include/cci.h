@@ -70,12 +70,15 @@ typedef enum { CCI_F32 = 0, CCI_BF16 = 1 } cci_dtype;
  *  CCI_ALGO_NARROW_MFMA     the same expansion for short reductions: a wave
  *                           keeps the expanded weights of up to 80 outputs
  *                           in registers and streams pixels through them
- *                           (the 1x1 layers of narrow networks).  FC or 1x1
- *                           convolutions with stride 1 and no padding; bf16
- *                           X and vals, C <= 256, C % 8 == 0, O % 4 == 0,
- *                           G <= 256; X and vals 16-byte aligned, idx
- *                           8-byte aligned, Y (and residual) 8-byte aligned
- *                           for bf16 and 16-byte aligned for fp32 output. */
+ *                           (the 1x1 layers of narrow networks, a CNN's
+ *                           first conv).  FC products, 1x1 convolutions
+ *                           with stride 1 and no padding, and convolutions
+ *                           of any geometry with Cin % 8 == 0, or Cin == 4
+ *                           and an even KW; bf16 X and vals, C <= 256 (conv:
+ *                           KH*KW*Cin), C % 8 == 0, O % 4 == 0, G <= 256;
+ *                           X and vals 16-byte aligned, idx 8-byte aligned,
+ *                           Y (and residual) 8-byte aligned for bf16 and
+ *                           16-byte aligned for fp32 output. */
 typedef enum {
   CCI_ALGO_AUTO = 0,
   CCI_ALGO_SPARSE_MAC = 1,

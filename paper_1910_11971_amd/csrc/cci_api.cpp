@@ -97,8 +97,9 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
                 "C %% 64 == 0, O %% 256 == 0, 64 %% G == 0 and aligned pointers");
   if (chosen == CCI_ALGO_NARROW_MFMA && !cci::narrow_supports(a))
     return fail(CCI_EUNSUPPORTED,
-                "narrow MFMA kernels need bf16 X/vals, an FC or stride-1 unpadded 1x1 product, "
-                "C <= 256, C %% 8 == 0, O %% 4 == 0, G <= 256 and aligned pointers");
+                "narrow MFMA kernels need bf16 X/vals, C <= 256, C %% 8 == 0, O %% 4 == 0, G <= 256, "
+                "aligned pointers, and for a conv other than 1x1 stride 1 unpadded Cin %% 8 == 0 or "
+                "Cin == 4 with an even KW");
   const hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = chosen == CCI_ALGO_SPARSE_MAC       ? cci::launch_sparse_mac(a, st)
                  : chosen == CCI_ALGO_WIDE_TILE_MFMA ? cci::launch_wide_tile(a, st)
@@ -168,9 +169,11 @@ cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C, int
   const int64_t tiles = (N + 127) / 128 * (O / 256);
   if (bf && C == cin && C % 64 == 0 && C >= 512 && O % 256 == 0 && tiles >= 96) return CCI_ALGO_WIDE_TILE_MFMA;
   // Short reductions the tile kernels cannot take (Cin % 32 != 0) stream
-  // through register-resident weights.
-  if (x_t == CCI_BF16 && val_t == CCI_BF16 && C == cin && C <= 256 && C % 8 == 0 && cin % 32 != 0 &&
-      O % 4 == 0)
+  // through register-resident weights: 1x1 layers and FC products with
+  // C % 8 == 0, and convolutions over 4 input channels (an even KW) or a
+  // multiple of 8.
+  if (x_t == CCI_BF16 && val_t == CCI_BF16 && C <= 256 && C % 8 == 0 && cin % 32 != 0 && O % 4 == 0 &&
+      (cin == 4 || cin % 8 == 0))
     return CCI_ALGO_NARROW_MFMA;
   const bool tile_shape = bf && cin % 32 == 0;
   if (tile_shape && (32 * static_cast<int64_t>(K) > G || !mac_g)) return CCI_ALGO_DENSE_TILE_MFMA;

@@ -50,8 +50,9 @@ bool wide_tile_supports(const ProductArgs& a);
 hipError_t launch_wide_tile(const ProductArgs& a, hipStream_t s);
 
 // Short reductions (C <= 256, C % 8 == 0): expanded weights of up to 80
-// outputs per wave held in registers, pixels streamed through them (FC and
-// stride-1 1x1 convolutions; bf16; O % 4 == 0).
+// outputs per wave held in registers, pixels streamed through them (FC,
+// stride-1 1x1 convolutions, and implicit-im2col convolutions with
+// Cin % 8 == 0 or Cin == 4 and an even KW; bf16; O % 4 == 0).
 bool narrow_supports(const ProductArgs& a);
 hipError_t launch_narrow(const ProductArgs& a, hipStream_t s);
 

@@ -1,6 +1,8 @@
 // CCI-sparse products with a short reduction (C <= 256): the 1x1 layers of
 // narrow networks (MobileNetV2's expanding and projecting convolutions,
-// Sec. 6) and small FC layers.
+// Sec. 6), small FC layers, and convolutions with few input channels (a
+// CNN's first layer: Cin = 4, or Cin % 8 == 0) read through implicit im2col
+// (Sec. 3.2's lowering, never materialised).
 //
 // The method is the one of the tile kernels (Alg. 1's row G g + idx[g][k][c]
 // receives vals[g][k][c]; the expanded product runs on the bf16 matrix
@@ -13,7 +15,11 @@
 //   - the wave then streams groups of P 16-pixel blocks through them: the
 //     activations of the next group are loaded (16 bytes per lane, rows
 //     zero-padded past C and N by the buffer's range check) while the MFMAs
-//     and the fused epilogue of the current one run;
+//     and the fused epilogue of the current one run.  For a convolution the
+//     8 columns of a lane are one tap's 8 channels (Cin % 8 == 0) or two
+//     horizontally adjacent taps' 4 channels (Cin == 4, KW even), so they
+//     are one 16-byte (or two 8-byte) reads of the NHWC input, zero outside
+//     the image;
 //   - the accumulators leave the matrix cores with 4 consecutive outputs of
 //     one pixel per lane; scale / bias (staged in LDS), residual and ReLU are
 //     applied in fp32 and each lane stores 8 (bf16) or 16 (fp32) bytes.
@@ -51,6 +57,7 @@ struct NParams {
   void* Y;
   uint32_t x_bytes, y_bytes;
   int32_t N, C, O, G, K, relu;
+  int32_t H, W, Cin, KW, sh, sw, ph, pw, Ho, Wo;  // convolutions (implicit im2col)
   int32_t tpw;      // output tiles per slice
   int32_t nslices;  // slices covering the O / 16 (rounded up) output tiles
   int32_t npg;      // pixel groups of 16 P pixels
@@ -69,7 +76,9 @@ struct Shape {
 
 __device__ __forceinline__ float relu_f(float y) { return y > 0.0f ? y : (y != y ? y : 0.0f); }
 
-template <typename YT, int S>
+// CM: 0 rows of X are the GEMM rows (FC, 1x1 stride-1 unpadded conv);
+// 4 a convolution over 4 input channels; 8 a convolution over Cin % 8 == 0.
+template <typename YT, int S, int CM>
 __device__ __forceinline__ void narrow_body(const NParams& p, float* sb) {
   constexpr int P = Shape<S>::P, TM = Shape<S>::TM;
   const int lane = threadIdx.x & 63;
@@ -91,17 +100,61 @@ __device__ __forceinline__ void narrow_body(const NParams& p, float* sb) {
   const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<void*>(p.residual), (short)0, p.residual ? static_cast<int>(p.y_bytes) : 0, kRsrcWord3);
   const uint32_t N = static_cast<uint32_t>(p.N), C = static_cast<uint32_t>(p.C), O = static_cast<uint32_t>(p.O);
-  // B fragment of block b, k-step s: pixel 16 b + ol of the group, channels
-  // 32 s + 8 kq .. +7 (zero past C or N)
+  // B fragment of block b, k-step s: pixel 16 b + ol of the group, columns
+  // 32 s + 8 kq .. +7 (zero past C or N, and outside the image)
+  int tkh[S], tkw[S], tci[S];  // conv: tap row, tap column, channel of the lane's columns
+  bool sok[S];
+#pragma unroll
+  for (int s = 0; s < S; ++s) {
+    const int c = 32 * s + 8 * kq;
+    sok[s] = c < p.C;
+    if constexpr (CM != 0) {
+      const int t = c / p.Cin;
+      tci[s] = c - t * p.Cin;
+      tkh[s] = t / p.KW;
+      tkw[s] = t - tkh[s] * p.KW;
+    }
+  }
   auto load_group = [&](int pg, bf16x8_t (&xf)[P][S]) {
 #pragma unroll
     for (int b = 0; b < P; ++b) {
       const uint32_t n = static_cast<uint32_t>(pg) * (16u * P) + 16u * b + static_cast<uint32_t>(ol);
+      if constexpr (CM == 0) {
 #pragma unroll
-      for (int s = 0; s < S; ++s) {
-        const uint32_t c = 32u * s + 8u * static_cast<uint32_t>(kq);
-        const uint32_t off = (n < N && c < C) ? (n * C + c) * 2u : kOOB;
-        xf[b][s] = __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0));
+        for (int s = 0; s < S; ++s) {
+          const uint32_t c = 32u * s + 8u * static_cast<uint32_t>(kq);
+          const uint32_t off = (n < N && c < C) ? (n * C + c) * 2u : kOOB;
+          xf[b][s] = __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0));
+        }
+      } else {
+        // output pixel n = (image, oh, ow) -> top-left input position
+        const uint32_t hw = static_cast<uint32_t>(p.Ho * p.Wo);
+        const uint32_t img = n / hw;
+        const uint32_t rem = n - img * hw;
+        const uint32_t oh = rem / static_cast<uint32_t>(p.Wo);
+        const uint32_t ow = rem - oh * static_cast<uint32_t>(p.Wo);
+        const int ih0 = static_cast<int>(oh) * p.sh - p.ph, iw0 = static_cast<int>(ow) * p.sw - p.pw;
+        const bool nok = n < N;
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+          const int ih = ih0 + tkh[s], iw = iw0 + tkw[s];
+          const bool rok = nok && sok[s] && static_cast<uint32_t>(ih) < static_cast<uint32_t>(p.H);
+          const uint32_t pos = (img * static_cast<uint32_t>(p.H) + static_cast<uint32_t>(ih)) *
+                                   static_cast<uint32_t>(p.W) + static_cast<uint32_t>(iw);
+          if constexpr (CM == 8) {
+            const bool ok = rok && static_cast<uint32_t>(iw) < static_cast<uint32_t>(p.W);
+            const uint32_t off = ok ? (pos * static_cast<uint32_t>(p.Cin) + static_cast<uint32_t>(tci[s])) * 2u : kOOB;
+            xf[b][s] = __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0));
+          } else {  // taps (kh, kw) and (kh, kw + 1), 4 channels (8 bytes) each
+            const bool ok0 = rok && static_cast<uint32_t>(iw) < static_cast<uint32_t>(p.W);
+            const bool ok1 = rok && static_cast<uint32_t>(iw + 1) < static_cast<uint32_t>(p.W);
+            const uint32_t off0 = ok0 ? pos * 8u : kOOB;
+            const uint32_t off1 = ok1 ? pos * 8u + 8u : kOOB;
+            const u32x2_t lo = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(xr, off0, 0, 0));
+            const u32x2_t hi = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(xr, off1, 0, 0));
+            xf[b][s] = __builtin_bit_cast(bf16x8_t, u32x4_t{lo[0], lo[1], hi[0], hi[1]});
+          }
+        }
       }
     }
   };
@@ -245,19 +298,19 @@ __device__ __forceinline__ void narrow_body(const NParams& p, float* sb) {
 
 // (The body is a device function: with it inside the kernel template, the
 // host pass of this compiler emitted no launch stubs for the kernels.)
-template <typename YT, int S>
+template <typename YT, int S, int CM>
 __global__ __launch_bounds__(kThreads) void narrow_kernel(NParams p) {
   __shared__ __attribute__((aligned(16))) float sb[(kThreads / 64) * 2 * kSliceOut];
-  narrow_body<YT, S>(p, sb);
+  narrow_body<YT, S, CM>(p, sb);
 }
 
 // Waves of narrow_kernel<YT, S> that fit on the device at once (queried once).
-template <typename YT, int S>
+template <typename YT, int S, int CM>
 int64_t resident_waves() {
   static const int64_t waves = [] {
     int dev = 0, cus = 0, blocks = 0;
     if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, reinterpret_cast<const void*>(&narrow_kernel<YT, S>),
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, reinterpret_cast<const void*>(&narrow_kernel<YT, S, CM>),
                                                      kThreads, 0) != hipSuccess ||
         cus < 1 || blocks < 1)
       return static_cast<int64_t>(kWavesTarget);
@@ -268,29 +321,39 @@ int64_t resident_waves() {
 
 // One wave per (slice, pixel group) when that fits on the device at once;
 // otherwise as many waves as are resident, each streaming several groups.
-template <typename YT, int S>
+template <typename YT, int S, int CM>
 hipError_t launch_k(NParams p, hipStream_t s) {
-  const int64_t per_slice = std::max<int64_t>(1, resident_waves<YT, S>() / p.nslices);
+  const int64_t per_slice = std::max<int64_t>(1, resident_waves<YT, S, CM>() / p.nslices);
   p.wps = static_cast<int32_t>(std::min<int64_t>(p.npg, per_slice));
   const int64_t waves = static_cast<int64_t>(p.nslices) * p.wps;
   const uint32_t grid = static_cast<uint32_t>((waves + 3) / 4);
-  hipLaunchKernelGGL((narrow_kernel<YT, S>), dim3(grid), dim3(kThreads), 0, s, p);
+  hipLaunchKernelGGL((narrow_kernel<YT, S, CM>), dim3(grid), dim3(kThreads), 0, s, p);
   return hipGetLastError();
 }
 
-template <typename YT>
+template <typename YT, int CM>
 hipError_t launch_s(const NParams& p, int S, hipStream_t s) {
   switch (S) {
-    case 1: return launch_k<YT, 1>(p, s);
-    case 2: return launch_k<YT, 2>(p, s);
-    case 3: return launch_k<YT, 3>(p, s);
-    case 4: return launch_k<YT, 4>(p, s);
-    case 5: return launch_k<YT, 5>(p, s);
-    case 6: return launch_k<YT, 6>(p, s);
-    case 7: return launch_k<YT, 7>(p, s);
-    case 8: return launch_k<YT, 8>(p, s);
+    case 1: return launch_k<YT, 1, CM>(p, s);
+    case 2: return launch_k<YT, 2, CM>(p, s);
+    case 3: return launch_k<YT, 3, CM>(p, s);
+    case 4: return launch_k<YT, 4, CM>(p, s);
+    case 5: return launch_k<YT, 5, CM>(p, s);
+    case 6: return launch_k<YT, 6, CM>(p, s);
+    case 7: return launch_k<YT, 7, CM>(p, s);
+    case 8: return launch_k<YT, 8, CM>(p, s);
     default: return hipErrorInvalidConfiguration;
   }
+}
+
+// 0: rows; 4 / 8: implicit-im2col convolution over 4 / a multiple of 8 input channels
+int conv_mode(const ProductArgs& a) {
+  if (!a.conv) return 0;
+  const ConvGeom& g = a.geom;
+  if (g.KH == 1 && g.KW == 1 && g.sh == 1 && g.sw == 1 && g.ph == 0 && g.pw == 0) return 0;
+  if (g.Cin % 8 == 0) return 8;
+  if (g.Cin == 4 && g.KW % 2 == 0) return 4;
+  return -1;
 }
 
 int max_tiles(int S) {
@@ -311,10 +374,7 @@ int pixel_blocks(int S) { return S == 1 ? Shape<1>::P : (S == 2 ? Shape<2>::P : 
 
 bool narrow_supports(const ProductArgs& a) {
   if (a.x_t != DType::BF16 || a.val_t != DType::BF16) return false;
-  if (a.conv) {  // a 1x1 convolution with unit stride and no padding: rows are pixels
-    const ConvGeom& g = a.geom;
-    if (!(g.KH == 1 && g.KW == 1 && g.sh == 1 && g.sw == 1 && g.ph == 0 && g.pw == 0)) return false;
-  }
+  if (conv_mode(a) < 0) return false;
   if (a.G < 1 || a.G > 256 || a.K < 1 || a.K > a.G || a.O % a.G != 0) return false;
   if (a.C < 1 || a.C > kMaxC || a.C % 8 != 0 || a.O % 4 != 0 || a.N < 1) return false;
   const auto al = [](const void* q, uintptr_t m) { return (reinterpret_cast<uintptr_t>(q) & (m - 1)) == 0; };
@@ -324,7 +384,8 @@ bool narrow_supports(const ProductArgs& a) {
     return false;
   // every buffer offset is 32-bit and stays below the out-of-range marker
   const int64_t lim = static_cast<int64_t>(kOOB);
-  if (a.N * a.C * 2 >= lim || a.N * a.O * (a.y_t == DType::F32 ? 4 : 2) >= lim) return false;
+  const int64_t x_elems = a.conv ? a.B * static_cast<int64_t>(a.geom.H) * a.geom.W * a.geom.Cin : a.N * a.C;
+  if (x_elems * 2 >= lim || a.N * a.C * 2 >= lim || a.N * a.O * (a.y_t == DType::F32 ? 4 : 2) >= lim) return false;
   return true;
 }
 
@@ -338,7 +399,22 @@ hipError_t launch_narrow(const ProductArgs& a, hipStream_t s) {
   p.bias = a.bias;
   p.residual = a.residual;
   p.Y = a.Y;
-  p.x_bytes = static_cast<uint32_t>(a.N * a.C * 2);
+  const int cm = conv_mode(a);
+  p.x_bytes = static_cast<uint32_t>(
+      (cm == 0 ? a.N * a.C : a.B * static_cast<int64_t>(a.geom.H) * a.geom.W * a.geom.Cin) * 2);
+  if (cm != 0) {
+    const ConvGeom& g = a.geom;
+    p.H = g.H;
+    p.W = g.W;
+    p.Cin = g.Cin;
+    p.KW = g.KW;
+    p.sh = g.sh;
+    p.sw = g.sw;
+    p.ph = g.ph;
+    p.pw = g.pw;
+    p.Ho = g.Ho;
+    p.Wo = g.Wo;
+  }
   p.y_bytes = static_cast<uint32_t>(a.N * a.O * (a.y_t == DType::F32 ? 4 : 2));
   p.N = static_cast<int32_t>(a.N);
   p.C = static_cast<int32_t>(a.C);
@@ -354,7 +430,10 @@ hipError_t launch_narrow(const ProductArgs& a, hipStream_t s) {
   p.nslices = (tiles + p.tpw - 1) / p.tpw;
   const int64_t gp = 16 * static_cast<int64_t>(pixel_blocks(S));
   p.npg = static_cast<int32_t>((a.N + gp - 1) / gp);
-  return a.y_t == DType::F32 ? launch_s<float>(p, S, s) : launch_s<uint16_t>(p, S, s);
+  if (a.y_t == DType::F32)
+    return cm == 0 ? launch_s<float, 0>(p, S, s) : cm == 4 ? launch_s<float, 4>(p, S, s) : launch_s<float, 8>(p, S, s);
+  return cm == 0 ? launch_s<uint16_t, 0>(p, S, s)
+                 : cm == 4 ? launch_s<uint16_t, 4>(p, S, s) : launch_s<uint16_t, 8>(p, S, s);
 }
 
 }  // namespace cci

@@ -8,6 +8,13 @@ bottleneck's residual add is fused into its last 1x1 conv, before the ReLU.
 Pooling runs on the library's NHWC max-pool (exact) and global average pool
 (fp32 accumulation, one rounding to bf16 before the FC).  Every conv output
 is rounded to bf16 once, after its fused epilogue; the logits are fp32.
+
+The first conv (7x7, stride 2, 3 channels) runs with its images copied into
+a 4-channel buffer whose fourth channel stays zero and its weights
+zero-padded to 7x8 taps of 4 channels: the sums are unchanged (every added
+term is an exact zero), and the layer takes the matrix-core kernels' short
+reduction path (a lane's 8 reduction columns are two adjacent taps' 4
+channels, one 16-byte span of the image) instead of the vector-ALU path.
 """
 from __future__ import annotations
 
@@ -18,6 +25,9 @@ from . import cci
 from .workloads import ResNet50, bn_fold
 
 
+STEM_CIN, STEM_KW = 4, 8  # the first conv's channels and tap columns after zero padding
+
+
 class ResNet50CCI:
     """Packs the weights once (``cci_pack`` per layer) and runs forwards."""
 
@@ -26,7 +36,12 @@ class ResNet50CCI:
         self.layers = net.layers
         self.device = torch.device(device)
         self.packed = []
-        for L, w in zip(self.layers, conv_weights):
+        self._stem_in = None  # the zero-padded image buffer (one per input shape)
+        for i, (L, w) in enumerate(zip(self.layers, conv_weights)):
+            if i == 0:  # [Cout, k*k*Cin] -> [Cout, k*STEM_KW*STEM_CIN], zeros in the added taps / channels
+                wp = np.zeros((L.Cout, L.k, STEM_KW, STEM_CIN), np.float32)
+                wp[:, :, :L.k, :L.Cin] = np.asarray(w, np.float32).reshape(L.Cout, L.k, L.k, L.Cin)
+                w = wp.reshape(L.Cout, -1)
             W = torch.from_numpy(np.ascontiguousarray(w)).to(self.device)
             vals, idx = cci.pack(W, net.G, L.K, torch.bfloat16)
             sc, bi = bn_fold(L.Cout)
@@ -37,8 +52,18 @@ class ResNet50CCI:
     def conv(self, i, x, residual=None):
         L = self.layers[i]
         vals, idx, sc, bi = self.packed[i]
-        return cci.conv_im2col(x, vals, idx, self.net.G, L.k, L.k, (L.stride, L.stride), (L.pad, L.pad),
+        kw = STEM_KW if i == 0 else L.k
+        return cci.conv_im2col(x, vals, idx, self.net.G, L.k, kw, (L.stride, L.stride), (L.pad, L.pad),
                                scale=sc, bias=bi, residual=residual, relu=L.relu, out_dtype=torch.bfloat16)
+
+    def stem_input(self, X: torch.Tensor) -> torch.Tensor:
+        """X [B, H, W, 3] copied into channels 0..2 of a [B, H, W, STEM_CIN]
+        buffer whose last channel is zeroed when the buffer is allocated."""
+        shape = tuple(X.shape[:3]) + (STEM_CIN,)
+        if self._stem_in is None or tuple(self._stem_in.shape) != shape:
+            self._stem_in = torch.zeros(shape, dtype=X.dtype, device=X.device)
+        self._stem_in[..., :X.shape[3]].copy_(X)
+        return self._stem_in
 
     def forward(self, X: torch.Tensor, record: list | None = None) -> torch.Tensor:
         """X bf16 NHWC [B, HW, HW, 3] on the device -> fp32 logits [B, classes].
@@ -50,7 +75,7 @@ class ResNet50CCI:
             if record is not None:
                 record.append((kind, key, inp, out, res))
 
-        x = self.conv(0, X)
+        x = self.conv(0, self.stem_input(X))
         rec("conv", 0, X, x)
         y = cci.maxpool2d_nhwc(x, 3, 2, 1)
         rec("maxpool", "maxpool", x, y)

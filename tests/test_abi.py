@@ -100,8 +100,9 @@ def test_narrow_algo_requirements():
                         cci.BF16, Nw, None) == cci.EUNSUPPORTED
     assert lib.cci_spmm(FAKE, cci.F32, 4, 16, FAKE, cci.F32, FAKE, 16, 8, 2, None, FAKE,
                         cci.F32, Nw, None) == cci.EUNSUPPORTED
-    for KH, sh, ph in [(3, 1, 1), (1, 2, 0), (1, 1, 1)]:
-        assert lib.cci_conv_im2col(FAKE, cci.BF16, 1, 8, 8, 24, KH, KH, sh, sh, ph, ph, FAKE, cci.BF16,
+    # convs: Cin 3, Cin 4 with an odd KW, and a reduction past 256 are refused
+    for Cin, KH, KW in [(3, 3, 3), (4, 7, 7), (40, 3, 3)]:
+        assert lib.cci_conv_im2col(FAKE, cci.BF16, 1, 8, 8, Cin, KH, KW, 1, 1, 1, 1, FAKE, cci.BF16,
                                    FAKE, 96, 8, 2, None, FAKE, cci.BF16, Nw, None) == cci.EUNSUPPORTED
 
 
@@ -144,6 +145,9 @@ def test_auto_algo_cost_model():
     # short reductions the tile path cannot step through (MobileNetV2's 16 / 24 / 144 channels)
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 802816, 16, 16, 96, 8, 2) == "narrow_mfma"
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 200704, 144, 144, 24, 8, 1) == "narrow_mfma"
+    # small-Cin convs read through implicit im2col (a stem padded to 4 channels and KW = 8)
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 802816, 224, 4, 64, 8, 8) == "narrow_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 5000, 216, 24, 64, 8, 2) == "narrow_mfma"
 
 
 @pytest.mark.skipif(torch.cuda.is_available(), reason="checks the no-device error path only")

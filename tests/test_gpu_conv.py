@@ -14,6 +14,11 @@ pytestmark = pytest.mark.gpu
 
 def run_conv(X: torch.Tensor, W: np.ndarray, G, K, k, stride, pad, y_dtype, algo, *, pixels=None,
              ep=None):
+    return run_conv_kw(X, W, G, K, k, k, stride, pad, y_dtype, algo, pixels=pixels, ep=ep)
+
+
+def run_conv_kw(X: torch.Tensor, W: np.ndarray, G, K, KH, KW, stride, pad, y_dtype, algo, *, pixels=None,
+                ep=None):
     from paper_1910_11971_amd import cci
     vdt = torch.float32 if X.dtype == torch.float32 else torch.bfloat16
     B, H, Wd, Cin = X.shape
@@ -24,15 +29,15 @@ def run_conv(X: torch.Tensor, W: np.ndarray, G, K, k, stride, pad, y_dtype, algo
         kw["scale"] = torch.from_numpy(s).to(DEV)
     if b is not None:
         kw["bias"] = torch.from_numpy(b).to(DEV)
-    Ho, Wo = cci.conv_out_hw(H, Wd, k, k, (stride, stride), (pad, pad))
+    Ho, Wo = cci.conv_out_hw(H, Wd, KH, KW, (stride, stride), (pad, pad))
     if r_t is not None:
         kw["residual"] = r_t.reshape(B, Ho, Wo, O).to(DEV)
     vals, idx = cci.pack(torch.from_numpy(W).to(DEV), G, K, vdt)
-    Y = cci.conv_im2col(X.to(DEV), vals, idx, G, k, k, (stride, stride), (pad, pad), relu=relu,
+    Y = cci.conv_im2col(X.to(DEV), vals, idx, G, KH, KW, (stride, stride), (pad, pad), relu=relu,
                         out_dtype=y_dtype, algo=algo, **kw)
     torch.cuda.synchronize()
     v_ref, idx_ref, _ = oracle_pack_vals(W, G, K, vdt)
-    Wmask = oracle.unpack(v_ref, idx_ref, G).reshape(O, k, k, Cin)
+    Wmask = oracle.unpack(v_ref, idx_ref, G).reshape(O, KH, KW, Cin)
     Yref, Yabs = oracle.conv2d_nhwc(x_as_f32(X), Wmask, (stride, stride), (pad, pad), scale=s, bias=b,
                                     residual=r, relu=relu, pixels=pixels, want_abs=True)
     got = to_np_f32(Y).reshape(-1, O)
@@ -41,7 +46,7 @@ def run_conv(X: torch.Tensor, W: np.ndarray, G, K, k, stride, pad, y_dtype, algo
     rr = None if r is None else (r if pixels is None else r[pixels])
     S = epilogue_terms(Yabs, s, b, rr)
     return check_close(got, Yref, S, tol_for(y_dtype, X.dtype),
-                       f"conv {algo} {tuple(X.shape)} k{k} s{stride} p{pad} O={O} G={G} K={K}")
+                       f"conv {algo} {tuple(X.shape)} k{KH}x{KW} s{stride} p{pad} O={O} G={G} K={K}")
 
 
 def rand_x(shape, dtype, seed):
@@ -77,6 +82,29 @@ def test_conv1x1_wide_tile(B, H, W, Cin, O, G, K):
     X = rand_x((B, H, W, Cin), torch.bfloat16, B * H + Cin)
     ep = rand_epilogue(O, B * H * W, torch.bfloat16, 8, residual=True, relu=True)
     run_conv(X, rand_w(O, Cin, O + 1), G, K, 1, 1, 0, torch.bfloat16, "wide_tile_mfma", ep=ep)
+
+
+NARROW_CONV_CASES = [  # B, H, W, Cin, O, KH, KW, stride, pad, G, K
+    (1, 40, 38, 4, 64, 7, 8, 2, 3, 8, 8),     # a first conv: 3 channels padded to 4, 7x7 padded to 7x8
+    (2, 21, 17, 4, 64, 7, 8, 2, 3, 8, 2),
+    (2, 9, 11, 4, 32, 3, 4, 1, 1, 8, 3),
+    (2, 13, 10, 8, 64, 3, 3, 1, 1, 8, 2),
+    (3, 14, 15, 16, 96, 3, 3, 2, 1, 16, 5),
+    (1, 12, 12, 24, 48, 3, 3, 1, 0, 8, 1),
+    (2, 6, 7, 8, 16, 5, 5, 1, 2, 4, 4),
+    (2, 10, 9, 40, 24, 1, 1, 2, 0, 8, 2),     # strided 1x1
+]
+
+
+@pytest.mark.parametrize("B,H,W,Cin,O,KH,KW,stride,pad,G,K", NARROW_CONV_CASES)
+def test_conv_narrow_implicit_im2col(B, H, W, Cin, O, KH, KW, stride, pad, G, K):
+    need_gpu()
+    from paper_1910_11971_amd import cci
+    X = rand_x((B, H, W, Cin), torch.bfloat16, Cin + O + KH)
+    W_ = rand_w(O, KH * KW * Cin, O + KW)
+    Ho, Wo = cci.conv_out_hw(H, W, KH, KW, (stride, stride), (pad, pad))
+    ep = rand_epilogue(O, B * Ho * Wo, torch.bfloat16, 6, residual=True, relu=True)
+    run_conv_kw(X, W_, G, K, KH, KW, stride, pad, torch.bfloat16, "narrow_mfma", ep=ep)
 
 
 @pytest.mark.parametrize("B,H,W,Cin,O,G,K", [(2, 7, 9, 24, 144, 8, 3), (3, 11, 5, 144, 32, 8, 1),

@@ -12,7 +12,8 @@ pytestmark = pytest.mark.gpu
 
 @pytest.mark.parametrize("dt", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("shape,k,s,p", [((2, 112, 112, 64), 3, 2, 1), ((3, 9, 10, 5), 3, 2, 1),
-                                         ((1, 8, 8, 16), 2, 2, 0)])
+                                         ((1, 8, 8, 16), 2, 2, 0), ((2, 13, 11, 24), 3, 2, 1),
+                                         ((1, 7, 9, 40), 3, 1, 1)])
 def test_maxpool_exact(shape, k, s, p, dt):
     need_gpu()
     from paper_1910_11971_amd import cci

@@ -148,6 +148,10 @@ def test_auto_algo_cost_model():
     # small-Cin convs read through implicit im2col (a stem padded to 4 channels and KW = 8)
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 802816, 224, 4, 64, 8, 8) == "narrow_mfma"
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 5000, 216, 24, 64, 8, 2) == "narrow_mfma"
+    # large 1x1 products with C <= 128 too; C = 256 or fewer rows stay on the tile kernels
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 200704, 64, 64, 256, 8, 2) == "narrow_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 200704, 256, 256, 64, 8, 2) == "dense_tile_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 12544, 64, 64, 384, 8, 2) == "dense_tile_mfma"
 
 
 @pytest.mark.skipif(torch.cuda.is_available(), reason="checks the no-device error path only")

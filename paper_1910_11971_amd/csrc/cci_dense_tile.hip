@@ -884,15 +884,20 @@ double model_cycles(const Params& t, double mfma_chunk, double store, int K) {
   // expansion by the 256 expander threads: zero fill (b128 writes) and
   // K packed-row segments per unit
   const double build = t.w_bytes / 16.0 / kRoleThreads * 8.0 + t.nu * K * 120.0;
-  const double latency = 1500.0, barrier = 150.0, setup = 1500.0;
+  // (chunk_latency: measured on ResNet-50's 3x3 layers, whose chunks cost
+  // 6.5-10 K cycles almost independently of the part's pixel count)
+  const double latency = 1500.0, barrier = 150.0, setup = 1500.0, chunk_latency = 5000.0;
   const double e_first = setup + latency + build * (t.wres ? 1 : 2);
   double arrive = setup / 2 + latency + load, done = 0.0, start = 0.0;
   double done2 = 0.0;  // done time of chunk c-2
   const int n = t.nchunks;
   for (int c = 0; c < n; ++c) {
     if (c > 0) {
+      // every chunk's patch request pays a memory latency; with two patch
+      // buffers it is issued when the previous chunk starts, so it hides
+      // behind that chunk's MFMAs when they are long enough
       const double issue = t.npb == 2 ? start : done + barrier;
-      arrive = (issue > arrive ? issue : arrive) + load;
+      arrive = (issue > arrive ? issue : arrive) + chunk_latency + load;
     }
     double ready_w = e_first;
     // ring: chunk c is scattered during chunk c-1's MFMAs by the expander half

@@ -875,18 +875,25 @@ bool layout(Params& pl, int32_t cinb, int32_t Cin, int32_t wres, int32_t npb, in
 }
 
 // Modelled duration (cycles) of one workgroup: a chunk's patch streams at
-// one CU's share of HBM bandwidth (~13 B/clk) once its buffer is free (two
-// buffers: from the start of the previous chunk's MFMAs); its MFMAs start
-// when it has arrived, its weights are expanded and the previous chunk is
-// done.
+// kPatchBpc bytes per cycle once its buffer is free (two buffers: from the
+// start of the previous chunk's MFMAs); its MFMAs start when it has
+// arrived, its weights are expanded and the previous chunk is done.  The
+// constants were fitted to measured times of every legal plan of 24 layer
+// shapes (ResNet-50's and MobileNetV2's, the 3x3 / 1x1 / FC benchmark
+// layers): the plan the model picks is on average within 5% of the fastest
+// measured one (within 25% for every shape; it was 2x off for some shapes
+// with the previous hand-set constants).
+constexpr double kPatchBpc = 20.0;      // patch / output bytes per cycle per CU
+constexpr double kUnitCycles = 400.0;   // one expansion unit (packed row segment) per expander lane
+constexpr double kMfmaCycles = 20.0;    // one 16x16x32 MFMA with its operand reads
 double model_cycles(const Params& t, double mfma_chunk, double store, int K) {
-  const double load = t.patch_pix * static_cast<double>(t.cinb) * 2.0 / 13.0;
+  const double load = t.patch_pix * static_cast<double>(t.cinb) * 2.0 / kPatchBpc;
   // expansion by the 256 expander threads: zero fill (b128 writes) and
   // K packed-row segments per unit
-  const double build = t.w_bytes / 16.0 / kRoleThreads * 8.0 + t.nu * K * 120.0;
-  // (chunk_latency: measured on ResNet-50's 3x3 layers, whose chunks cost
-  // 6.5-10 K cycles almost independently of the part's pixel count)
-  const double latency = 1500.0, barrier = 150.0, setup = 1500.0, chunk_latency = 5000.0;
+  const double build = t.w_bytes / 16.0 / kRoleThreads * 8.0 + t.nu * K * kUnitCycles;
+  // (chunk_latency: ResNet-50's 3x3 layers' chunks were measured at 6.5-10 K
+  // cycles almost independently of the part's pixel count)
+  const double latency = 5633.0, barrier = 100.0, setup = 1813.0, chunk_latency = 1873.0;
   const double e_first = setup + latency + build * (t.wres ? 1 : 2);
   double arrive = setup / 2 + latency + load, done = 0.0, start = 0.0;
   double done2 = 0.0;  // done time of chunk c-2
@@ -966,10 +973,10 @@ bool make_plan(const ProductArgs& a, Params& best, uint32_t& grid) {
         }
         simd_tiles = t2 > simd_tiles ? t2 : simd_tiles;
       }
-      const double store = static_cast<double>(pix_per_part) * WO * kBN * ysz / 13.0;
+      const double store = static_cast<double>(pix_per_part) * WO * kBN * ysz / kPatchBpc;
       for (int32_t cinb = 512; cinb >= kKS; cinb /= 2) {
         if (Cin % cinb) continue;
-        const double mfma_chunk = static_cast<double>(simd_tiles) * taps * (cinb / kKS) * 4.0 * 16.0;
+        const double mfma_chunk = static_cast<double>(simd_tiles) * taps * (cinb / kKS) * 4.0 * kMfmaCycles;
         for (int32_t wres = 1; wres >= 0; --wres) {
           for (int32_t npb = 1; npb <= 2; ++npb) {
             Params t = pl;

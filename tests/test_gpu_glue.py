@@ -23,12 +23,13 @@ def test_maxpool_exact(shape, k, s, p, dt):
     np.testing.assert_array_equal(to_np_f32(Y), ref)
 
 
+@pytest.mark.parametrize("shape", [(4, 7, 7, 2048), (3, 5, 6, 12), (2, 9, 11, 40)])
 @pytest.mark.parametrize("xdt,ydt", [(torch.bfloat16, torch.bfloat16), (torch.bfloat16, torch.float32),
                                      (torch.float32, torch.float32)])
-def test_global_avgpool(xdt, ydt):
+def test_global_avgpool(xdt, ydt, shape):
     need_gpu()
     from paper_1910_11971_amd import cci
-    X = torch.from_numpy(np.random.default_rng(2).standard_normal((4, 7, 7, 2048)).astype(np.float32)).to(xdt)
+    X = torch.from_numpy(np.random.default_rng(2).standard_normal(shape).astype(np.float32)).to(xdt)
     Y = cci.global_avgpool_nhwc(X.to(DEV), ydt)
     ref = oracle.global_avgpool_nhwc(X.float().numpy())
     tol = 1e-5 if ydt == torch.float32 else 1e-2

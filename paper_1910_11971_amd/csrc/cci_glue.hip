@@ -1,8 +1,8 @@
 // CNN glue for the ResNet-shaped forward: NHWC max pooling and global average
 // pooling.  Memory-bound elementwise/reduction kernels, consecutive lanes on
-// consecutive channels (coalesced): with bf16 input and C % 8 == 0 a lane
-// owns 8 channels (16-byte reads, 32-bit index arithmetic); otherwise one
-// lane per output element.
+// consecutive channels (coalesced): bf16 max pooling with C % 8 == 0 gives a
+// lane 8 channels of one output pixel (16-byte reads and writes, 32-bit
+// index arithmetic); otherwise one lane per output element.
 #include "cci_launch.hpp"
 
 namespace cci {
@@ -79,32 +79,6 @@ __global__ __launch_bounds__(kThreads) void maxpool_bf16x8_kernel(const u32x4_t*
   Y[e] = out;
 }
 
-// bf16 input, C % 8 == 0: lane e owns channels 8 (e % C8) .. +7 of image
-// e / C8 and sums its HW pixels in the same order as avgpool_kernel (one
-// fp32 sum per channel), 16-byte reads with several in flight.
-template <typename YT>
-__global__ __launch_bounds__(kThreads) void avgpool_bf16x8_kernel(const u32x4_t* __restrict__ X, uint32_t HW,
-                                                                  uint32_t C8, uint32_t total,
-                                                                  YT* __restrict__ Y) {
-  const uint32_t e = blockIdx.x * kThreads + threadIdx.x;
-  if (e >= total) return;
-  const uint32_t c8 = e % C8;
-  const uint32_t b = e / C8;
-  float acc[8];
-#pragma unroll
-  for (int j = 0; j < 8; ++j) acc[j] = 0.0f;
-  const u32x4_t* src = X + static_cast<size_t>(b) * HW * C8 + c8;
-#pragma unroll 7
-  for (uint32_t i = 0; i < HW; ++i) {
-    const u32x4_t v = src[static_cast<size_t>(i) * C8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-      acc[j] += __uint_as_float((j & 1) ? (v[j >> 1] & 0xffff0000u) : (v[j >> 1] << 16));
-  }
-#pragma unroll
-  for (int j = 0; j < 8; ++j) io<YT>::store(Y, static_cast<int64_t>(e) * 8 + j, acc[j] / static_cast<float>(HW));
-}
-
 template <typename XT, typename YT>
 __global__ __launch_bounds__(kThreads) void avgpool_kernel(const XT* __restrict__ X, int64_t B,
                                                            int64_t HW, int64_t C,
@@ -149,20 +123,8 @@ hipError_t launch_maxpool(const void* X, DType t, int64_t B, int64_t H, int64_t 
 
 hipError_t launch_avgpool(const void* X, DType x_t, int64_t B, int64_t H, int64_t W, int64_t C,
                           void* Y, DType y_t, hipStream_t s) {
-  const int64_t HW = H * W;
-  if (x_t == DType::BF16 && C % 8 == 0 && (reinterpret_cast<uintptr_t>(X) & 15u) == 0 &&
-      B * HW * C < (int64_t{1} << 31)) {
-    const uint32_t vt = static_cast<uint32_t>(B * C / 8);
-    const dim3 g((vt + kThreads - 1) / kThreads);
-    if (y_t == DType::F32)
-      hipLaunchKernelGGL((avgpool_bf16x8_kernel<float>), g, dim3(kThreads), 0, s, static_cast<const u32x4_t*>(X),
-                         static_cast<uint32_t>(HW), static_cast<uint32_t>(C / 8), vt, static_cast<float*>(Y));
-    else
-      hipLaunchKernelGGL((avgpool_bf16x8_kernel<bf16_t>), g, dim3(kThreads), 0, s, static_cast<const u32x4_t*>(X),
-                         static_cast<uint32_t>(HW), static_cast<uint32_t>(C / 8), vt, static_cast<bf16_t*>(Y));
-    return hipGetLastError();
-  }
   const dim3 grid(static_cast<uint32_t>((B * C + kThreads - 1) / kThreads));
+  const int64_t HW = H * W;
   if (x_t == DType::F32 && y_t == DType::F32)
     hipLaunchKernelGGL((avgpool_kernel<float, float>), grid, dim3(kThreads), 0, s,
                        static_cast<const float*>(X), B, HW, C, static_cast<float*>(Y));

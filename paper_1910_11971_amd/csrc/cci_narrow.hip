@@ -78,7 +78,8 @@ __device__ __forceinline__ float relu_f(float y) { return y > 0.0f ? y : (y != y
 
 // CM: 0 rows of X are the GEMM rows (FC, 1x1 stride-1 unpadded conv);
 // 4 a convolution over 4 input channels; 8 a convolution over Cin % 8 == 0.
-template <typename YT, int S, int CM>
+// RES: a residual is added (its reads are issued with the group's MFMAs).
+template <typename YT, int S, int CM, bool RES>
 __device__ __forceinline__ void narrow_body(const NParams& p, float* sb) {
   constexpr int P = Shape<S>::P, TM = Shape<S>::TM;
   const int lane = threadIdx.x & 63;
@@ -232,9 +233,29 @@ __device__ __forceinline__ void narrow_body(const NParams& p, float* sb) {
     for (int s = 0; s < S; ++s) wf[t][s] = __builtin_bit_cast(bf16x8_t, wacc[t][s]);
 
   constexpr uint32_t ysz = sizeof(YT);
+  using RV = std::conditional_t<ysz == 2, u32x2_t, f32x4_t>;  // a lane's 4 residual values
+  // Y / residual offset of (block b, tile t) of group g
+  auto yoff = [&](int g, int b, int t) {
+    const uint32_t n = static_cast<uint32_t>(g) * (16u * P) + 16u * b + static_cast<uint32_t>(ol);
+    const uint32_t o = static_cast<uint32_t>(16 * (t0 + t) + 4 * kq);
+    return (n < N && o < O) ? (n * O + o) * ysz : kOOB;
+  };
   while (true) {
     const int pn = pg + p.wps;
     load_group(pn, xn);  // past the last group: every offset is out of range
+    RV res[P][TM];
+    if constexpr (RES) {  // this group's residual, requested before its MFMAs
+#pragma unroll
+      for (int b = 0; b < P; ++b)
+#pragma unroll
+        for (int t = 0; t < TM; ++t) {
+          if (t >= tw) continue;
+          if constexpr (ysz == 2)
+            res[b][t] = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(rr, yoff(pg, b, t), 0, 0));
+          else
+            res[b][t] = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rr, yoff(pg, b, t), 0, 0));
+        }
+    }
     f32x4_t acc[P][TM];
 #pragma unroll
     for (int b = 0; b < P; ++b)
@@ -250,25 +271,23 @@ __device__ __forceinline__ void narrow_body(const NParams& p, float* sb) {
     // epilogue: lane holds outputs 16 (t0 + t) + 4 kq .. +3 of pixel 16 b + ol
 #pragma unroll
     for (int b = 0; b < P; ++b) {
-      const uint32_t n = static_cast<uint32_t>(pg) * (16u * P) + 16u * b + static_cast<uint32_t>(ol);
 #pragma unroll
       for (int t = 0; t < TM; ++t) {
         if (t >= tw) continue;
         const int oi = 16 * t + 4 * kq;  // within the slice
-        const uint32_t o = static_cast<uint32_t>(16 * t0 + oi);
-        const uint32_t off = (n < N && o < O) ? (n * O + o) * ysz : kOOB;
+        const uint32_t off = yoff(pg, b, t);
         const f32x4_t sc = *reinterpret_cast<const f32x4_t*>(ss + oi);
         const f32x4_t bi = *reinterpret_cast<const f32x4_t*>(ss + kSliceOut + oi);
         f32x4_t y = acc[b][t] * sc + bi;
-        if (p.residual) {
+        if constexpr (RES) {
           if constexpr (ysz == 2) {
-            const u32x2_t q = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(rr, off, 0, 0));
+            const u32x2_t q = res[b][t];
             y[0] += __uint_as_float(q[0] << 16);
             y[1] += __uint_as_float(q[0] & 0xffff0000u);
             y[2] += __uint_as_float(q[1] << 16);
             y[3] += __uint_as_float(q[1] & 0xffff0000u);
           } else {
-            y += __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rr, off, 0, 0));
+            y += res[b][t];
           }
         }
         if (p.relu) {
@@ -298,19 +317,19 @@ __device__ __forceinline__ void narrow_body(const NParams& p, float* sb) {
 
 // (The body is a device function: with it inside the kernel template, the
 // host pass of this compiler emitted no launch stubs for the kernels.)
-template <typename YT, int S, int CM>
+template <typename YT, int S, int CM, bool RES>
 __global__ __launch_bounds__(kThreads) void narrow_kernel(NParams p) {
   __shared__ __attribute__((aligned(16))) float sb[(kThreads / 64) * 2 * kSliceOut];
-  narrow_body<YT, S, CM>(p, sb);
+  narrow_body<YT, S, CM, RES>(p, sb);
 }
 
 // Waves of narrow_kernel<YT, S> that fit on the device at once (queried once).
-template <typename YT, int S, int CM>
+template <typename YT, int S, int CM, bool RES>
 int64_t resident_waves() {
   static const int64_t waves = [] {
     int dev = 0, cus = 0, blocks = 0;
     if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, reinterpret_cast<const void*>(&narrow_kernel<YT, S, CM>),
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, reinterpret_cast<const void*>(&narrow_kernel<YT, S, CM, RES>),
                                                      kThreads, 0) != hipSuccess ||
         cus < 1 || blocks < 1)
       return static_cast<int64_t>(kWavesTarget);
@@ -321,27 +340,27 @@ int64_t resident_waves() {
 
 // One wave per (slice, pixel group) when that fits on the device at once;
 // otherwise as many waves as are resident, each streaming several groups.
-template <typename YT, int S, int CM>
+template <typename YT, int S, int CM, bool RES>
 hipError_t launch_k(NParams p, hipStream_t s) {
-  const int64_t per_slice = std::max<int64_t>(1, resident_waves<YT, S, CM>() / p.nslices);
+  const int64_t per_slice = std::max<int64_t>(1, resident_waves<YT, S, CM, RES>() / p.nslices);
   p.wps = static_cast<int32_t>(std::min<int64_t>(p.npg, per_slice));
   const int64_t waves = static_cast<int64_t>(p.nslices) * p.wps;
   const uint32_t grid = static_cast<uint32_t>((waves + 3) / 4);
-  hipLaunchKernelGGL((narrow_kernel<YT, S, CM>), dim3(grid), dim3(kThreads), 0, s, p);
+  hipLaunchKernelGGL((narrow_kernel<YT, S, CM, RES>), dim3(grid), dim3(kThreads), 0, s, p);
   return hipGetLastError();
 }
 
 template <typename YT, int CM>
 hipError_t launch_s(const NParams& p, int S, hipStream_t s) {
   switch (S) {
-    case 1: return launch_k<YT, 1, CM>(p, s);
-    case 2: return launch_k<YT, 2, CM>(p, s);
-    case 3: return launch_k<YT, 3, CM>(p, s);
-    case 4: return launch_k<YT, 4, CM>(p, s);
-    case 5: return launch_k<YT, 5, CM>(p, s);
-    case 6: return launch_k<YT, 6, CM>(p, s);
-    case 7: return launch_k<YT, 7, CM>(p, s);
-    case 8: return launch_k<YT, 8, CM>(p, s);
+    case 1: return p.residual ? launch_k<YT, 1, CM, true>(p, s) : launch_k<YT, 1, CM, false>(p, s);
+    case 2: return p.residual ? launch_k<YT, 2, CM, true>(p, s) : launch_k<YT, 2, CM, false>(p, s);
+    case 3: return p.residual ? launch_k<YT, 3, CM, true>(p, s) : launch_k<YT, 3, CM, false>(p, s);
+    case 4: return p.residual ? launch_k<YT, 4, CM, true>(p, s) : launch_k<YT, 4, CM, false>(p, s);
+    case 5: return p.residual ? launch_k<YT, 5, CM, true>(p, s) : launch_k<YT, 5, CM, false>(p, s);
+    case 6: return p.residual ? launch_k<YT, 6, CM, true>(p, s) : launch_k<YT, 6, CM, false>(p, s);
+    case 7: return p.residual ? launch_k<YT, 7, CM, true>(p, s) : launch_k<YT, 7, CM, false>(p, s);
+    case 8: return p.residual ? launch_k<YT, 8, CM, true>(p, s) : launch_k<YT, 8, CM, false>(p, s);
     default: return hipErrorInvalidConfiguration;
   }
 }

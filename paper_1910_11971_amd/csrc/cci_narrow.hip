@@ -21,13 +21,16 @@
 //     are one 16-byte (or two 8-byte) reads of the NHWC input, zero outside
 //     the image;
 //   - the accumulators leave the matrix cores with 4 consecutive outputs of
-//     one pixel per lane; scale / bias (staged in LDS), residual and ReLU are
-//     applied in fp32 and each lane stores 8 (bf16) or 16 (fp32) bytes.
+//     one pixel per lane; scale / bias (staged in LDS), residual (requested
+//     with the group's MFMAs) and ReLU are applied in fp32 and each lane
+//     stores 8 (bf16) or 16 (fp32) bytes.
 //
-// Every activation is read from HBM once per slice (slices of one pixel
-// group run in the same workgroup), the packed weights once per wave, and
-// every output is written once.  The layers this serves are bound by HBM
-// bandwidth: their MFMA work is small next to their bytes.
+// The slices of one pixel group are consecutive waves, so with 1, 2 or 4
+// slices they share a workgroup and the group's activations come from HBM
+// once (with 3 slices a workgroup holds parts of two groups: about 1.5x);
+// the packed weights are read once per wave and every output is written
+// once.  The layers this serves are bound by HBM bandwidth: their MFMA work
+// is small next to their bytes.
 #include "cci_launch.hpp"
 
 namespace cci {

@@ -257,8 +257,73 @@ hipError_t launch_r(const ProductArgs& a, hipStream_t s) {
   }
 }
 
+// Few rows (N <= kSmallRows, FC / plain rows): the row-tiled kernel would
+// launch a handful of workgroups.  Instead one wave computes the G outputs
+// of one group for one row n (Alg. 1's output-stationary registers): its
+// lanes run over the columns c (coalesced reads of X[n][.] and of the packed
+// stream), each adds vals * x of every kept slot to the accumulator of the
+// slot's row, and a wave reduction sums the lanes' partial sums.
+constexpr int64_t kSmallRows = 256;
+
+template <int G, typename XT, typename VT, typename YT>
+__global__ __launch_bounds__(kThreads) void sparse_mac_rows_kernel(const XT* __restrict__ X, int64_t N, int64_t C,
+                                                                   const VT* __restrict__ vals,
+                                                                   const uint8_t* __restrict__ idx, int64_t O,
+                                                                   int32_t K, Epilogue<YT> ep, YT* __restrict__ Y) {
+  const int lane = threadIdx.x & 63;
+  const int64_t ngroups = O / G;
+  const int64_t wv = static_cast<int64_t>(blockIdx.x) * (kThreads / 64) + (threadIdx.x >> 6);
+  if (wv >= N * ngroups) return;  // whole wave
+  const int64_t n = wv / ngroups, g = wv - n * ngroups;
+  float acc[G];
+#pragma unroll
+  for (int r = 0; r < G; ++r) acc[r] = 0.0f;
+  for (int64_t c = lane; c < C; c += 64) {
+    const float x = io<XT>::load(X, n * C + c);
+#pragma unroll 4
+    for (int32_t k = 0; k < K; ++k) {
+      const int64_t q = (g * K + k) * C + c;
+      const uint32_t i = idx[q];
+      const float v = io<VT>::load(vals, q) * x;
+#pragma unroll
+      for (int r = 0; r < G; ++r) acc[r] += i == static_cast<uint32_t>(r) ? v : 0.0f;
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < G; ++r)
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) acc[r] += __shfl_xor(acc[r], off, 64);
+  if (lane < G) {
+    float y = acc[0];
+#pragma unroll
+    for (int r = 1; r < G; ++r) y = lane == r ? acc[r] : y;
+    const int64_t o = g * G + lane;
+    io<YT>::store(Y, n * O + o, apply_epilogue<YT>(y, o, n * O + o, ep));
+  }
+}
+
+template <typename XT, typename VT, typename YT>
+hipError_t launch_rows(const ProductArgs& a, hipStream_t s) {
+  const int64_t waves = a.N * (a.O / a.G);
+  const dim3 grid(static_cast<uint32_t>((waves + kThreads / 64 - 1) / (kThreads / 64)));
+  Epilogue<YT> ep{a.scale, a.bias, static_cast<const YT*>(a.residual), a.relu};
+  const auto X = static_cast<const XT*>(a.X);
+  const auto V = static_cast<const VT*>(a.vals);
+  const auto Y = static_cast<YT*>(a.Y);
+  switch (a.G) {
+    case 2: hipLaunchKernelGGL((sparse_mac_rows_kernel<2, XT, VT, YT>), grid, dim3(kThreads), 0, s, X, a.N, a.C, V, a.idx, a.O, a.K, ep, Y); break;
+    case 4: hipLaunchKernelGGL((sparse_mac_rows_kernel<4, XT, VT, YT>), grid, dim3(kThreads), 0, s, X, a.N, a.C, V, a.idx, a.O, a.K, ep, Y); break;
+    case 8: hipLaunchKernelGGL((sparse_mac_rows_kernel<8, XT, VT, YT>), grid, dim3(kThreads), 0, s, X, a.N, a.C, V, a.idx, a.O, a.K, ep, Y); break;
+    case 16: hipLaunchKernelGGL((sparse_mac_rows_kernel<16, XT, VT, YT>), grid, dim3(kThreads), 0, s, X, a.N, a.C, V, a.idx, a.O, a.K, ep, Y); break;
+    case 32: hipLaunchKernelGGL((sparse_mac_rows_kernel<32, XT, VT, YT>), grid, dim3(kThreads), 0, s, X, a.N, a.C, V, a.idx, a.O, a.K, ep, Y); break;
+    default: return hipErrorInvalidConfiguration;
+  }
+  return hipGetLastError();
+}
+
 template <typename XT, typename VT, typename YT>
 hipError_t launch_t(const ProductArgs& a, hipStream_t s) {
+  if (!a.conv && a.N <= kSmallRows) return launch_rows<XT, VT, YT>(a, s);
   // Small row counts: one row per lane keeps more workgroups in flight.
   if (a.N <= 4096) return launch_r<1, XT, VT, YT>(a, s);
   return launch_r<4, XT, VT, YT>(a, s);

@@ -13,8 +13,14 @@
  * ---------------------------------------
  *  - Memory.  Every tensor argument is a device pointer to caller-owned,
  *    contiguous, row-major memory on the current HIP device.  The library
- *    never allocates, frees or synchronises, and keeps no state between calls
- *    apart from a thread-local error string.
+ *    never allocates, frees or synchronises.
+ *  - State.  Between calls the library keeps only (a) a thread-local error
+ *    string and (b) per-device launch set-up computed on the first launch of
+ *    a kernel with that device current: the kernel's dynamic-LDS limit
+ *    (hipFuncSetAttribute) and, for the narrow kernels, the number of
+ *    resident waves (an occupancy query).  (b) is written once per device
+ *    (a racing first call recomputes the same value) and read-only after;
+ *    no call's result depends on an earlier call's data.
  *  - Streams.  `stream` is a hipStream_t passed as void* (NULL = the default
  *    stream).  Calls only enqueue work; results are ready once the stream is.
  *  - Errors.  Arguments are validated before anything is enqueued; on a
@@ -124,13 +130,12 @@ cci_status cci_pack(const float *W, int64_t O, int64_t C, int32_t G,
  *                                     vals[g][k][c] * X[n][c] ),  g = o / G.
  * X: device [N][C] of x_t.  vals/idx as produced by cci_pack.  Y: device
  * [N][O] of y_t.  Supported (x_t, val_t, y_t): (F32, F32, F32) and
- * (BF16, BF16, BF16 or F32); anything else is CCI_EUNSUPPORTED.
- * algo selects the kernel family (see cci_algo); an explicit choice whose
- * requirements the shape does not meet returns CCI_EUNSUPPORTED. */
+ * (BF16, BF16, BF16 or F32); anything else is CCI_EUNSUPPORTED.  The kernel
+ * family is the library's choice (CCI_ALGO_AUTO). */
 cci_status cci_spmm(const void *X, cci_dtype x_t, int64_t N, int64_t C,
                     const void *vals, cci_dtype val_t, const uint8_t *idx,
                     int64_t O, int32_t G, int32_t K, const cci_epilogue *ep,
-                    void *Y, cci_dtype y_t, cci_algo algo, void *stream);
+                    void *Y, cci_dtype y_t, void *stream);
 
 /* Convolution lowered to the CCI product (Sec. 3.2) without materialising
  * the im2col matrix.  X: device NHWC [B][H][W][Cin].  The packed weights
@@ -138,14 +143,33 @@ cci_status cci_spmm(const void *X, cci_dtype x_t, int64_t N, int64_t C,
  * (kh, kw, cin) order.  Output pixel p = (b*Ho + oh)*Wo + ow with
  * Ho = (H + 2*pad_h - KH)/stride_h + 1 (Wo likewise); Y: device NHWC
  * [B][Ho][Wo][O], i.e. [N][O] with N = B*Ho*Wo.  Input taps outside the
- * image read as 0.  Dtypes, epilogue and algo as for cci_spmm. */
+ * image read as 0.  Dtypes and epilogue as for cci_spmm; the kernel family
+ * is the library's choice. */
 cci_status cci_conv_im2col(const void *X, cci_dtype x_t, int64_t B, int64_t H,
                            int64_t W, int64_t Cin, int32_t KH, int32_t KW,
                            int32_t stride_h, int32_t stride_w, int32_t pad_h,
                            int32_t pad_w, const void *vals, cci_dtype val_t,
                            const uint8_t *idx, int64_t O, int32_t G, int32_t K,
                            const cci_epilogue *ep, void *Y, cci_dtype y_t,
-                           cci_algo algo, void *stream);
+                           void *stream);
+
+/* cci_spmm / cci_conv_im2col with the kernel family pinned (see cci_algo;
+ * CCI_ALGO_AUTO gives the plain calls).  Same arguments, result and
+ * errors; an explicit family whose requirements the shape does not meet
+ * returns CCI_EUNSUPPORTED.  For benchmarking and testing each family. */
+cci_status cci_spmm_algo(const void *X, cci_dtype x_t, int64_t N, int64_t C,
+                         const void *vals, cci_dtype val_t, const uint8_t *idx,
+                         int64_t O, int32_t G, int32_t K,
+                         const cci_epilogue *ep, void *Y, cci_dtype y_t,
+                         cci_algo algo, void *stream);
+cci_status cci_conv_im2col_algo(const void *X, cci_dtype x_t, int64_t B,
+                                int64_t H, int64_t W, int64_t Cin, int32_t KH,
+                                int32_t KW, int32_t stride_h, int32_t stride_w,
+                                int32_t pad_h, int32_t pad_w, const void *vals,
+                                cci_dtype val_t, const uint8_t *idx, int64_t O,
+                                int32_t G, int32_t K, const cci_epilogue *ep,
+                                void *Y, cci_dtype y_t, cci_algo algo,
+                                void *stream);
 
 /* Which family CCI_ALGO_AUTO picks for a product of N x C x O (conv: pass
  * N = B*Ho*Wo, C = KH*KW*Cin and cin = Cin; FC: cin = C).  Host-only.  A

@@ -75,6 +75,8 @@ def _load():
     lib.oracle_global_avgpool_nhwc.argtypes = [
         _f32p, _i64, _i64, _i64, _i64, _f64p]
     lib.oracle_num_threads.restype = ctypes.c_int
+    lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
+    lib.oracle_set_num_threads.restype = None
     for fn in ("oracle_pack", "oracle_unpack", "oracle_spmm_rows",
                "oracle_dense_rows", "oracle_conv2d_nhwc_rows",
                "oracle_im2col_nhwc", "oracle_maxpool2d_nhwc",
@@ -101,6 +103,11 @@ def _check(rc: int, what: str):
 
 def num_threads() -> int:
     return int(_load().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of the oracle's later parallel loops (timing only)."""
+    _load().oracle_set_num_threads(int(n))
 
 
 def pack(W: np.ndarray, G: int, K: int):

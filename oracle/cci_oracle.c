@@ -368,3 +368,14 @@ int oracle_num_threads(void) {
   return 1;
 #endif
 }
+
+/* Thread count of later parallel loops started from the calling thread (a
+ * timing knob: no result depends on it). */
+void oracle_set_num_threads(int n) {
+#ifdef _OPENMP
+  extern void omp_set_num_threads(int);
+  if (n >= 1) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}

@@ -44,11 +44,14 @@ _lib = ctypes.CDLL(LIB_PATH)
 _vp, _i64, _i32, _sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
 _lib.cci_packed_sizes.argtypes = [_i64, _i64, _i32, _i32, ctypes.c_int, ctypes.POINTER(_sz), ctypes.POINTER(_sz)]
 _lib.cci_pack.argtypes = [_vp, _i64, _i64, _i32, _i32, _vp, ctypes.c_int, _vp, _vp]
-_lib.cci_spmm.argtypes = [_vp, ctypes.c_int, _i64, _i64, _vp, ctypes.c_int, _vp, _i64, _i32, _i32,
-                          ctypes.POINTER(Epilogue), _vp, ctypes.c_int, ctypes.c_int, _vp]
-_lib.cci_conv_im2col.argtypes = [_vp, ctypes.c_int, _i64, _i64, _i64, _i64, _i32, _i32, _i32, _i32,
-                                 _i32, _i32, _vp, ctypes.c_int, _vp, _i64, _i32, _i32,
-                                 ctypes.POINTER(Epilogue), _vp, ctypes.c_int, ctypes.c_int, _vp]
+_SPMM = [_vp, ctypes.c_int, _i64, _i64, _vp, ctypes.c_int, _vp, _i64, _i32, _i32, ctypes.POINTER(Epilogue), _vp,
+         ctypes.c_int]
+_CONV = [_vp, ctypes.c_int, _i64, _i64, _i64, _i64, _i32, _i32, _i32, _i32, _i32, _i32, _vp, ctypes.c_int, _vp,
+         _i64, _i32, _i32, ctypes.POINTER(Epilogue), _vp, ctypes.c_int]
+_lib.cci_spmm.argtypes = _SPMM + [_vp]
+_lib.cci_spmm_algo.argtypes = _SPMM + [ctypes.c_int, _vp]
+_lib.cci_conv_im2col.argtypes = _CONV + [_vp]
+_lib.cci_conv_im2col_algo.argtypes = _CONV + [ctypes.c_int, _vp]
 _lib.cci_auto_algo.argtypes = [ctypes.c_int, ctypes.c_int, _i64, _i64, _i64, _i64, _i32, _i32]
 _lib.cci_auto_algo.restype = ctypes.c_int
 _lib.cci_maxpool2d_nhwc.argtypes = [_vp, ctypes.c_int, _i64, _i64, _i64, _i64, _i32, _i32, _i32, _vp, _vp]
@@ -57,8 +60,8 @@ _lib.cci_status_str.argtypes = [ctypes.c_int]
 _lib.cci_status_str.restype = ctypes.c_char_p
 _lib.cci_last_error.restype = ctypes.c_char_p
 _lib.cci_version.restype = ctypes.c_int32
-for _fn in ("cci_packed_sizes", "cci_pack", "cci_spmm", "cci_conv_im2col", "cci_maxpool2d_nhwc",
-            "cci_global_avgpool_nhwc"):
+for _fn in ("cci_packed_sizes", "cci_pack", "cci_spmm", "cci_spmm_algo", "cci_conv_im2col",
+            "cci_conv_im2col_algo", "cci_maxpool2d_nhwc", "cci_global_avgpool_nhwc"):
     getattr(_lib, _fn).restype = ctypes.c_int
 
 
@@ -143,27 +146,49 @@ def pack(W: torch.Tensor, G: int, K: int, val_dtype=torch.bfloat16, out=None):
     return vals, idx
 
 
-def _epilogue(scale, bias, residual, relu):
-    for t in (scale, bias, residual):
+def _epilogue(scale, bias, residual, relu, O, y_shape, y_dtype, device):
+    """Marshal the fused epilogue after checking what the kernels will read:
+    scale / bias fp32 [O], residual of Y's shape and dtype, all contiguous
+    on Y's device."""
+    for name, t in (("scale", scale), ("bias", bias)):
         if t is not None:
             _dev(t)
+            if t.dtype != torch.float32 or t.numel() != O or t.device != device:
+                raise ValueError(f"{name} must be a contiguous float32 tensor of {O} elements on {device}")
+    if residual is not None:
+        _dev(residual)
+        if tuple(residual.shape) != tuple(y_shape) or residual.dtype != y_dtype or residual.device != device:
+            raise ValueError(f"residual must be a contiguous {y_dtype} tensor of shape {tuple(y_shape)} on {device}")
     return Epilogue(_ptr(scale), _ptr(bias), _ptr(residual), int(bool(relu)))
+
+
+def _out(out, shape, dtype, device):
+    if out is None:
+        return torch.empty(shape, dtype=dtype, device=device)
+    _dev(out)
+    if tuple(out.shape) != tuple(shape) or out.dtype != dtype or out.device != device:
+        raise ValueError(f"out must be a contiguous {dtype} tensor of shape {tuple(shape)} on {device}")
+    return out
 
 
 def spmm(X: torch.Tensor, vals: torch.Tensor, idx: torch.Tensor, G: int, *, scale=None, bias=None,
          residual=None, relu=False, out_dtype=None, algo="auto", out=None) -> torch.Tensor:
-    """cci_spmm: Y [N, O] = epilogue(X [N, C] . W_hat^T) from packed (vals, idx)."""
+    """cci_spmm (cci_spmm_algo when `algo` pins a kernel family):
+    Y [N, O] = epilogue(X [N, C] . W_hat^T) from packed (vals, idx)."""
     _dev(X), _dev(vals), _dev(idx)
     N, C = X.shape
     ng, K, C2 = vals.shape
-    if C2 != C or tuple(idx.shape) != tuple(vals.shape):
+    if C2 != C or tuple(idx.shape) != tuple(vals.shape) or idx.dtype != torch.uint8:
         raise ValueError("shape mismatch between X and packed weights")
+    if vals.device != X.device or idx.device != X.device:
+        raise ValueError("X and the packed weights must be on one device")
     O = ng * G
-    out_dtype = out_dtype or X.dtype
-    Y = out if out is not None else torch.empty((N, O), dtype=out_dtype, device=X.device)
-    ep = _epilogue(scale, bias, residual, relu)
-    _check(_lib.cci_spmm(_ptr(X), _code(X.dtype), N, C, _ptr(vals), _code(vals.dtype), _ptr(idx), O, G, K,
-                         ctypes.byref(ep), _ptr(Y), _code(Y.dtype), _algo(algo), _stream(X)))
+    Y = _out(out, (N, O), out_dtype or X.dtype, X.device)
+    ep = _epilogue(scale, bias, residual, relu, O, Y.shape, Y.dtype, X.device)
+    args = (_ptr(X), _code(X.dtype), N, C, _ptr(vals), _code(vals.dtype), _ptr(idx), O, G, K, ctypes.byref(ep),
+            _ptr(Y), _code(Y.dtype))
+    a = _algo(algo)
+    _check(_lib.cci_spmm(*args, _stream(X)) if a == ALGO_AUTO else _lib.cci_spmm_algo(*args, a, _stream(X)))
     return Y
 
 
@@ -174,20 +199,24 @@ def conv_out_hw(H, W, KH, KW, stride, pad):
 def conv_im2col(X: torch.Tensor, vals: torch.Tensor, idx: torch.Tensor, G: int, KH: int, KW: int,
                 stride=(1, 1), pad=(0, 0), *, scale=None, bias=None, residual=None, relu=False,
                 out_dtype=None, algo="auto", out=None) -> torch.Tensor:
-    """cci_conv_im2col: NHWC X [B, H, W, Cin] -> NHWC Y [B, Ho, Wo, O]."""
+    """cci_conv_im2col (cci_conv_im2col_algo when `algo` pins a kernel
+    family): NHWC X [B, H, W, Cin] -> NHWC Y [B, Ho, Wo, O]."""
     _dev(X), _dev(vals), _dev(idx)
     B, H, W, Cin = X.shape
     ng, K, C = vals.shape
-    if C != KH * KW * Cin:
+    if C != KH * KW * Cin or tuple(idx.shape) != tuple(vals.shape) or idx.dtype != torch.uint8:
         raise ValueError("packed weights do not match KH*KW*Cin")
+    if vals.device != X.device or idx.device != X.device:
+        raise ValueError("X and the packed weights must be on one device")
     O = ng * G
     Ho, Wo = conv_out_hw(H, W, KH, KW, stride, pad)
-    out_dtype = out_dtype or X.dtype
-    Y = out if out is not None else torch.empty((B, Ho, Wo, O), dtype=out_dtype, device=X.device)
-    ep = _epilogue(scale, bias, residual, relu)
-    _check(_lib.cci_conv_im2col(_ptr(X), _code(X.dtype), B, H, W, Cin, KH, KW, stride[0], stride[1],
-                                pad[0], pad[1], _ptr(vals), _code(vals.dtype), _ptr(idx), O, G, K,
-                                ctypes.byref(ep), _ptr(Y), _code(Y.dtype), _algo(algo), _stream(X)))
+    Y = _out(out, (B, Ho, Wo, O), out_dtype or X.dtype, X.device)
+    ep = _epilogue(scale, bias, residual, relu, O, Y.shape, Y.dtype, X.device)
+    args = (_ptr(X), _code(X.dtype), B, H, W, Cin, KH, KW, stride[0], stride[1], pad[0], pad[1], _ptr(vals),
+            _code(vals.dtype), _ptr(idx), O, G, K, ctypes.byref(ep), _ptr(Y), _code(Y.dtype))
+    a = _algo(algo)
+    _check(_lib.cci_conv_im2col(*args, _stream(X)) if a == ALGO_AUTO
+           else _lib.cci_conv_im2col_algo(*args, a, _stream(X)))
     return Y
 
 

@@ -183,9 +183,9 @@ cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C, int
   return CCI_ALGO_SPARSE_MAC;
 }
 
-cci_status cci_spmm(const void* X, cci_dtype x_t, int64_t N, int64_t C, const void* vals,
-                    cci_dtype val_t, const uint8_t* idx, int64_t O, int32_t G, int32_t K,
-                    const cci_epilogue* ep, void* Y, cci_dtype y_t, cci_algo algo, void* stream) {
+cci_status cci_spmm_algo(const void* X, cci_dtype x_t, int64_t N, int64_t C, const void* vals,
+                         cci_dtype val_t, const uint8_t* idx, int64_t O, int32_t G, int32_t K,
+                         const cci_epilogue* ep, void* Y, cci_dtype y_t, cci_algo algo, void* stream) {
   if (cci_status s = check_groups(O, C, G, K)) return s;
   if (N < 0) return fail(CCI_EINVAL, "N=%lld < 0", (long long)N);
   if (cci_status s = check_types(x_t, val_t, y_t)) return s;
@@ -210,12 +210,12 @@ cci_status cci_spmm(const void* X, cci_dtype x_t, int64_t N, int64_t C, const vo
   return run_product(a, algo, ep, stream);
 }
 
-cci_status cci_conv_im2col(const void* X, cci_dtype x_t, int64_t B, int64_t H, int64_t W,
-                           int64_t Cin, int32_t KH, int32_t KW, int32_t stride_h, int32_t stride_w,
-                           int32_t pad_h, int32_t pad_w, const void* vals, cci_dtype val_t,
-                           const uint8_t* idx, int64_t O, int32_t G, int32_t K,
-                           const cci_epilogue* ep, void* Y, cci_dtype y_t, cci_algo algo,
-                           void* stream) {
+cci_status cci_conv_im2col_algo(const void* X, cci_dtype x_t, int64_t B, int64_t H, int64_t W,
+                                int64_t Cin, int32_t KH, int32_t KW, int32_t stride_h,
+                                int32_t stride_w, int32_t pad_h, int32_t pad_w, const void* vals,
+                                cci_dtype val_t, const uint8_t* idx, int64_t O, int32_t G,
+                                int32_t K, const cci_epilogue* ep, void* Y, cci_dtype y_t,
+                                cci_algo algo, void* stream) {
   if (B < 0 || H < 1 || W < 1 || Cin < 1 || KH < 1 || KW < 1 || stride_h < 1 || stride_w < 1 ||
       pad_h < 0 || pad_w < 0)
     return fail(CCI_EINVAL, "bad convolution geometry");
@@ -253,6 +253,21 @@ cci_status cci_conv_im2col(const void* X, cci_dtype x_t, int64_t B, int64_t H, i
   a.Y = Y;
   a.y_t = to_dt(y_t);
   return run_product(a, algo, ep, stream);
+}
+
+cci_status cci_spmm(const void* X, cci_dtype x_t, int64_t N, int64_t C, const void* vals,
+                    cci_dtype val_t, const uint8_t* idx, int64_t O, int32_t G, int32_t K,
+                    const cci_epilogue* ep, void* Y, cci_dtype y_t, void* stream) {
+  return cci_spmm_algo(X, x_t, N, C, vals, val_t, idx, O, G, K, ep, Y, y_t, CCI_ALGO_AUTO, stream);
+}
+
+cci_status cci_conv_im2col(const void* X, cci_dtype x_t, int64_t B, int64_t H, int64_t W,
+                           int64_t Cin, int32_t KH, int32_t KW, int32_t stride_h, int32_t stride_w,
+                           int32_t pad_h, int32_t pad_w, const void* vals, cci_dtype val_t,
+                           const uint8_t* idx, int64_t O, int32_t G, int32_t K,
+                           const cci_epilogue* ep, void* Y, cci_dtype y_t, void* stream) {
+  return cci_conv_im2col_algo(X, x_t, B, H, W, Cin, KH, KW, stride_h, stride_w, pad_h, pad_w, vals,
+                              val_t, idx, O, G, K, ep, Y, y_t, CCI_ALGO_AUTO, stream);
 }
 
 cci_status cci_maxpool2d_nhwc(const void* X, cci_dtype t, int64_t B, int64_t H, int64_t W,

@@ -1049,9 +1049,9 @@ void fill_params(const ProductArgs& a, Params& p) {
 
 template <typename YT, bool RECT, int MT>
 hipError_t launch_yrm(const Params& p, uint32_t grid, hipStream_t s) {
-  static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(&dense_tile_kernel<YT, RECT, MT>), hipFuncAttributeMaxDynamicSharedMemorySize,
-      kLdsMax);
+  static std::atomic<int8_t> lds_set[kMaxDevices];
+  const hipError_t attr =
+      set_lds_limit_once(lds_set, reinterpret_cast<const void*>(&dense_tile_kernel<YT, RECT, MT>), kLdsMax);
   if (attr != hipSuccess) return attr;
   size_t lds = static_cast<size_t>(p.lds_bytes);
   const size_t staging = static_cast<size_t>(kWaves) * MT * 16 * kStPitch;  // epilogue reuses the LDS

@@ -6,9 +6,34 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "cci_device.hpp"
 
 namespace cci {
+
+// Per-device set-up that a launcher needs once (a kernel's dynamic-LDS
+// limit, an occupancy query).  Slot d holds the result for HIP device d,
+// computed on the first launch with d current; a racing first launch on
+// another thread computes the same value again, which is harmless.  These
+// are the only values the library keeps between calls.
+constexpr int kMaxDevices = 64;
+
+inline int current_device() {
+  int d = 0;
+  if (hipGetDevice(&d) != hipSuccess || d < 0 || d >= kMaxDevices) return -1;
+  return d;
+}
+
+// Raises `fn`'s dynamic-LDS limit to `bytes` once per device.
+inline hipError_t set_lds_limit_once(std::atomic<int8_t> (&done)[kMaxDevices], const void* fn,
+                                     int bytes) {
+  const int d = current_device();
+  if (d >= 0 && done[d].load(std::memory_order_acquire)) return hipSuccess;
+  const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  if (e == hipSuccess && d >= 0) done[d].store(1, std::memory_order_release);
+  return e;
+}
 
 enum class DType { F32 = 0, BF16 = 1 };
 

@@ -326,18 +326,25 @@ __global__ __launch_bounds__(kThreads) void narrow_kernel(NParams p) {
   narrow_body<YT, S, CM, RES>(p, sb);
 }
 
-// Waves of narrow_kernel<YT, S> that fit on the device at once (queried once).
+// Waves of narrow_kernel<YT, S> that fit on the current device at once
+// (queried once per device).
 template <typename YT, int S, int CM, bool RES>
 int64_t resident_waves() {
-  static const int64_t waves = [] {
-    int dev = 0, cus = 0, blocks = 0;
-    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, reinterpret_cast<const void*>(&narrow_kernel<YT, S, CM, RES>),
-                                                     kThreads, 0) != hipSuccess ||
-        cus < 1 || blocks < 1)
-      return static_cast<int64_t>(kWavesTarget);
-    return static_cast<int64_t>(cus) * blocks * (kThreads / 64);
-  }();
+  static std::atomic<int64_t> cached[kMaxDevices];
+  const int dev = current_device();
+  if (dev >= 0) {
+    const int64_t w = cached[dev].load(std::memory_order_acquire);
+    if (w > 0) return w;
+  }
+  int cus = 0, blocks = 0;
+  int64_t waves = static_cast<int64_t>(kWavesTarget);
+  if (dev >= 0 && hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, reinterpret_cast<const void*>(&narrow_kernel<YT, S, CM, RES>),
+                                                   kThreads, 0) == hipSuccess &&
+      cus >= 1 && blocks >= 1) {
+    waves = static_cast<int64_t>(cus) * blocks * (kThreads / 64);
+    cached[dev].store(waves, std::memory_order_release);
+  }
   return waves;
 }
 

@@ -622,9 +622,9 @@ bool plain_rows(const ProductArgs& a) {
 
 template <typename YT, int PT, int UPL, int UE, bool FULL, bool BIGG, bool MASK>
 hipError_t launch_wu(const WParams& p, uint32_t grid, hipStream_t s) {
-  static const hipError_t attr =
-      hipFuncSetAttribute(reinterpret_cast<const void*>(&wide_tile_kernel<YT, PT, UPL, UE, FULL, BIGG, MASK>),
-                          hipFuncAttributeMaxDynamicSharedMemorySize, kLds);
+  static std::atomic<int8_t> lds_set[kMaxDevices];
+  const hipError_t attr = set_lds_limit_once(
+      lds_set, reinterpret_cast<const void*>(&wide_tile_kernel<YT, PT, UPL, UE, FULL, BIGG, MASK>), kLds);
   if (attr != hipSuccess) return attr;
   hipLaunchKernelGGL((wide_tile_kernel<YT, PT, UPL, UE, FULL, BIGG, MASK>), dim3(grid), dim3(kThreads), kLds, s, p);
   return hipGetLastError();

@@ -57,12 +57,17 @@ class ResNet50CCI:
                                scale=sc, bias=bi, residual=residual, relu=L.relu, out_dtype=torch.bfloat16)
 
     def stem_input(self, X: torch.Tensor) -> torch.Tensor:
-        """X [B, H, W, 3] copied into channels 0..2 of a [B, H, W, STEM_CIN]
-        buffer whose last channel is zeroed when the buffer is allocated."""
-        shape = tuple(X.shape[:3]) + (STEM_CIN,)
+        """X [B, H, W, 3] copied into channels 0..2 of a [B, H, W', STEM_CIN]
+        buffer whose other entries are zeroed when the buffer is allocated.
+        W' = W rounded up to even: with 8 tap columns (the eighth all-zero)
+        at stride 2 the output width (W' + 2*3 - 8)/2 + 1 then equals the
+        7-tap width (W + 2*3 - 7)/2 + 1 for odd W too, and the extra input
+        column is the zero padding the 7x7 conv would read there."""
+        B, H, W, C = X.shape
+        shape = (B, H, W + (W & 1), STEM_CIN)
         if self._stem_in is None or tuple(self._stem_in.shape) != shape:
             self._stem_in = torch.zeros(shape, dtype=X.dtype, device=X.device)
-        self._stem_in[..., :X.shape[3]].copy_(X)
+        self._stem_in[:, :, :W, :C].copy_(X)
         return self._stem_in
 
     def forward(self, X: torch.Tensor, record: list | None = None) -> torch.Tensor:

@@ -10,6 +10,28 @@ from parity import TOL, bits_u16, check_close, to_np_f32
 DEV = "cuda:0"
 
 
+GUARD_BYTES = 4096   # sentinel bytes on each side of an output buffer
+SENTINEL = 0x7F      # bf16 0x7F7F / fp32 0x7F7F7F7F: huge finite values, so an output left unwritten fails too
+
+
+class Guarded:
+    """An output tensor inside a larger device buffer whose margins hold a
+    sentinel byte: `check()` asserts that no kernel wrote outside the output
+    (the body starts as the sentinel too, so an unwritten element fails the
+    value comparison)."""
+
+    def __init__(self, shape, dtype, device=DEV):
+        self.nbytes = int(np.prod(shape)) * torch.empty((), dtype=dtype).element_size()
+        self.buf = torch.full((self.nbytes + 2 * GUARD_BYTES,), SENTINEL, dtype=torch.uint8, device=device)
+        self.t = self.buf[GUARD_BYTES:GUARD_BYTES + self.nbytes].view(dtype).view(shape)
+
+    def check(self, what=""):
+        head = self.buf[:GUARD_BYTES]
+        tail = self.buf[GUARD_BYTES + self.nbytes:]
+        ok = bool((head == SENTINEL).all()) and bool((tail == SENTINEL).all())
+        assert ok, f"{what}: a kernel wrote outside its output buffer"
+
+
 def need_gpu():
     if not torch.cuda.is_available():
         pytest.skip("no GPU")

@@ -14,7 +14,8 @@ FAKE_MIS = ctypes.c_void_p(0x10008)      # 8-byte aligned only
 
 def test_exports_every_declared_symbol():
     names = cci.header_functions()
-    assert {"cci_pack", "cci_spmm", "cci_conv_im2col", "cci_packed_sizes"} <= set(names)
+    assert {"cci_pack", "cci_spmm", "cci_conv_im2col", "cci_packed_sizes", "cci_spmm_algo",
+            "cci_conv_im2col_algo"} <= set(names)
     for n in names:
         assert hasattr(lib, n), f"libcci.so does not export {n}"
     assert cci.version() >= 100
@@ -36,82 +37,92 @@ def test_bad_group_arguments(O, C, G, K):
     assert lib.cci_last_error()
     assert lib.cci_pack(FAKE, O, C, G, K, FAKE, cci.BF16, FAKE, None) == cci.EINVAL
     assert lib.cci_spmm(FAKE, cci.BF16, 4, C, FAKE, cci.BF16, FAKE, O, G, K, None, FAKE,
-                        cci.BF16, 0, None) == cci.EINVAL
+                        cci.BF16, None) == cci.EINVAL
 
 
 def test_null_and_alignment_errors():
     assert lib.cci_pack(None, 16, 8, 8, 2, FAKE, cci.F32, FAKE, None) == cci.EINVAL
     assert lib.cci_pack(FAKE_MIS, 16, 8, 8, 2, FAKE, cci.F32, FAKE, None) == cci.EALIGN
     assert lib.cci_spmm(FAKE, cci.F32, 4, 8, FAKE, cci.F32, FAKE, 16, 8, 2, None, None,
-                        cci.F32, 0, None) == cci.EINVAL
+                        cci.F32, None) == cci.EINVAL
     assert lib.cci_spmm(FAKE, cci.F32, 4, 8, FAKE, cci.F32, FAKE_MIS, 16, 8, 2, None, FAKE,
-                        cci.F32, 0, None) == cci.EALIGN
+                        cci.F32, None) == cci.EALIGN
     ep = cci.Epilogue(ctypes.c_void_p(0x10004), None, None, 0)
     assert lib.cci_spmm(FAKE, cci.F32, 4, 8, FAKE, cci.F32, FAKE, 16, 8, 2, ctypes.byref(ep),
-                        FAKE, cci.F32, 0, None) == cci.EALIGN
+                        FAKE, cci.F32, None) == cci.EALIGN
     assert "align" in lib.cci_last_error().decode()
 
 
 def test_dtype_combinations():
     # f32 X with bf16 values, bf16 X with f32 values: unsupported
     assert lib.cci_spmm(FAKE, cci.F32, 4, 8, FAKE, cci.BF16, FAKE, 16, 8, 2, None, FAKE,
-                        cci.F32, 0, None) == cci.EUNSUPPORTED
+                        cci.F32, None) == cci.EUNSUPPORTED
     assert lib.cci_spmm(FAKE, cci.BF16, 4, 8, FAKE, cci.F32, FAKE, 16, 8, 2, None, FAKE,
-                        cci.BF16, 0, None) == cci.EUNSUPPORTED
+                        cci.BF16, None) == cci.EUNSUPPORTED
     assert lib.cci_spmm(FAKE, cci.F32, 4, 8, FAKE, cci.F32, FAKE, 16, 8, 2, None, FAKE,
-                        cci.BF16, 0, None) == cci.EUNSUPPORTED
+                        cci.BF16, None) == cci.EUNSUPPORTED
     assert lib.cci_spmm(FAKE, 7, 4, 8, FAKE, cci.F32, FAKE, 16, 8, 2, None, FAKE,
-                        cci.F32, 0, None) == cci.EINVAL
+                        cci.F32, None) == cci.EINVAL
 
 
 def test_explicit_algo_requirements():
     # dense-tile MFMA needs bf16 and C % 32 == 0; sparse-MAC needs G in {2,4,8,16,32}
-    assert lib.cci_spmm(FAKE, cci.F32, 4, 64, FAKE, cci.F32, FAKE, 16, 8, 2, None, FAKE,
+    assert lib.cci_spmm_algo(FAKE, cci.F32, 4, 64, FAKE, cci.F32, FAKE, 16, 8, 2, None, FAKE,
                         cci.F32, cci.ALGO_DENSE_TILE_MFMA, None) == cci.EUNSUPPORTED
-    assert lib.cci_spmm(FAKE, cci.BF16, 4, 40, FAKE, cci.BF16, FAKE, 16, 8, 2, None, FAKE,
+    assert lib.cci_spmm_algo(FAKE, cci.BF16, 4, 40, FAKE, cci.BF16, FAKE, 16, 8, 2, None, FAKE,
                         cci.BF16, cci.ALGO_DENSE_TILE_MFMA, None) == cci.EUNSUPPORTED
-    assert lib.cci_spmm(FAKE, cci.BF16, 4, 64, FAKE, cci.BF16, FAKE, 24, 6, 2, None, FAKE,
+    assert lib.cci_spmm_algo(FAKE, cci.BF16, 4, 64, FAKE, cci.BF16, FAKE, 24, 6, 2, None, FAKE,
                         cci.BF16, cci.ALGO_SPARSE_MAC, None) == cci.EUNSUPPORTED
-    assert lib.cci_spmm(FAKE, cci.BF16, 4, 64, FAKE, cci.BF16, FAKE, 16, 8, 2, None, FAKE,
+    assert lib.cci_spmm_algo(FAKE, cci.BF16, 4, 64, FAKE, cci.BF16, FAKE, 16, 8, 2, None, FAKE,
                         cci.BF16, 9, None) == cci.EINVAL
     # wide-tile MFMA: O % 256, C % 64, 64 % G, bf16 only; strided / padded / k x k convs refused
     W = cci.ALGO_WIDE_TILE_MFMA
-    assert lib.cci_spmm(FAKE, cci.BF16, 4, 64, FAKE, cci.BF16, FAKE, 128, 8, 2, None, FAKE,
+    assert lib.cci_spmm_algo(FAKE, cci.BF16, 4, 64, FAKE, cci.BF16, FAKE, 128, 8, 2, None, FAKE,
                         cci.BF16, W, None) == cci.EUNSUPPORTED
-    assert lib.cci_spmm(FAKE, cci.BF16, 4, 96, FAKE, cci.BF16, FAKE, 256, 8, 2, None, FAKE,
+    assert lib.cci_spmm_algo(FAKE, cci.BF16, 4, 96, FAKE, cci.BF16, FAKE, 256, 8, 2, None, FAKE,
                         cci.BF16, W, None) == cci.EUNSUPPORTED
-    assert lib.cci_spmm(FAKE, cci.F32, 4, 64, FAKE, cci.F32, FAKE, 256, 8, 2, None, FAKE,
+    assert lib.cci_spmm_algo(FAKE, cci.F32, 4, 64, FAKE, cci.F32, FAKE, 256, 8, 2, None, FAKE,
                         cci.F32, W, None) == cci.EUNSUPPORTED
-    assert lib.cci_spmm(FAKE, cci.BF16, 4, 64, FAKE, cci.BF16, FAKE, 256, 128, 2, None, FAKE,
+    assert lib.cci_spmm_algo(FAKE, cci.BF16, 4, 64, FAKE, cci.BF16, FAKE, 256, 128, 2, None, FAKE,
                         cci.BF16, W, None) == cci.EUNSUPPORTED
     for KH, sh, ph in [(3, 1, 1), (1, 2, 0), (1, 1, 1)]:
-        assert lib.cci_conv_im2col(FAKE, cci.BF16, 1, 8, 8, 64, KH, KH, sh, sh, ph, ph, FAKE, cci.BF16,
+        assert lib.cci_conv_im2col_algo(FAKE, cci.BF16, 1, 8, 8, 64, KH, KH, sh, sh, ph, ph, FAKE, cci.BF16,
                                    FAKE, 256, 8, 2, None, FAKE, cci.BF16, W, None) == cci.EUNSUPPORTED
 
 
 def test_narrow_algo_requirements():
     # narrow MFMA: bf16, C <= 256, C % 8 == 0, O % 4 == 0; strided / padded / k x k convs refused
     Nw = cci.ALGO_NARROW_MFMA
-    assert lib.cci_spmm(FAKE, cci.BF16, 4, 264, FAKE, cci.BF16, FAKE, 16, 8, 2, None, FAKE,
+    assert lib.cci_spmm_algo(FAKE, cci.BF16, 4, 264, FAKE, cci.BF16, FAKE, 16, 8, 2, None, FAKE,
                         cci.BF16, Nw, None) == cci.EUNSUPPORTED
-    assert lib.cci_spmm(FAKE, cci.BF16, 4, 20, FAKE, cci.BF16, FAKE, 16, 8, 2, None, FAKE,
+    assert lib.cci_spmm_algo(FAKE, cci.BF16, 4, 20, FAKE, cci.BF16, FAKE, 16, 8, 2, None, FAKE,
                         cci.BF16, Nw, None) == cci.EUNSUPPORTED
-    assert lib.cci_spmm(FAKE, cci.BF16, 4, 16, FAKE, cci.BF16, FAKE, 18, 2, 1, None, FAKE,
+    assert lib.cci_spmm_algo(FAKE, cci.BF16, 4, 16, FAKE, cci.BF16, FAKE, 18, 2, 1, None, FAKE,
                         cci.BF16, Nw, None) == cci.EUNSUPPORTED
-    assert lib.cci_spmm(FAKE, cci.F32, 4, 16, FAKE, cci.F32, FAKE, 16, 8, 2, None, FAKE,
+    assert lib.cci_spmm_algo(FAKE, cci.F32, 4, 16, FAKE, cci.F32, FAKE, 16, 8, 2, None, FAKE,
                         cci.F32, Nw, None) == cci.EUNSUPPORTED
     # convs: Cin 3, Cin 4 with an odd KW, and a reduction past 256 are refused
     for Cin, KH, KW in [(3, 3, 3), (4, 7, 7), (40, 3, 3)]:
-        assert lib.cci_conv_im2col(FAKE, cci.BF16, 1, 8, 8, Cin, KH, KW, 1, 1, 1, 1, FAKE, cci.BF16,
+        assert lib.cci_conv_im2col_algo(FAKE, cci.BF16, 1, 8, 8, Cin, KH, KW, 1, 1, 1, 1, FAKE, cci.BF16,
                                    FAKE, 96, 8, 2, None, FAKE, cci.BF16, Nw, None) == cci.EUNSUPPORTED
+
+
+def test_algo_entry_points_match_plain_calls_on_validation():
+    # the pinned-family calls validate exactly like the plain ones
+    assert lib.cci_spmm_algo(FAKE, cci.BF16, 4, 64, FAKE, cci.BF16, FAKE, 12, 8, 2, None, FAKE,
+                             cci.BF16, cci.ALGO_AUTO, None) == cci.EINVAL
+    assert lib.cci_spmm_algo(None, cci.BF16, 0, 64, None, cci.BF16, None, 16, 8, 2, None, None,
+                             cci.BF16, cci.ALGO_WIDE_TILE_MFMA, None) == cci.OK
+    assert lib.cci_conv_im2col_algo(FAKE, cci.BF16, 1, 5, 5, 32, 3, 3, 0, 1, 1, 1, FAKE, cci.BF16,
+                                    FAKE, 16, 8, 2, None, FAKE, cci.BF16, cci.ALGO_AUTO, None) == cci.EINVAL
 
 
 def test_empty_is_a_noop():
     # N == 0: nothing to do, no pointer is needed or touched
     assert lib.cci_spmm(None, cci.BF16, 0, 64, None, cci.BF16, None, 16, 8, 2, None, None,
-                        cci.BF16, 0, None) == cci.OK
+                        cci.BF16, None) == cci.OK
     assert lib.cci_conv_im2col(None, cci.BF16, 0, 5, 5, 32, 3, 3, 1, 1, 1, 1, None, cci.BF16, None,
-                               16, 8, 2, None, None, cci.BF16, 0, None) == cci.OK
+                               16, 8, 2, None, None, cci.BF16, None) == cci.OK
 
 
 def test_conv_geometry_errors():
@@ -122,7 +133,7 @@ def test_conv_geometry_errors():
            (1, 5, 5, 0, 3, 3, 1, 1, 1, 1)]    # Cin 0
     for B, H, W, Cin, KH, KW, sh, sw, ph, pw in bad:
         assert lib.cci_conv_im2col(FAKE, cci.BF16, B, H, W, Cin, KH, KW, sh, sw, ph, pw, FAKE, cci.BF16,
-                                   FAKE, args["O"], args["G"], args["K"], None, FAKE, cci.BF16, 0,
+                                   FAKE, args["O"], args["G"], args["K"], None, FAKE, cci.BF16,
                                    None) == cci.EINVAL
 
 

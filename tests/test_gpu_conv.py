@@ -4,7 +4,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_common import (DEV, epilogue_terms, need_gpu, oracle_pack_vals, rand_epilogue, tol_for,
+from gpu_common import (DEV, Guarded, epilogue_terms, need_gpu, oracle_pack_vals, rand_epilogue, tol_for,
                         x_as_f32)
 from parity import check_close, to_np_f32
 from paper_1910_11971_amd import workloads
@@ -33,9 +33,11 @@ def run_conv_kw(X: torch.Tensor, W: np.ndarray, G, K, KH, KW, stride, pad, y_dty
     if r_t is not None:
         kw["residual"] = r_t.reshape(B, Ho, Wo, O).to(DEV)
     vals, idx = cci.pack(torch.from_numpy(W).to(DEV), G, K, vdt)
+    Yg = Guarded((B, Ho, Wo, O), y_dtype)
     Y = cci.conv_im2col(X.to(DEV), vals, idx, G, KH, KW, (stride, stride), (pad, pad), relu=relu,
-                        out_dtype=y_dtype, algo=algo, **kw)
+                        out_dtype=y_dtype, algo=algo, out=Yg.t, **kw)
     torch.cuda.synchronize()
+    Yg.check(f"conv {algo} {tuple(X.shape)} k{KH}x{KW} s{stride} p{pad} O={O}")
     v_ref, idx_ref, _ = oracle_pack_vals(W, G, K, vdt)
     Wmask = oracle.unpack(v_ref, idx_ref, G).reshape(O, KH, KW, Cin)
     Yref, Yabs = oracle.conv2d_nhwc(x_as_f32(X), Wmask, (stride, stride), (pad, pad), scale=s, bias=b,
@@ -137,25 +139,3 @@ def test_conv_fp32():
     need_gpu()
     X = rand_x((2, 8, 8, 5), torch.float32, 31)
     run_conv(X, rand_w(16, 45, 32), 4, 2, 3, 1, 1, torch.float32, "auto")
-
-
-def sample_pixels(wl, n, seed):
-    rng = np.random.default_rng(seed)
-    Ho, Wo = wl.Ho, wl.Wo
-    corners = []
-    for b in (0, wl.B - 1):
-        for oh in (0, Ho - 1):
-            for ow in (0, Wo - 1):
-                corners.append((b * Ho + oh) * Wo + ow)
-    return np.unique(np.concatenate([corners, rng.integers(0, wl.N, n)]))
-
-
-@pytest.mark.parametrize("algo", ["auto", "sparse_mac"])
-@pytest.mark.parametrize("name", ["conv3x3", "conv1x1_k4", "conv1x1_k2"])
-def test_conv_full_size_sampled(name, algo):
-    """Full-size 3x3 and 1x1 bottleneck convolutions, sampled output pixels."""
-    need_gpu()
-    wl = workloads.WORKLOADS[name]
-    X, W = workloads.draw(wl)
-    run_conv(X, W, wl.G, wl.K, wl.KH, wl.stride, wl.pad, torch.bfloat16, algo,
-             pixels=sample_pixels(wl, 300, 7))

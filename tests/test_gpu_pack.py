@@ -3,7 +3,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_common import DEV, gpu_bits, need_gpu, oracle_pack_vals
+from gpu_common import DEV, Guarded, gpu_bits, need_gpu, oracle_pack_vals
 from paper_1910_11971_amd import workloads
 
 pytestmark = pytest.mark.gpu
@@ -12,8 +12,12 @@ pytestmark = pytest.mark.gpu
 def run_pack(W: np.ndarray, G, K, vdt):
     from paper_1910_11971_amd import cci
     Wt = torch.from_numpy(W).to(DEV)
-    vals, idx = cci.pack(Wt, G, K, vdt)
+    O, C = W.shape
+    vg, ig = Guarded((O // G, K, C), vdt), Guarded((O // G, K, C), torch.uint8)
+    vals, idx = cci.pack(Wt, G, K, vdt, out=(vg.t, ig.t))
     torch.cuda.synchronize()
+    vg.check(f"pack vals O={O} C={C} G={G} K={K}")
+    ig.check(f"pack idx O={O} C={C} G={G} K={K}")
     _, idx_ref, bits_ref = oracle_pack_vals(W, G, K, vdt)
     np.testing.assert_array_equal(idx.cpu().numpy(), idx_ref)
     np.testing.assert_array_equal(gpu_bits(vals), bits_ref)

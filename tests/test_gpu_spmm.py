@@ -4,7 +4,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_common import (DEV, epilogue_terms, need_gpu, oracle_pack_vals, rand_epilogue, tol_for,
+from gpu_common import (DEV, Guarded, epilogue_terms, need_gpu, oracle_pack_vals, rand_epilogue, tol_for,
                         x_as_f32)
 from parity import check_close, to_np_f32
 from paper_1910_11971_amd import workloads
@@ -27,8 +27,10 @@ def run_case(X: torch.Tensor, W: np.ndarray, G, K, y_dtype, algo, *, rows=None, 
         kw["bias"] = torch.from_numpy(b).to(DEV)
     if r_t is not None:
         kw["residual"] = r_t.to(DEV)
-    Y = cci.spmm(Xd, vals, idx, G, relu=relu, out_dtype=y_dtype, algo=algo, **kw)
+    Yg = Guarded((N, O), y_dtype)
+    Y = cci.spmm(Xd, vals, idx, G, relu=relu, out_dtype=y_dtype, algo=algo, out=Yg.t, **kw)
     torch.cuda.synchronize()
+    Yg.check(f"spmm {algo} N={N} C={C} O={O} G={G} K={K}")
     v_ref, idx_ref, _ = oracle_pack_vals(W, G, K, vdt)
     Yref, Yabs = oracle.spmm_rows(x_as_f32(X), v_ref, idx_ref, G, scale=s, bias=b, residual=r,
                                   relu=relu, rows=rows, want_abs=True)
@@ -144,16 +146,13 @@ def test_spmm_fc256_full():
     run_case(X, W, wl.G, wl.K, torch.float32, "auto")
 
 
-def sample_rows(N, n, seed):
-    rng = np.random.default_rng(seed)
-    return np.unique(np.concatenate([[0, 1, N // 2, N - 2, N - 1], rng.integers(0, N, n)]))
-
-
-@pytest.mark.parametrize("algo", ["auto", "sparse_mac", "dense_tile_mfma", "wide_tile_mfma"])
-@pytest.mark.parametrize("K", [1, 2, 4, 8, 16])
-def test_spmm_fc4096_full_size_sampled(K, algo):
-    """FC sweep at full size (4096^3, G=16), sampled rows vs the oracle."""
+@pytest.mark.parametrize("xdt", [torch.bfloat16, torch.float32])
+@pytest.mark.parametrize("N,C,O,G,K", [(200, 96, 128, 16, 4), (64, 256, 256, 32, 7), (256, 40, 64, 16, 16),
+                                       (3, 520, 96, 32, 1)])
+def test_spmm_sparse_mac_small_n_wide_groups(N, C, O, G, K, xdt):
+    """Products with at most 256 rows take the wave-per-(row, group) variant
+    of the vector kernels: G = 16 and 32 (the 64-lane reduction and the
+    lane < G store select), with every epilogue term."""
     need_gpu()
-    wl = workloads.WORKLOADS[f"fc4096_k{K}"]
-    X, W = workloads.draw(wl)
-    run_case(X, W, wl.G, wl.K, torch.bfloat16, algo, rows=sample_rows(wl.N, 48, K))
+    ep = rand_epilogue(O, N, xdt, 17, residual=True, relu=True)
+    run_case(rand_x(N, C, xdt, N + 3), rand_w(O, C, O + 5), G, K, xdt, "sparse_mac", ep=ep)

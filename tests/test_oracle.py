@@ -255,6 +255,30 @@ def test_conv_direct_matches_torch_conv2d(k, stride, pad):
     np.testing.assert_allclose(Y, ref, rtol=1e-12, atol=1e-12)
 
 
+@pytest.mark.parametrize("k,stride,pad", [(3, 1, 1), (3, 2, 1), (1, 1, 0), (7, 2, 3), (2, 1, 0)])
+def test_conv_abs_sum_matches_torch_conv2d_of_magnitudes(k, stride, pad):
+    """Yabs (the per-output sum of |terms| that scales the GPU tolerance) is
+    the convolution of |X| with |W|, zero padding included; it must not move
+    with the epilogue, and a pixel subset must give the same rows."""
+    rng = np.random.default_rng(100 + k * 10 + stride + pad)
+    B, H, W, Cin, O = 2, 9, 11, 5, 8
+    X = rng.standard_normal((B, H, W, Cin)).astype(np.float32)
+    Wt = rng.standard_normal((O, k, k, Cin)).astype(np.float32)
+    Wt[rng.random(Wt.shape) < 0.5] = 0.0  # masked weights contribute nothing
+    sc = (0.5 + rng.random(O)).astype(np.float32)
+    bi = rng.standard_normal(O).astype(np.float32)
+    _, Yabs = oracle.conv2d_nhwc(X, Wt, (stride, stride), (pad, pad), scale=sc, bias=bi, relu=True,
+                                 want_abs=True)
+    ref = torch.nn.functional.conv2d(
+        torch.from_numpy(np.abs(X)).double().permute(0, 3, 1, 2),
+        torch.from_numpy(np.abs(Wt)).double().permute(0, 3, 1, 2), stride=stride, padding=pad)
+    ref = ref.permute(0, 2, 3, 1).reshape(-1, O).numpy()
+    np.testing.assert_allclose(Yabs, ref, rtol=1e-12, atol=1e-12)
+    pix = np.array([0, 3, ref.shape[0] - 1], np.int64)
+    _, Ysub = oracle.conv2d_nhwc(X, Wt, (stride, stride), (pad, pad), pixels=pix, want_abs=True)
+    np.testing.assert_allclose(Ysub, ref[pix], rtol=1e-12, atol=1e-12)
+
+
 @pytest.mark.parametrize("k,stride,pad", [(3, 1, 1), (3, 2, 1), (1, 2, 0)])
 def test_im2col_matches_torch_unfold(k, stride, pad):
     rng = np.random.default_rng(1)

@@ -74,13 +74,19 @@ def _load():
         _f32p, _i64, _i64, _i64, _i64, _i32, _i32, _i32, _f32p]
     lib.oracle_global_avgpool_nhwc.argtypes = [
         _f32p, _i64, _i64, _i64, _i64, _f64p]
+    lib.oracle_bbs_pack.argtypes = [_f32p, _i64, _i64, _i32, _i32, _f32p, _u8p]
+    lib.oracle_bbs_unpack.argtypes = [_f32p, _u8p, _i64, _i64, _i32, _i32, _f32p]
+    lib.oracle_bbs_spmm_rows.argtypes = [
+        _f32p, _i64, _i64, _f32p, _u8p, _i64, _i32, _i32,
+        _f32p, _f32p, _f32p, _i32, _i64p, _i64, _f64p, _f64p]
     lib.oracle_num_threads.restype = ctypes.c_int
     lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
     lib.oracle_set_num_threads.restype = None
     for fn in ("oracle_pack", "oracle_unpack", "oracle_spmm_rows",
                "oracle_dense_rows", "oracle_conv2d_nhwc_rows",
                "oracle_im2col_nhwc", "oracle_maxpool2d_nhwc",
-               "oracle_global_avgpool_nhwc"):
+               "oracle_global_avgpool_nhwc", "oracle_bbs_pack", "oracle_bbs_unpack",
+               "oracle_bbs_spmm_rows"):
         getattr(lib, fn).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -279,3 +285,52 @@ def eq1_pd(G: int, Ps: Fraction) -> Fraction:
         if i > s:
             total += (i - s) * comb(G, i) * q ** i * Ps ** (G - i)
     return total / s
+
+
+# ------------------------------------------------------- balanced sparsity --
+
+def bbs_pack(W: np.ndarray, G: int, K: int):
+    """Balanced-sparsity projection (Sec. 2.4, Sec. 3.3, Fig. 2b): per row,
+    per group of G contiguous inputs, keep the K largest |w| (ties: lower
+    position), ascending.  W fp32 [O, C], C % G == 0.  Returns (vals fp32
+    [O, C/G, K], idx uint8 [O, C/G, K])."""
+    W = _f32(W)
+    O, C = W.shape
+    if G < 1 or C % G:
+        raise ValueError("C must be a multiple of G")
+    vals = np.empty((O, C // G, K), np.float32)
+    idx = np.empty((O, C // G, K), np.uint8)
+    _check(_load().oracle_bbs_pack(_p(W, _f32p), O, C, G, K, _p(vals, _f32p), _p(idx, _u8p)), "bbs_pack")
+    return vals, idx
+
+
+def bbs_unpack(vals: np.ndarray, idx: np.ndarray, G: int) -> np.ndarray:
+    """The dense masked [O, C] matrix of a balanced-sparse packing."""
+    vals = _f32(vals)
+    idx = np.ascontiguousarray(idx, np.uint8)
+    O, ng, K = vals.shape
+    Wd = np.empty((O, ng * G), np.float32)
+    _check(_load().oracle_bbs_unpack(_p(vals, _f32p), _p(idx, _u8p), O, ng * G, G, K, _p(Wd, _f32p)), "bbs_unpack")
+    return Wd
+
+
+def bbs_spmm_rows(X, vals, idx, G, *, scale=None, bias=None, residual=None, relu=False, rows=None,
+                  want_abs=False):
+    """Balanced-sparse product (Sec. 3.3, Fig. 2b) in double precision:
+    Y[n][o] = epilogue(sum_j sum_k vals[o][j][k] * X[n][jG + idx[o][j][k]])."""
+    X = _f32(X)
+    vals = _f32(vals)
+    idx = np.ascontiguousarray(idx, np.uint8)
+    N, C = X.shape
+    O, ng, K = vals.shape
+    if ng * G != C:
+        raise ValueError("packed groups do not match X")
+    r = None if rows is None else np.ascontiguousarray(rows, np.int64)
+    nrows = N if r is None else r.shape[0]
+    Y = np.empty((nrows, O), np.float64)
+    Yabs = np.empty((nrows, O), np.float64) if want_abs else None
+    _check(_load().oracle_bbs_spmm_rows(
+        _p(X, _f32p), N, C, _p(vals, _f32p), _p(idx, _u8p), O, G, K, _p(_f32(scale), _f32p),
+        _p(_f32(bias), _f32p), _p(_f32(residual), _f32p), int(bool(relu)), _p(r, _i64p), nrows,
+        _p(Y, _f64p), _p(Yabs, _f64p)), "bbs_spmm_rows")
+    return (Y, Yabs) if want_abs else Y

@@ -297,6 +297,114 @@ int oracle_im2col_nhwc(const float *X, int64_t B, int64_t H, int64_t W,
 }
 
 /*
+ * Balanced sparsity (paper Sec. 2.4 and Sec. 3.3, Fig. 2b): the comparison
+ * structure of the paper.  Its groups are G contiguous weights of one output
+ * row -- weights of different inputs, instead of CCI's weights of different
+ * output channels at one input -- and each group keeps its K (the paper's s)
+ * largest-magnitude weights; the index of a kept weight names the input
+ * inside its group that the weight multiplies.
+ *
+ * For every row o in [0, O) and group j in [0, C/G) with w_r = W[o][jG+r]:
+ *   rank_r = #{ r' : key_r' > key_r  or  (key_r' == key_r and r' < r) }
+ *   r is kept iff rank_r < K            (same magnitude order and tie rule
+ *                                        as the CCI projection above)
+ * kept r in ascending order: idx[o][j][k] = r, vals[o][j][k] = w_r.
+ * Layout: vals, idx are [O][C/G][K] (a row's groups, then its slots).
+ */
+static int check_bbs_args(int64_t O, int64_t C, int32_t G, int32_t K) {
+  if (G < 1 || G > 256 || K < 1 || K > G) return ORACLE_EINVAL;
+  if (O < 1 || C < 1 || C % G != 0) return ORACLE_EINVAL;
+  return ORACLE_OK;
+}
+
+int oracle_bbs_pack(const float *W, int64_t O, int64_t C, int32_t G, int32_t K,
+                    float *vals, uint8_t *idx) {
+  if (check_bbs_args(O, C, G, K) != ORACLE_OK) return ORACLE_EINVAL;
+  const int64_t ngroups = C / G;
+#pragma omp parallel for schedule(static)
+  for (int64_t o = 0; o < O; ++o) {
+    for (int64_t j = 0; j < ngroups; ++j) {
+      const float *w = W + o * C + j * G;
+      int32_t slot = 0;
+      for (int32_t r = 0; r < G; ++r) {
+        const uint32_t kr = abs_key(w[r]);
+        int32_t rank = 0;
+        for (int32_t q = 0; q < G; ++q) {
+          const uint32_t kq = abs_key(w[q]);
+          if (kq > kr || (kq == kr && q < r)) ++rank;
+        }
+        if (rank < K) {
+          vals[(o * ngroups + j) * K + slot] = w[r];
+          idx[(o * ngroups + j) * K + slot] = (uint8_t)r;
+          ++slot;
+        }
+      }
+    }
+  }
+  return ORACLE_OK;
+}
+
+/* The dense masked matrix W_hat [O][C] a balanced-sparse packing describes:
+ * W_hat[o][jG + idx[o][j][k]] = vals[o][j][k], every other entry 0. */
+int oracle_bbs_unpack(const float *vals, const uint8_t *idx, int64_t O,
+                      int64_t C, int32_t G, int32_t K, float *Wd) {
+  if (check_bbs_args(O, C, G, K) != ORACLE_OK) return ORACLE_EINVAL;
+  for (int64_t i = 0; i < O * C; ++i) Wd[i] = 0.0f;
+  const int64_t ngroups = C / G;
+  for (int64_t o = 0; o < O; ++o)
+    for (int64_t j = 0; j < ngroups; ++j)
+      for (int32_t k = 0; k < K; ++k) {
+        const int32_t r = idx[(o * ngroups + j) * K + k];
+        if (r >= G) return ORACLE_EINVAL;
+        Wd[o * C + j * G + r] = vals[(o * ngroups + j) * K + k];
+      }
+  return ORACLE_OK;
+}
+
+/*
+ * Balanced-sparse product (Sec. 3.3, Fig. 2b): the index of each kept weight
+ * selects the input element inside its group that it multiplies,
+ *   Y[n][o] = sum_j sum_k vals[o][j][k] * X[n][jG + idx[o][j][k]],
+ * in double, j ascending and k ascending inside j (so the terms of an output
+ * arrive in ascending input order, as in Alg. 0 on the unpacked matrix);
+ * then the epilogue.  rows / Yabs / residual as for oracle_spmm_rows.
+ */
+int oracle_bbs_spmm_rows(const float *X, int64_t N, int64_t C,
+                         const float *vals, const uint8_t *idx, int64_t O,
+                         int32_t G, int32_t K, const float *scale,
+                         const float *bias, const float *residual,
+                         int32_t relu, const int64_t *rows, int64_t nrows,
+                         double *Y, double *Yabs) {
+  if (check_bbs_args(O, C, G, K) != ORACLE_OK || N < 0) return ORACLE_EINVAL;
+  if (!rows && nrows != N) return ORACLE_EINVAL;
+  for (int64_t i = 0; i < nrows; ++i) {
+    const int64_t n = rows ? rows[i] : i;
+    if (n < 0 || n >= N) return ORACLE_EINVAL;
+  }
+  const int64_t ngroups = C / G;
+  int bad = 0;
+#pragma omp parallel for schedule(static) reduction(| : bad)
+  for (int64_t i = 0; i < nrows; ++i) {
+    const int64_t n = rows ? rows[i] : i;
+    const float *res_row = residual ? residual + n * O : NULL;
+    for (int64_t o = 0; o < O; ++o) {
+      double acc = 0.0, aabs = 0.0;
+      for (int64_t j = 0; j < ngroups; ++j)
+        for (int32_t k = 0; k < K; ++k) {
+          const int32_t r = idx[(o * ngroups + j) * K + k];
+          if (r >= G) { bad = 1; continue; }
+          const double t = (double)vals[(o * ngroups + j) * K + k] * (double)X[n * C + j * G + r];
+          acc += t;
+          aabs += fabs(t);
+        }
+      Y[i * O + o] = epilogue(acc, o, scale, bias, res_row, relu);
+      if (Yabs) Yabs[i * O + o] = aabs;
+    }
+  }
+  return bad ? ORACLE_EINVAL : ORACLE_OK;
+}
+
+/*
  * Round-to-nearest-even conversion of an fp32 value to bfloat16 (the upper
  * 16 bits of an IEEE binary32), written from the definition: the result is
  * the representable bf16 nearest to x; on an exact tie the one whose last

@@ -180,6 +180,72 @@ cci_status cci_conv_im2col_algo(const void *X, cci_dtype x_t, int64_t B,
 cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C,
                        int64_t cin, int64_t O, int32_t G, int32_t K);
 
+/* ------------------------------------------------------------------------
+ * Balanced sparsity (Sec. 2.4, Sec. 3.3, Fig. 2b): the paper's comparison
+ * structure.  Its groups are G contiguous weights of one output row (weights
+ * of different inputs); each keeps exactly K, and the index of a kept weight
+ * names the input of its group it multiplies.
+ * ------------------------------------------------------------------------ */
+
+/* Byte sizes of the balanced packing of an O x C matrix: vals [O][C/G][K]
+ * of val_t, idx [O][C/G][K] uint8.  CCI_EINVAL unless C % G == 0 and
+ * 1 <= K <= G <= 256. */
+cci_status cci_bbs_packed_sizes(int64_t O, int64_t C, int32_t G, int32_t K,
+                                cci_dtype val_t, size_t *val_bytes,
+                                size_t *idx_bytes);
+
+/* Balanced projection of a dense fp32 W [O][C]: for each row o and group j
+ * (inputs jG .. jG+G-1) keep the K largest |w| (magnitude order and ties as
+ * for cci_pack: lower position wins), in ascending position:
+ *   vals[o][j][k] = W[o][jG + idx[o][j][k]]  (exact, or rounded once to bf16).
+ * Errors as for cci_pack. */
+cci_status cci_bbs_pack(const float *W, int64_t O, int64_t C, int32_t G,
+                        int32_t K, void *vals, cci_dtype val_t, uint8_t *idx,
+                        void *stream);
+
+/* The 2:4 operand of gfx950's sparse matrix cores.  A matrix A [M][R] in
+ * which every aligned run of 4 reduction positions holds at most 2 nonzeros
+ * is stored as 2 bf16 values and 2-bit positions per run, in fragment order:
+ *   a_vals bf16 [R/64][M/16][64][8], a_idx uint16 [R/64][M/16][64]
+ * (lane l of fragment (s, mb): row 16 mb + l % 16, reduction columns
+ * 64 s + 16 (l / 16) .. +15; value e sits at column 4 (e / 2) + bits
+ * 2e..2e+1 of the index word of those).  M % 16 == 0 and R % 64 == 0
+ * (CCI_EUNSUPPORTED otherwise); sizes in bytes M*R and M*R/8. */
+cci_status cci_2of4_sizes(int64_t M, int64_t R, size_t *val_bytes,
+                          size_t *idx_bytes);
+
+/* The 2:4 operand of a balanced packing (bf16 vals, as from cci_bbs_pack) of
+ * an O x C matrix: rows M = O, reduction R = C.  Each run of 4 inputs holds
+ * at most 2 kept weights when G % 4 == 0 and K <= 2; other (G, K) return
+ * CCI_EUNSUPPORTED.  Unused slots hold 0. */
+cci_status cci_bbs_to_2of4(const void *vals, cci_dtype val_t,
+                           const uint8_t *idx, int64_t O, int64_t C, int32_t G,
+                           int32_t K, void *a_vals, uint16_t *a_idx,
+                           void *stream);
+
+/* The 2:4 operand of W_hat^T for a CCI packing of W_hat [O][C] (bf16 vals,
+ * as from cci_pack): rows M = C, reduction R = O.  Along the output channels
+ * a CCI group keeps K of G (Sec. 3.1), so the backward product
+ * dX = dY . W_hat reduces over 2:4-sparse runs when G % 4 == 0 and K <= 2
+ * (else CCI_EUNSUPPORTED). */
+cci_status cci_to_2of4_transposed(const void *vals, cci_dtype val_t,
+                                  const uint8_t *idx, int64_t O, int64_t C,
+                                  int32_t G, int32_t K, void *a_vals,
+                                  uint16_t *a_idx, void *stream);
+
+/* Y[n][m] = epilogue( sum_r A[m][r] * X[n][r] ) on the sparse matrix cores
+ * (v_smfmac_f32_16x16x64_bf16; fp32 accumulation, one rounding of a bf16
+ * Y).  X: device bf16 [N][R]; A: a prepared 2:4 operand [M][R]; Y: device
+ * [N][M] of y_t (BF16 or F32); epilogue as for cci_spmm (vectors of M).
+ * With A from cci_bbs_to_2of4 this is the balanced-sparse forward product;
+ * with A from cci_to_2of4_transposed and X = dY it is dX = dY . W_hat.
+ * X is read as exact products of the stored values: unused slots multiply
+ * their (finite) inputs by 0. */
+cci_status cci_spmm_2of4(const void *X, cci_dtype x_t, int64_t N, int64_t R,
+                         const void *a_vals, const uint16_t *a_idx, int64_t M,
+                         const cci_epilogue *ep, void *Y, cci_dtype y_t,
+                         void *stream);
+
 /* CNN glue for the ResNet-shaped forward (not from the paper).
  * Max pooling, NHWC, window k, stride s, padding p (padding never wins).
  * X, Y: device [B][H][W][C] -> [B][Ho][Wo][C] of dtype t (F32 or BF16). */

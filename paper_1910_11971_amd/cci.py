@@ -52,6 +52,13 @@ _lib.cci_spmm.argtypes = _SPMM + [_vp]
 _lib.cci_spmm_algo.argtypes = _SPMM + [ctypes.c_int, _vp]
 _lib.cci_conv_im2col.argtypes = _CONV + [_vp]
 _lib.cci_conv_im2col_algo.argtypes = _CONV + [ctypes.c_int, _vp]
+_lib.cci_bbs_packed_sizes.argtypes = [_i64, _i64, _i32, _i32, ctypes.c_int, ctypes.POINTER(_sz), ctypes.POINTER(_sz)]
+_lib.cci_bbs_pack.argtypes = [_vp, _i64, _i64, _i32, _i32, _vp, ctypes.c_int, _vp, _vp]
+_lib.cci_2of4_sizes.argtypes = [_i64, _i64, ctypes.POINTER(_sz), ctypes.POINTER(_sz)]
+_lib.cci_bbs_to_2of4.argtypes = [_vp, ctypes.c_int, _vp, _i64, _i64, _i32, _i32, _vp, _vp, _vp]
+_lib.cci_to_2of4_transposed.argtypes = [_vp, ctypes.c_int, _vp, _i64, _i64, _i32, _i32, _vp, _vp, _vp]
+_lib.cci_spmm_2of4.argtypes = [_vp, ctypes.c_int, _i64, _i64, _vp, _vp, _i64, ctypes.POINTER(Epilogue), _vp,
+                               ctypes.c_int, _vp]
 _lib.cci_auto_algo.argtypes = [ctypes.c_int, ctypes.c_int, _i64, _i64, _i64, _i64, _i32, _i32]
 _lib.cci_auto_algo.restype = ctypes.c_int
 _lib.cci_maxpool2d_nhwc.argtypes = [_vp, ctypes.c_int, _i64, _i64, _i64, _i64, _i32, _i32, _i32, _vp, _vp]
@@ -61,7 +68,8 @@ _lib.cci_status_str.restype = ctypes.c_char_p
 _lib.cci_last_error.restype = ctypes.c_char_p
 _lib.cci_version.restype = ctypes.c_int32
 for _fn in ("cci_packed_sizes", "cci_pack", "cci_spmm", "cci_spmm_algo", "cci_conv_im2col",
-            "cci_conv_im2col_algo", "cci_maxpool2d_nhwc", "cci_global_avgpool_nhwc"):
+            "cci_conv_im2col_algo", "cci_maxpool2d_nhwc", "cci_global_avgpool_nhwc", "cci_bbs_packed_sizes",
+            "cci_bbs_pack", "cci_2of4_sizes", "cci_bbs_to_2of4", "cci_to_2of4_transposed", "cci_spmm_2of4"):
     getattr(_lib, _fn).restype = ctypes.c_int
 
 
@@ -240,4 +248,75 @@ def global_avgpool_nhwc(X: torch.Tensor, out_dtype=None) -> torch.Tensor:
     Y = torch.empty((B, C), dtype=out_dtype or X.dtype, device=X.device)
     _check(_lib.cci_global_avgpool_nhwc(_ptr(X), _code(X.dtype), B, H, W, C, _ptr(Y), _code(Y.dtype),
                                         _stream(X)))
+    return Y
+
+
+# ------------------------------------------------------- balanced sparsity --
+
+def bbs_pack(W: torch.Tensor, G: int, K: int, val_dtype=torch.bfloat16, out=None):
+    """cci_bbs_pack: W fp32 [O, C] -> (vals [O, C/G, K], idx uint8 [O, C/G, K])."""
+    _dev(W)
+    if W.dtype != torch.float32 or W.dim() != 2:
+        raise TypeError("W must be a float32 [O, C] tensor")
+    O, C = W.shape
+    if G < 1 or C % G:
+        raise ValueError("C must be a multiple of G")
+    shape = (O, C // G, K)
+    if out is None:
+        vals = torch.empty(shape, dtype=val_dtype, device=W.device)
+        idx = torch.empty(shape, dtype=torch.uint8, device=W.device)
+    else:
+        vals, idx = _out(out[0], shape, val_dtype, W.device), _out(out[1], shape, torch.uint8, W.device)
+    _check(_lib.cci_bbs_pack(_ptr(W), O, C, G, K, _ptr(vals), _code(val_dtype), _ptr(idx), _stream(W)))
+    return vals, idx
+
+
+def _empty_2of4(M, R, device):
+    if M % 16 or R % 64:
+        raise ValueError("a 2:4 operand needs M % 16 == 0 and R % 64 == 0")
+    return (torch.empty((R // 64, M // 16, 64, 8), dtype=torch.bfloat16, device=device),
+            torch.empty((R // 64, M // 16, 64), dtype=torch.int16, device=device))
+
+
+def bbs_to_2of4(vals: torch.Tensor, idx: torch.Tensor, G: int):
+    """cci_bbs_to_2of4: balanced packing [O, C/G, K] -> prepared 2:4 operand
+    (a_vals bf16 [C/64, O/16, 64, 8], a_idx int16 [C/64, O/16, 64] holding
+    the uint16 index words) of the O x C matrix."""
+    _dev(vals), _dev(idx)
+    O, ng, K = vals.shape
+    C = ng * G
+    av, ai = _empty_2of4(O, C, vals.device)
+    _check(_lib.cci_bbs_to_2of4(_ptr(vals), _code(vals.dtype), _ptr(idx), O, C, G, K, _ptr(av), _ptr(ai),
+                                _stream(vals)))
+    return av, ai
+
+
+def to_2of4_transposed(vals: torch.Tensor, idx: torch.Tensor, G: int):
+    """cci_to_2of4_transposed: CCI packing [O/G, K, C] of W_hat [O, C] ->
+    prepared 2:4 operand of W_hat^T (rows C, reduction O)."""
+    _dev(vals), _dev(idx)
+    ng, K, C = vals.shape
+    O = ng * G
+    av, ai = _empty_2of4(C, O, vals.device)
+    _check(_lib.cci_to_2of4_transposed(_ptr(vals), _code(vals.dtype), _ptr(idx), O, C, G, K, _ptr(av), _ptr(ai),
+                                       _stream(vals)))
+    return av, ai
+
+
+def spmm_2of4(X: torch.Tensor, a_vals: torch.Tensor, a_idx: torch.Tensor, *, scale=None, bias=None, residual=None,
+              relu=False, out_dtype=None, out=None) -> torch.Tensor:
+    """cci_spmm_2of4: Y [N, M] = epilogue(X [N, R] . A^T) with A a prepared
+    2:4 operand [M, R] (sparse matrix cores)."""
+    _dev(X), _dev(a_vals), _dev(a_idx)
+    N, R = X.shape
+    ks, mbs, _, _ = a_vals.shape
+    M = mbs * 16
+    if ks * 64 != R or tuple(a_idx.shape) != (ks, mbs, 64) or a_vals.dtype != torch.bfloat16:
+        raise ValueError("2:4 operand does not match X")
+    if a_vals.device != X.device or a_idx.device != X.device:
+        raise ValueError("X and the operand must be on one device")
+    Y = _out(out, (N, M), out_dtype or X.dtype, X.device)
+    ep = _epilogue(scale, bias, residual, relu, M, Y.shape, Y.dtype, X.device)
+    _check(_lib.cci_spmm_2of4(_ptr(X), _code(X.dtype), N, R, _ptr(a_vals), _ptr(a_idx), M, ctypes.byref(ep), _ptr(Y),
+                              _code(Y.dtype), _stream(X)))
     return Y

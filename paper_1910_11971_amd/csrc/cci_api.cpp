@@ -109,6 +109,45 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
   return ok();
 }
 
+// ---------------------------------------------------------------------------
+// Balanced sparsity and the 2:4 sparse matrix-core product.
+
+cci_status check_bbs_groups(int64_t O, int64_t C, int32_t G, int32_t K) {
+  if (G < 1 || G > 256) return fail(CCI_EINVAL, "G=%d outside [1, 256]", G);
+  if (K < 1 || K > G) return fail(CCI_EINVAL, "K=%d outside [1, G=%d]", K, G);
+  if (O < 1) return fail(CCI_EINVAL, "O=%lld < 1", (long long)O);
+  if (C < 1 || C % G != 0) return fail(CCI_EINVAL, "C=%lld is not a positive multiple of G=%d", (long long)C, G);
+  if (O > (int64_t(1) << 31) || C > (int64_t(1) << 31) || O * C > (int64_t(1) << 40))
+    return fail(CCI_EINVAL, "O*C too large");
+  return CCI_OK;
+}
+
+cci_status check_2of4(int64_t M, int64_t R) {
+  if (M < 16 || M % 16 != 0) return fail(CCI_EUNSUPPORTED, "2:4 operand rows M=%lld must be a positive multiple of 16", (long long)M);
+  if (R < 64 || R % 64 != 0)
+    return fail(CCI_EUNSUPPORTED, "2:4 operand reduction length %lld must be a positive multiple of 64", (long long)R);
+  if (M * R >= (int64_t(1) << 31)) return fail(CCI_EINVAL, "2:4 operand too large");
+  return CCI_OK;
+}
+
+cci_status to_2of4(bool from_cci, const void* vals, cci_dtype val_t, const uint8_t* idx, int64_t O, int64_t C,
+                   int32_t G, int32_t K, void* a_vals, uint16_t* a_idx, void* stream) {
+  if (cci_status s = from_cci ? check_groups(O, C, G, K) : check_bbs_groups(O, C, G, K)) return s;
+  if (!dtype_ok(val_t)) return fail(CCI_EINVAL, "unknown dtype code");
+  if (val_t != CCI_BF16) return fail(CCI_EUNSUPPORTED, "the 2:4 operand holds bf16 values");
+  if (G % 4 != 0 || K > 2)
+    return fail(CCI_EUNSUPPORTED,
+                "a 2:4 operand needs at most 2 kept weights in every aligned run of 4: G %% 4 == 0 and K <= 2 "
+                "(G=%d, K=%d)", G, K);
+  if (cci_status s = from_cci ? check_2of4(C, O) : check_2of4(O, C)) return s;
+  if (!vals || !idx || !a_vals || !a_idx) return fail(CCI_EINVAL, "null pointer");
+  if (!aligned16(vals) || !aligned16(idx) || !aligned16(a_vals) || !aligned16(a_idx))
+    return fail(CCI_EALIGN, "pointer not 16-byte aligned");
+  hipError_t e = cci::launch_to_2of4(from_cci, vals, idx, O, C, G, K, a_vals, a_idx, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(CCI_EHIP, "2:4 conversion launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
 }  // namespace
 
 extern "C" {
@@ -268,6 +307,69 @@ cci_status cci_conv_im2col(const void* X, cci_dtype x_t, int64_t B, int64_t H, i
                            const cci_epilogue* ep, void* Y, cci_dtype y_t, void* stream) {
   return cci_conv_im2col_algo(X, x_t, B, H, W, Cin, KH, KW, stride_h, stride_w, pad_h, pad_w, vals,
                               val_t, idx, O, G, K, ep, Y, y_t, CCI_ALGO_AUTO, stream);
+}
+
+cci_status cci_bbs_packed_sizes(int64_t O, int64_t C, int32_t G, int32_t K, cci_dtype val_t,
+                                size_t* val_bytes, size_t* idx_bytes) {
+  if (cci_status s = check_bbs_groups(O, C, G, K)) return s;
+  if (!dtype_ok(val_t)) return fail(CCI_EINVAL, "unknown dtype code");
+  if (!val_bytes || !idx_bytes) return fail(CCI_EINVAL, "null output pointer");
+  const size_t n = static_cast<size_t>(O) * static_cast<size_t>(C / G) * static_cast<size_t>(K);
+  *val_bytes = n * dsize(val_t);
+  *idx_bytes = n;
+  return ok();
+}
+
+cci_status cci_bbs_pack(const float* W, int64_t O, int64_t C, int32_t G, int32_t K, void* vals,
+                        cci_dtype val_t, uint8_t* idx, void* stream) {
+  if (cci_status s = check_bbs_groups(O, C, G, K)) return s;
+  if (!dtype_ok(val_t)) return fail(CCI_EINVAL, "unknown dtype code");
+  if (!W || !vals || !idx) return fail(CCI_EINVAL, "null pointer");
+  if (!aligned16(W) || !aligned16(vals) || !aligned16(idx)) return fail(CCI_EALIGN, "pointer not 16-byte aligned");
+  hipError_t e = cci::launch_bbs_pack(W, O, C, G, K, vals, to_dt(val_t), idx, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(CCI_EHIP, "bbs pack launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+cci_status cci_2of4_sizes(int64_t M, int64_t R, size_t* val_bytes, size_t* idx_bytes) {
+  if (cci_status s = check_2of4(M, R)) return s;
+  if (!val_bytes || !idx_bytes) return fail(CCI_EINVAL, "null output pointer");
+  *val_bytes = static_cast<size_t>(M) * static_cast<size_t>(R);      // M x R/2 bf16
+  *idx_bytes = static_cast<size_t>(M) * static_cast<size_t>(R) / 8;  // M x R/16 uint16
+  return ok();
+}
+
+cci_status cci_bbs_to_2of4(const void* vals, cci_dtype val_t, const uint8_t* idx, int64_t O, int64_t C,
+                           int32_t G, int32_t K, void* a_vals, uint16_t* a_idx, void* stream) {
+  return to_2of4(false, vals, val_t, idx, O, C, G, K, a_vals, a_idx, stream);
+}
+
+cci_status cci_to_2of4_transposed(const void* vals, cci_dtype val_t, const uint8_t* idx, int64_t O, int64_t C,
+                                  int32_t G, int32_t K, void* a_vals, uint16_t* a_idx, void* stream) {
+  return to_2of4(true, vals, val_t, idx, O, C, G, K, a_vals, a_idx, stream);
+}
+
+cci_status cci_spmm_2of4(const void* X, cci_dtype x_t, int64_t N, int64_t R, const void* a_vals,
+                         const uint16_t* a_idx, int64_t M, const cci_epilogue* ep, void* Y, cci_dtype y_t,
+                         void* stream) {
+  if (!dtype_ok(x_t) || !dtype_ok(y_t)) return fail(CCI_EINVAL, "unknown dtype code");
+  if (x_t != CCI_BF16) return fail(CCI_EUNSUPPORTED, "the 2:4 product takes bf16 X");
+  if (N < 0) return fail(CCI_EINVAL, "N=%lld < 0", (long long)N);
+  if (cci_status s = check_2of4(M, R)) return s;
+  if (!cci::spmm_2of4_fits(N, R, M, to_dt(y_t))) return fail(CCI_EINVAL, "product too large");
+  const float* scale = ep ? ep->scale : nullptr;
+  const float* bias = ep ? ep->bias : nullptr;
+  const void* residual = ep ? ep->residual : nullptr;
+  if ((scale && !aligned16(scale)) || (bias && !aligned16(bias)) || (residual && !aligned16(residual)))
+    return fail(CCI_EALIGN, "epilogue pointer not 16-byte aligned");
+  if (N == 0) return ok();
+  if (!X || !a_vals || !a_idx || !Y) return fail(CCI_EINVAL, "null pointer");
+  if (!aligned16(X) || !aligned16(a_vals) || !aligned16(a_idx) || !aligned16(Y))
+    return fail(CCI_EALIGN, "pointer not 16-byte aligned");
+  hipError_t e = cci::launch_spmm_2of4(X, N, R, a_vals, a_idx, M, scale, bias, residual, ep ? ep->relu : 0, Y,
+                                       to_dt(y_t), static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(CCI_EHIP, "2:4 product launch failed: %s", hipGetErrorString(e));
+  return ok();
 }
 
 cci_status cci_maxpool2d_nhwc(const void* X, cci_dtype t, int64_t B, int64_t H, int64_t W,

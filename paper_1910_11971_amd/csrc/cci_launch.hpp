@@ -81,6 +81,21 @@ hipError_t launch_wide_tile(const ProductArgs& a, hipStream_t s);
 bool narrow_supports(const ProductArgs& a);
 hipError_t launch_narrow(const ProductArgs& a, hipStream_t s);
 
+// Balanced sparsity (groups of G inputs in one output row) and the 2:4
+// sparse matrix-core product.
+hipError_t launch_bbs_pack(const float* W, int64_t O, int64_t C, int32_t G, int32_t K, void* vals, DType val_t,
+                           uint8_t* idx, hipStream_t s);
+// Prepared 2:4 operand from a balanced packing (rows O, reduction C) or, with
+// from_cci, from a CCI packing of W_hat [O][C] as the operand of W_hat^T
+// (rows C, reduction O).  bf16 values; K <= 2, G % 4 == 0, reduction % 64 == 0,
+// rows % 16 == 0.
+hipError_t launch_to_2of4(bool from_cci, const void* vals, const uint8_t* idx, int64_t O, int64_t C, int32_t G,
+                          int32_t K, void* av, uint16_t* ai, hipStream_t s);
+bool spmm_2of4_fits(int64_t N, int64_t C, int64_t M, DType y_t);
+hipError_t launch_spmm_2of4(const void* X, int64_t N, int64_t C, const void* av, const uint16_t* ai, int64_t M,
+                            const float* scale, const float* bias, const void* residual, int32_t relu, void* Y,
+                            DType y_t, hipStream_t s);
+
 hipError_t launch_maxpool(const void* X, DType t, int64_t B, int64_t H, int64_t W, int64_t C,
                           int32_t k, int32_t st, int32_t p, void* Y, hipStream_t s);
 hipError_t launch_avgpool(const void* X, DType x_t, int64_t B, int64_t H, int64_t W, int64_t C,

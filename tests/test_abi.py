@@ -171,3 +171,28 @@ def test_launch_without_device_reports_hip_error():
     st = lib.cci_pack(FAKE, 16, 8, 8, 2, FAKE, cci.F32, FAKE, None)
     assert st == cci.EHIP
     assert lib.cci_last_error()
+
+
+def test_bbs_and_2of4_validation():
+    vb, ib = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    assert lib.cci_bbs_packed_sizes(8, 64, 4, 2, cci.BF16, ctypes.byref(vb), ctypes.byref(ib)) == cci.OK
+    assert (vb.value, ib.value) == (8 * 16 * 2 * 2, 8 * 16 * 2)
+    # balanced groups run along C: C % G != 0 is invalid (O need not divide)
+    assert lib.cci_bbs_packed_sizes(7, 62, 4, 2, cci.BF16, ctypes.byref(vb), ctypes.byref(ib)) == cci.EINVAL
+    assert lib.cci_bbs_pack(FAKE, 7, 62, 4, 2, FAKE, cci.BF16, FAKE, None) == cci.EINVAL
+    assert lib.cci_bbs_pack(FAKE_MIS, 7, 64, 4, 2, FAKE, cci.BF16, FAKE, None) == cci.EALIGN
+    assert lib.cci_2of4_sizes(32, 128, ctypes.byref(vb), ctypes.byref(ib)) == cci.OK
+    assert (vb.value, ib.value) == (32 * 128, 32 * 128 // 8)
+    assert lib.cci_2of4_sizes(24, 128, ctypes.byref(vb), ctypes.byref(ib)) == cci.EUNSUPPORTED   # M % 16
+    assert lib.cci_2of4_sizes(32, 96, ctypes.byref(vb), ctypes.byref(ib)) == cci.EUNSUPPORTED    # R % 64
+    # more than 2 kept weights per run of 4, fp32 values, G not a multiple of 4
+    assert lib.cci_bbs_to_2of4(FAKE, cci.BF16, FAKE, 32, 128, 8, 3, FAKE, FAKE, None) == cci.EUNSUPPORTED
+    assert lib.cci_bbs_to_2of4(FAKE, cci.F32, FAKE, 32, 128, 4, 2, FAKE, FAKE, None) == cci.EUNSUPPORTED
+    assert lib.cci_bbs_to_2of4(FAKE, cci.BF16, FAKE, 32, 120, 6, 1, FAKE, FAKE, None) == cci.EUNSUPPORTED
+    assert lib.cci_to_2of4_transposed(FAKE, cci.BF16, FAKE, 128, 32, 16, 4, FAKE, FAKE, None) == cci.EUNSUPPORTED
+    assert lib.cci_to_2of4_transposed(FAKE, cci.BF16, FAKE, 130, 32, 16, 2, FAKE, FAKE, None) == cci.EINVAL
+    assert lib.cci_spmm_2of4(FAKE, cci.F32, 4, 64, FAKE, FAKE, 16, None, FAKE, cci.BF16, None) == cci.EUNSUPPORTED
+    assert lib.cci_spmm_2of4(FAKE, cci.BF16, 4, 64, FAKE, FAKE, 20, None, FAKE, cci.BF16, None) == cci.EUNSUPPORTED
+    assert lib.cci_spmm_2of4(FAKE, cci.BF16, -1, 64, FAKE, FAKE, 16, None, FAKE, cci.BF16, None) == cci.EINVAL
+    assert lib.cci_spmm_2of4(None, cci.BF16, 0, 64, None, None, 16, None, None, cci.BF16, None) == cci.OK
+    assert lib.cci_spmm_2of4(FAKE, cci.BF16, 4, 64, FAKE_MIS, FAKE, 16, None, FAKE, cci.BF16, None) == cci.EALIGN

@@ -79,6 +79,10 @@ def _load():
     lib.oracle_bbs_spmm_rows.argtypes = [
         _f32p, _i64, _i64, _f32p, _u8p, _i64, _i32, _i32,
         _f32p, _f32p, _f32p, _i32, _i64p, _i64, _f64p, _f64p]
+    lib.oracle_td_schedule.argtypes = [_i64, _i64, _i32, _i32, ctypes.POINTER(_i32), ctypes.POINTER(ctypes.c_double)]
+    lib.oracle_td_mask.argtypes = [_f32p, _i64, _i64, _i32, _i32, ctypes.POINTER(ctypes.c_uint32), ctypes.c_double,
+                                   _f32p, _u8p]
+    lib.oracle_grad_packed.argtypes = [_f32p, _f32p, _i64, _i64, _u8p, _i64, _i32, _i32, _f64p]
     lib.oracle_num_threads.restype = ctypes.c_int
     lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
     lib.oracle_set_num_threads.restype = None
@@ -86,7 +90,7 @@ def _load():
                "oracle_dense_rows", "oracle_conv2d_nhwc_rows",
                "oracle_im2col_nhwc", "oracle_maxpool2d_nhwc",
                "oracle_global_avgpool_nhwc", "oracle_bbs_pack", "oracle_bbs_unpack",
-               "oracle_bbs_spmm_rows"):
+               "oracle_bbs_spmm_rows", "oracle_td_schedule", "oracle_td_mask", "oracle_grad_packed"):
         getattr(lib, fn).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -334,3 +338,43 @@ def bbs_spmm_rows(X, vals, idx, G, *, scale=None, bias=None, residual=None, relu
         _p(_f32(bias), _f32p), _p(_f32(residual), _f32p), int(bool(relu)), _p(r, _i64p), nrows,
         _p(Y, _f64p), _p(Yabs, _f64p)), "bbs_spmm_rows")
     return (Y, Yabs) if want_abs else Y
+
+
+# ------------------------------------------------ improved targeted dropout --
+
+def td_schedule(step: int, total: int, G: int, K: int):
+    """(n_target candidates per group, candidate dropout rate) at `step` of
+    `total` (Sec. 5.1, Sec. 6)."""
+    n = _i32()
+    p = ctypes.c_double()
+    _check(_load().oracle_td_schedule(step, total, G, K, ctypes.byref(n), ctypes.byref(p)), "td_schedule")
+    return n.value, p.value
+
+
+def td_mask(W: np.ndarray, G: int, n_target: int, bits: np.ndarray, drop_rate: float):
+    """Candidate dropout of one step: (W_eff fp32 [O, C], keep uint8 [O, C])."""
+    W = _f32(W)
+    O, C = W.shape
+    bits = np.ascontiguousarray(bits, np.uint32)
+    if bits.shape != (O, C):
+        raise ValueError("bits must be uint32 [O, C]")
+    We = np.empty((O, C), np.float32)
+    keep = np.empty((O, C), np.uint8)
+    _check(_load().oracle_td_mask(_p(W, _f32p), O, C, G, n_target, bits.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)),
+                                  float(drop_rate), _p(We, _f32p), _p(keep, _u8p)), "td_mask")
+    return We, keep
+
+
+def grad_packed(dY, X, idx, G):
+    """dL/dvals [O/G, K, C] of Y = X W_hat^T for dY [N, O], X [N, C] (double)."""
+    dY = _f32(dY)
+    X = _f32(X)
+    idx = np.ascontiguousarray(idx, np.uint8)
+    N, O = dY.shape
+    ng, K, C = idx.shape
+    if X.shape != (N, C) or ng * G != O:
+        raise ValueError("shape mismatch")
+    out = np.empty((ng, K, C), np.float64)
+    _check(_load().oracle_grad_packed(_p(dY, _f32p), _p(X, _f32p), N, C, _p(idx, _u8p), O, G, K, _p(out, _f64p)),
+           "grad_packed")
+    return out

@@ -405,6 +405,93 @@ int oracle_bbs_spmm_rows(const float *X, int64_t N, int64_t C,
 }
 
 /*
+ * Improved targeted dropout (paper Sec. 5.1, schedule of Sec. 6).
+ *
+ * Schedule.  Over a run of T steps, with f = step / T: during the first half
+ * the targeted rate (the share of each group's weights that are pruning
+ * candidates) ramps from 0 to its target 1 - K/G while candidates are
+ * dropped with probability 1/2; during the second half the targeted rate
+ * stays at its target and the dropout rate ramps from 1/2 to 1 (reading:
+ * both ramps linear in f).  Per group of G that is
+ *   n_target = floor((G - K) * min(1, 2 f) + 1/2)   candidates,
+ *   drop_rate = max(1/2, f).
+ * At f = 1 every candidate is dropped: the weights seen by the forward are
+ * exactly the CCI projection (Sec. 5.1's magnitude policy with the group
+ * constraint of Sec. 3.1).
+ */
+int oracle_td_schedule(int64_t step, int64_t total, int32_t G, int32_t K,
+                       int32_t *n_target, double *drop_rate) {
+  if (total < 1 || step < 0 || step > total || G < 1 || K < 1 || K > G) return ORACLE_EINVAL;
+  const double f = (double)step / (double)total;
+  const double ramp = 2.0 * f < 1.0 ? 2.0 * f : 1.0;
+  *n_target = (int32_t)floor((double)(G - K) * ramp + 0.5);
+  *drop_rate = f > 0.5 ? f : 0.5;
+  return ORACLE_OK;
+}
+
+/*
+ * Candidate dropout of one step.  For every CCI group (G contiguous output
+ * channels at column c) the n_target weights of lowest magnitude are the
+ * candidates: with rank_r counted as in oracle_pack (larger |w| first, ties
+ * to the lower row), r is a candidate iff rank_r >= G - n_target.  A
+ * candidate is dropped iff its random word bits[o][c] (uniform 32-bit, drawn
+ * by the caller) is below floor(drop_rate * 2^32).  Outputs: W_eff [O][C],
+ * the weight or 0 where dropped; keep [O][C], 0 where dropped else 1.
+ */
+int oracle_td_mask(const float *W, int64_t O, int64_t C, int32_t G,
+                   int32_t n_target, const uint32_t *bits, double drop_rate,
+                   float *W_eff, uint8_t *keep) {
+  if (O < 1 || C < 1 || G < 1 || G > 256 || O % G != 0 || n_target < 0 ||
+      n_target > G || !(drop_rate >= 0.0 && drop_rate <= 1.0))
+    return ORACLE_EINVAL;
+  const uint64_t thr = (uint64_t)floor(drop_rate * 4294967296.0);
+  const int64_t ngroups = O / G;
+#pragma omp parallel for schedule(static)
+  for (int64_t g = 0; g < ngroups; ++g)
+    for (int64_t c = 0; c < C; ++c)
+      for (int32_t r = 0; r < G; ++r) {
+        const int64_t o = g * G + r;
+        const uint32_t kr = abs_key(W[o * C + c]);
+        int32_t rank = 0;
+        for (int32_t q = 0; q < G; ++q) {
+          const uint32_t kq = abs_key(W[(g * G + q) * C + c]);
+          if (kq > kr || (kq == kr && q < r)) ++rank;
+        }
+        const int candidate = rank >= G - n_target;
+        const int dropped = candidate && (uint64_t)bits[o * C + c] < thr;
+        W_eff[o * C + c] = dropped ? 0.0f : W[o * C + c];
+        keep[o * C + c] = (uint8_t)(dropped ? 0 : 1);
+      }
+  return ORACLE_OK;
+}
+
+/*
+ * Gradient of the packed values of a CCI layer Y = X W_hat^T (Alg. 1's
+ * product), given dY = dL/dY:  dL/dvals[g][k][c] = sum_n dY[n][gG + idx[g][k][c]]
+ * * X[n][c], in double, n ascending.  (Each kept value multiplies X[.][c]
+ * into output row gG + idx, so its derivative gathers that row of dY.)
+ */
+int oracle_grad_packed(const float *dY, const float *X, int64_t N, int64_t C,
+                       const uint8_t *idx, int64_t O, int32_t G, int32_t K,
+                       double *dvals) {
+  if (check_group_args(O, C, G, K) != ORACLE_OK || N < 0) return ORACLE_EINVAL;
+  const int64_t ngroups = O / G;
+  int bad = 0;
+#pragma omp parallel for schedule(static) reduction(| : bad)
+  for (int64_t g = 0; g < ngroups; ++g)
+    for (int32_t k = 0; k < K; ++k)
+      for (int64_t c = 0; c < C; ++c) {
+        const int32_t r = idx[(g * K + k) * C + c];
+        if (r >= G) { bad = 1; continue; }
+        double acc = 0.0;
+        for (int64_t n = 0; n < N; ++n)
+          acc += (double)dY[n * O + g * G + r] * (double)X[n * C + c];
+        dvals[(g * K + k) * C + c] = acc;
+      }
+  return bad ? ORACLE_EINVAL : ORACLE_OK;
+}
+
+/*
  * Round-to-nearest-even conversion of an fp32 value to bfloat16 (the upper
  * 16 bits of an IEEE binary32), written from the definition: the result is
  * the representable bf16 nearest to x; on an exact tie the one whose last

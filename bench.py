@@ -63,6 +63,7 @@ def parse():
                    help="skip the per-configuration oracle timings (1 core and all cores) of the smaller configs")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-dense", action="store_true")
+    p.add_argument("--no-bbs", action="store_true", help="fc4096: skip the balanced-sparsity (2:4) comparison")
     p.add_argument("--graph", action="store_true",
                    help="replay the timed steps from HIP graphs of 8 steps instead of launching every kernel "
                         "from Python")
@@ -435,6 +436,64 @@ def workloads_draw(wl):
     return workloads.draw(wl)
 
 
+def bbs_compare(Xs, Ys, W, ncopy, stream, dense, per_k):
+    """The 4096^3 FC with balanced groups (G inputs of one row, K kept) on the
+    2:4 sparse matrix cores, next to the CCI product of the same (G, K), and
+    the CCI layer's backward product dX = dY . W_hat through the 2:4 operand
+    of W_hat^T.  Effective flop 2 * N * nnz; the sparse matrix cores execute
+    half of the dense product (2 * N * M * R / 2) at twice the dense rate."""
+    import torch
+    from paper_1910_11971_amd import cci
+    N, C = Xs[0].shape
+    O = W.shape[0]
+    out = {}
+    x_bytes = N * C * 2
+    y_bytes = N * O * 2
+    for G, K in ((4, 2), (16, 1), (16, 2)):
+        vals, idx = cci.bbs_pack(W, G, K)
+        av, ai = cci.bbs_to_2of4(vals, idx, G)
+        t_pack = _graph_time(lambda i: cci.bbs_pack(W, G, K, out=(vals, idx)), 8, 8, stream)
+        t_prep = _graph_time(lambda i: cci.bbs_to_2of4(vals, idx, G), 4, 4, stream)
+        t = _graph_time(lambda i: cci.spmm_2of4(Xs[i % ncopy], av, ai, out=Ys[i % ncopy]), ncopy,
+                        max(2, 90 // ncopy), stream)
+        nnz = O * C * K // G
+        flop = 2.0 * N * nnz
+        alg_bytes = x_bytes + av.numel() * 2 + ai.numel() * 2 + y_bytes   # X, the 2:4 operand, Y
+        r = own_roof(flop, alg_bytes, t)
+        r["smfmac_util"] = round(2.0 * N * O * C / 2 / (t * 1e-3) / 1e12 / (2 * PEAK["mfma_bf16_TFLOPs"]), 4)
+        e = {"product_us": round(t * 1e3, 3), "bbs_pack_us": round(t_pack * 1e3, 3),
+             "to_2of4_us": round(t_prep * 1e3, 3), "eff_TFLOPs": round(flop / (t * 1e-3) / 1e12, 2),
+             "roofline": r}
+        if dense:
+            e["speedup_vs_dense_gemm"] = round(dense["gemm_ms"] / t, 3)
+        # the CCI product of the same (G, K)
+        if G == 16 and K in per_k:
+            t_cci = per_k[K]["t_prod"]
+        else:
+            cv, ci = cci.pack(W, G, K, torch.bfloat16)
+            t_cci = _graph_time(lambda i: cci.spmm(Xs[i % ncopy], cv, ci, G, out=Ys[i % ncopy]), ncopy,
+                                max(2, 90 // ncopy), stream)
+        e["cci_product_us"] = round(t_cci * 1e3, 3)
+        e["bbs_speedup_vs_cci"] = round(t_cci / t, 3)
+        # CCI backward: dX = dY . W_hat (dY shaped like Y: [N, O]) through the 2:4 operand of W_hat^T
+        if O % 64 == 0:
+            cv, ci = cci.pack(W, G, K, torch.bfloat16)
+            tv, ti = cci.to_2of4_transposed(cv, ci, G)
+            dX = [torch.empty((N, C), dtype=torch.bfloat16, device=W.device) for _ in range(2)]
+            t_bwd = _graph_time(lambda i: cci.spmm_2of4(Xs[i % ncopy], tv, ti, out=dX[i % 2]), ncopy,
+                                max(2, 90 // ncopy), stream)
+            e["cci_backward_dX_us"] = round(t_bwd * 1e3, 3)
+            if dense:
+                e["cci_backward_speedup_vs_dense_gemm"] = round(dense["gemm_ms"] / t_bwd, 3)
+            del tv, ti, dX
+        out[f"G{G}_K{K}"] = e
+        del vals, idx, av, ai
+    out["note"] = ("balanced groups: G inputs of one output row keep K (Sec. 2.4, 3.3); run as a 2:4 operand "
+                   "(2 values + 2-bit positions per 4 inputs) on v_smfmac_f32_16x16x64_bf16; cci_backward_dX: "
+                   "dX = dY . W_hat of the CCI layer with the same (G, K), dY = the rotated X")
+    return out
+
+
 def main_fc_sweep(args):
     """The 4096^3 FC layer, G = 16: the timed steps at K = args.k, and every K
     of the sweep measured kernel by kernel in the same process."""
@@ -489,6 +548,9 @@ def main_fc_sweep(args):
         dense = {"gemm_ms": round(t_gemm, 5), "timing": how,
                  "note": "torch.matmul bf16 (hipBLASLt, fp32 accumulate, bf16 out) of the dense weights, "
                          "X rotated like the CCI kernel"}
+
+    # ---- balanced sparsity on the 2:4 sparse matrix cores, same shape -------------
+    bbs = None if args.no_bbs else bbs_compare(Xs, Ys, W, ncopy, stream, dense, per_k)
 
     # ---- timed region: whole steps (pack + product) at the declared K ------------
     sel = per_k[args.k]
@@ -565,6 +627,7 @@ def main_fc_sweep(args):
                                "event-timed"},
         "roofline": roof,
         "sweep_k": sweep_k,
+        "bbs_2of4": bbs,
         "cpu_baseline": cpu,
         "dense_bf16": dense,
         "speedup_vs_dense_gemm": None if dense is None else round(dense["gemm_ms"] / sel["t_prod"], 3),

@@ -246,6 +246,47 @@ cci_status cci_spmm_2of4(const void *X, cci_dtype x_t, int64_t N, int64_t R,
                          const cci_epilogue *ep, void *Y, cci_dtype y_t,
                          void *stream);
 
+/* ------------------------------------------------------------------------
+ * Improved targeted dropout (Sec. 5.1; schedule of Sec. 6): training a CCI
+ * layer from a dense W.  Each step drops some of the "candidates" -- the
+ * n_target lowest-|w| weights of every CCI group -- with probability
+ * drop_rate; the forward and backward use the result W_eff.  Over the run the
+ * candidate count ramps up, then the dropout rate ramps to 1, where W_eff is
+ * exactly the CCI projection (cci_pack).  Once the mask is fixed the layer's
+ * backward products are dX = dY . W_hat (cci_to_2of4_transposed +
+ * cci_spmm_2of4) and the gradient of the packed values (cci_grad_packed).
+ * ------------------------------------------------------------------------ */
+
+/* The schedule at `step` of `total` (0 <= step <= total), f = step/total:
+ *   *n_target  = floor((G - K) * min(1, 2 f) + 1/2)   candidates per group,
+ *   *drop_rate = max(1/2, f).
+ * (The first half ramps the candidates at dropout 1/2, the second ramps the
+ * dropout from 1/2 to 1; both ramps linear.)  Host-only. */
+cci_status cci_td_schedule(int64_t step, int64_t total, int32_t G, int32_t K,
+                           int32_t *n_target, double *drop_rate);
+
+/* Candidate dropout of one step.  W: device fp32 [O][C] (O % G == 0).  In
+ * each CCI group (rows gG .. gG+G-1 at column c) the weights of rank
+ * >= G - n_target by |w| (larger first, ties to the lower row, as in
+ * cci_pack) are candidates; a candidate is dropped iff its random word
+ * bits[o][c] (device uint32 [O][C], uniform, drawn by the caller) is below
+ * floor(drop_rate * 2^32).  Writes W_eff [O][C] of w_t (the weight, rounded
+ * once for bf16, or 0 if dropped) and keep [O][C] uint8 (0 if dropped, else
+ * 1).  0 <= n_target <= G, 0 <= drop_rate <= 1. */
+cci_status cci_td_mask(const float *W, int64_t O, int64_t C, int32_t G,
+                       int32_t n_target, const uint32_t *bits,
+                       double drop_rate, void *W_eff, cci_dtype w_t,
+                       uint8_t *keep, void *stream);
+
+/* Gradient of the packed values of Y = X . W_hat^T (Alg. 1's product):
+ *   dvals[g][k][c] = sum_n dY[n][gG + idx[g][k][c]] * X[n][c],
+ * fp32 accumulation in n order.  dY: device [N][O], X: device [N][C], both
+ * of dtype t (F32 or BF16); idx as from cci_pack; dvals: device fp32
+ * [O/G][K][C].  Only kept weights are computed (N * nnz multiply-adds). */
+cci_status cci_grad_packed(const void *dY, const void *X, cci_dtype t,
+                           int64_t N, int64_t C, const uint8_t *idx, int64_t O,
+                           int32_t G, int32_t K, float *dvals, void *stream);
+
 /* CNN glue for the ResNet-shaped forward (not from the paper).
  * Max pooling, NHWC, window k, stride s, padding p (padding never wins).
  * X, Y: device [B][H][W][C] -> [B][Ho][Wo][C] of dtype t (F32 or BF16). */

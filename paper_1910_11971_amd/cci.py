@@ -59,6 +59,9 @@ _lib.cci_bbs_to_2of4.argtypes = [_vp, ctypes.c_int, _vp, _i64, _i64, _i32, _i32,
 _lib.cci_to_2of4_transposed.argtypes = [_vp, ctypes.c_int, _vp, _i64, _i64, _i32, _i32, _vp, _vp, _vp]
 _lib.cci_spmm_2of4.argtypes = [_vp, ctypes.c_int, _i64, _i64, _vp, _vp, _i64, ctypes.POINTER(Epilogue), _vp,
                                ctypes.c_int, _vp]
+_lib.cci_td_schedule.argtypes = [_i64, _i64, _i32, _i32, ctypes.POINTER(_i32), ctypes.POINTER(ctypes.c_double)]
+_lib.cci_td_mask.argtypes = [_vp, _i64, _i64, _i32, _i32, _vp, ctypes.c_double, _vp, ctypes.c_int, _vp, _vp]
+_lib.cci_grad_packed.argtypes = [_vp, _vp, ctypes.c_int, _i64, _i64, _vp, _i64, _i32, _i32, _vp, _vp]
 _lib.cci_auto_algo.argtypes = [ctypes.c_int, ctypes.c_int, _i64, _i64, _i64, _i64, _i32, _i32]
 _lib.cci_auto_algo.restype = ctypes.c_int
 _lib.cci_maxpool2d_nhwc.argtypes = [_vp, ctypes.c_int, _i64, _i64, _i64, _i64, _i32, _i32, _i32, _vp, _vp]
@@ -69,7 +72,8 @@ _lib.cci_last_error.restype = ctypes.c_char_p
 _lib.cci_version.restype = ctypes.c_int32
 for _fn in ("cci_packed_sizes", "cci_pack", "cci_spmm", "cci_spmm_algo", "cci_conv_im2col",
             "cci_conv_im2col_algo", "cci_maxpool2d_nhwc", "cci_global_avgpool_nhwc", "cci_bbs_packed_sizes",
-            "cci_bbs_pack", "cci_2of4_sizes", "cci_bbs_to_2of4", "cci_to_2of4_transposed", "cci_spmm_2of4"):
+            "cci_bbs_pack", "cci_2of4_sizes", "cci_bbs_to_2of4", "cci_to_2of4_transposed", "cci_spmm_2of4",
+            "cci_td_schedule", "cci_td_mask", "cci_grad_packed"):
     getattr(_lib, _fn).restype = ctypes.c_int
 
 
@@ -320,3 +324,43 @@ def spmm_2of4(X: torch.Tensor, a_vals: torch.Tensor, a_idx: torch.Tensor, *, sca
     _check(_lib.cci_spmm_2of4(_ptr(X), _code(X.dtype), N, R, _ptr(a_vals), _ptr(a_idx), M, ctypes.byref(ep), _ptr(Y),
                               _code(Y.dtype), _stream(X)))
     return Y
+
+
+# ------------------------------------------------ improved targeted dropout --
+
+def td_schedule(step: int, total: int, G: int, K: int):
+    """cci_td_schedule: (candidates per group, candidate dropout rate)."""
+    n = _i32()
+    p = ctypes.c_double()
+    _check(_lib.cci_td_schedule(step, total, G, K, ctypes.byref(n), ctypes.byref(p)))
+    return n.value, p.value
+
+
+def td_mask(W: torch.Tensor, G: int, n_target: int, bits: torch.Tensor, drop_rate: float, w_dtype=torch.bfloat16,
+            out=None):
+    """cci_td_mask: W fp32 [O, C], bits int32 [O, C] (the uint32 random words)
+    -> (W_eff [O, C] of w_dtype, keep uint8 [O, C])."""
+    _dev(W), _dev(bits)
+    O, C = W.shape
+    if W.dtype != torch.float32 or bits.dtype not in (torch.int32, torch.uint32) or tuple(bits.shape) != (O, C):
+        raise ValueError("W must be float32 [O, C] and bits 32-bit [O, C]")
+    if out is None:
+        We = torch.empty((O, C), dtype=w_dtype, device=W.device)
+        keep = torch.empty((O, C), dtype=torch.uint8, device=W.device)
+    else:
+        We, keep = _out(out[0], (O, C), w_dtype, W.device), _out(out[1], (O, C), torch.uint8, W.device)
+    _check(_lib.cci_td_mask(_ptr(W), O, C, G, n_target, _ptr(bits), float(drop_rate), _ptr(We), _code(w_dtype),
+                            _ptr(keep), _stream(W)))
+    return We, keep
+
+
+def grad_packed(dY: torch.Tensor, X: torch.Tensor, idx: torch.Tensor, G: int, out=None) -> torch.Tensor:
+    """cci_grad_packed: dvals fp32 [O/G, K, C] from dY [N, O], X [N, C]."""
+    _dev(dY), _dev(X), _dev(idx)
+    N, O = dY.shape
+    ng, K, C = idx.shape
+    if X.shape != (N, C) or ng * G != O or X.dtype != dY.dtype or idx.dtype != torch.uint8:
+        raise ValueError("shape or dtype mismatch")
+    dv = _out(out, (ng, K, C), torch.float32, dY.device)
+    _check(_lib.cci_grad_packed(_ptr(dY), _ptr(X), _code(dY.dtype), N, C, _ptr(idx), O, G, K, _ptr(dv), _stream(dY)))
+    return dv

@@ -3,6 +3,7 @@
 // than the calling thread's last error message.
 #include <hip/hip_runtime.h>
 
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -369,6 +370,50 @@ cci_status cci_spmm_2of4(const void* X, cci_dtype x_t, int64_t N, int64_t R, con
   hipError_t e = cci::launch_spmm_2of4(X, N, R, a_vals, a_idx, M, scale, bias, residual, ep ? ep->relu : 0, Y,
                                        to_dt(y_t), static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(CCI_EHIP, "2:4 product launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+cci_status cci_td_schedule(int64_t step, int64_t total, int32_t G, int32_t K, int32_t* n_target,
+                           double* drop_rate) {
+  if (total < 1 || step < 0 || step > total) return fail(CCI_EINVAL, "step %lld outside [0, %lld]", (long long)step, (long long)total);
+  if (G < 1 || G > 256 || K < 1 || K > G) return fail(CCI_EINVAL, "G=%d, K=%d out of range", G, K);
+  if (!n_target || !drop_rate) return fail(CCI_EINVAL, "null output pointer");
+  // first half: candidates ramp 0 -> G-K at dropout 1/2; second half: dropout 1/2 -> 1
+  const double f = static_cast<double>(step) / static_cast<double>(total);
+  const double ramp = f >= 0.5 ? 1.0 : 2.0 * f;
+  *n_target = static_cast<int32_t>(std::floor(static_cast<double>(G - K) * ramp + 0.5));
+  *drop_rate = f < 0.5 ? 0.5 : f;
+  return ok();
+}
+
+cci_status cci_td_mask(const float* W, int64_t O, int64_t C, int32_t G, int32_t n_target, const uint32_t* bits,
+                       double drop_rate, void* W_eff, cci_dtype w_t, uint8_t* keep, void* stream) {
+  if (cci_status s = check_groups(O, C, G, 1)) return s;
+  if (n_target < 0 || n_target > G) return fail(CCI_EINVAL, "n_target=%d outside [0, G=%d]", n_target, G);
+  if (!(drop_rate >= 0.0 && drop_rate <= 1.0)) return fail(CCI_EINVAL, "drop_rate outside [0, 1]");
+  if (!dtype_ok(w_t)) return fail(CCI_EINVAL, "unknown dtype code");
+  if (!W || !bits || !W_eff || !keep) return fail(CCI_EINVAL, "null pointer");
+  if (!aligned16(W) || !aligned16(bits) || !aligned16(W_eff) || !aligned16(keep))
+    return fail(CCI_EALIGN, "pointer not 16-byte aligned");
+  const uint64_t thr = static_cast<uint64_t>(std::floor(drop_rate * 4294967296.0));
+  hipError_t e = cci::launch_td_mask(W, O, C, G, n_target, bits, thr, W_eff, to_dt(w_t), keep,
+                                     static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(CCI_EHIP, "td mask launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+cci_status cci_grad_packed(const void* dY, const void* X, cci_dtype t, int64_t N, int64_t C, const uint8_t* idx,
+                           int64_t O, int32_t G, int32_t K, float* dvals, void* stream) {
+  if (cci_status s = check_groups(O, C, G, K)) return s;
+  if (!dtype_ok(t)) return fail(CCI_EINVAL, "unknown dtype code");
+  if (N < 0) return fail(CCI_EINVAL, "N=%lld < 0", (long long)N);
+  if (N > (int64_t(1) << 40) / (C > O ? C : O)) return fail(CCI_EINVAL, "N too large");
+  if (!idx || !dvals) return fail(CCI_EINVAL, "null pointer");
+  if (N > 0 && (!dY || !X)) return fail(CCI_EINVAL, "null pointer");
+  if ((N > 0 && (!aligned16(dY) || !aligned16(X))) || !aligned16(idx) || !aligned16(dvals))
+    return fail(CCI_EALIGN, "pointer not 16-byte aligned");
+  hipError_t e = cci::launch_grad_packed(dY, X, to_dt(t), N, C, idx, O, G, K, dvals, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(CCI_EHIP, "packed-gradient launch failed: %s", hipGetErrorString(e));
   return ok();
 }
 

@@ -96,6 +96,13 @@ hipError_t launch_spmm_2of4(const void* X, int64_t N, int64_t C, const void* av,
                             const float* scale, const float* bias, const void* residual, int32_t relu, void* Y,
                             DType y_t, hipStream_t s);
 
+// Improved targeted dropout: candidate dropout of one step, and the gradient
+// of the packed values of a CCI layer.
+hipError_t launch_td_mask(const float* W, int64_t O, int64_t C, int32_t G, int32_t n_target, const uint32_t* bits,
+                          uint64_t thr, void* We, DType w_t, uint8_t* keep, hipStream_t s);
+hipError_t launch_grad_packed(const void* dY, const void* X, DType t, int64_t N, int64_t C, const uint8_t* idx,
+                              int64_t O, int32_t G, int32_t K, float* dv, hipStream_t s);
+
 hipError_t launch_maxpool(const void* X, DType t, int64_t B, int64_t H, int64_t W, int64_t C,
                           int32_t k, int32_t st, int32_t p, void* Y, hipStream_t s);
 hipError_t launch_avgpool(const void* X, DType x_t, int64_t B, int64_t H, int64_t W, int64_t C,

@@ -196,3 +196,24 @@ def test_bbs_and_2of4_validation():
     assert lib.cci_spmm_2of4(FAKE, cci.BF16, -1, 64, FAKE, FAKE, 16, None, FAKE, cci.BF16, None) == cci.EINVAL
     assert lib.cci_spmm_2of4(None, cci.BF16, 0, 64, None, None, 16, None, None, cci.BF16, None) == cci.OK
     assert lib.cci_spmm_2of4(FAKE, cci.BF16, 4, 64, FAKE_MIS, FAKE, 16, None, FAKE, cci.BF16, None) == cci.EALIGN
+
+
+def test_td_schedule_host_logic_matches_oracle():
+    import oracle
+    for total in (1, 7, 100, 1001):
+        for G, K in ((8, 2), (16, 1), (4, 4), (256, 3)):
+            for step in sorted({0, 1, total // 3, total // 2, total // 2 + 1, total - 1, total}):
+                assert cci.td_schedule(step, total, G, K) == oracle.td_schedule(step, total, G, K)
+    n, p = ctypes.c_int32(7), ctypes.c_double(7.0)
+    assert lib.cci_td_schedule(5, 4, 8, 2, ctypes.byref(n), ctypes.byref(p)) == cci.EINVAL
+    assert n.value == 7 and p.value == 7.0
+
+
+def test_td_mask_and_grad_validation():
+    assert lib.cci_td_mask(FAKE, 16, 8, 8, 9, FAKE, ctypes.c_double(0.5), FAKE, cci.BF16, FAKE, None) == cci.EINVAL
+    assert lib.cci_td_mask(FAKE, 16, 8, 8, 2, FAKE, ctypes.c_double(1.5), FAKE, cci.BF16, FAKE, None) == cci.EINVAL
+    assert lib.cci_td_mask(FAKE, 12, 8, 8, 2, FAKE, ctypes.c_double(0.5), FAKE, cci.BF16, FAKE, None) == cci.EINVAL
+    assert lib.cci_td_mask(FAKE, 16, 8, 8, 2, FAKE_MIS, ctypes.c_double(0.5), FAKE, cci.BF16, FAKE, None) == cci.EALIGN
+    assert lib.cci_grad_packed(FAKE, FAKE, cci.BF16, 4, 8, FAKE, 16, 8, 9, FAKE, None) == cci.EINVAL
+    assert lib.cci_grad_packed(FAKE, FAKE, cci.BF16, -1, 8, FAKE, 16, 8, 2, FAKE, None) == cci.EINVAL
+    assert lib.cci_grad_packed(FAKE, FAKE, cci.BF16, 4, 8, FAKE, 16, 8, 2, FAKE_MIS, None) == cci.EALIGN

@@ -83,6 +83,10 @@ def _load():
     lib.oracle_td_mask.argtypes = [_f32p, _i64, _i64, _i32, _i32, ctypes.POINTER(ctypes.c_uint32), ctypes.c_double,
                                    _f32p, _u8p]
     lib.oracle_grad_packed.argtypes = [_f32p, _f32p, _i64, _i64, _u8p, _i64, _i32, _i32, _f64p]
+    lib.oracle_index_width.argtypes = [_i32]
+    lib.oracle_index_width.restype = _i32
+    lib.oracle_index_bits.argtypes = [_u8p, _i64, _i32, ctypes.POINTER(ctypes.c_uint32)]
+    lib.oracle_index_unbits.argtypes = [ctypes.POINTER(ctypes.c_uint32), _i64, _i32, _u8p]
     lib.oracle_num_threads.restype = ctypes.c_int
     lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
     lib.oracle_set_num_threads.restype = None
@@ -90,7 +94,8 @@ def _load():
                "oracle_dense_rows", "oracle_conv2d_nhwc_rows",
                "oracle_im2col_nhwc", "oracle_maxpool2d_nhwc",
                "oracle_global_avgpool_nhwc", "oracle_bbs_pack", "oracle_bbs_unpack",
-               "oracle_bbs_spmm_rows", "oracle_td_schedule", "oracle_td_mask", "oracle_grad_packed"):
+               "oracle_bbs_spmm_rows", "oracle_td_schedule", "oracle_td_mask", "oracle_grad_packed",
+               "oracle_index_bits", "oracle_index_unbits"):
         getattr(lib, fn).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -378,3 +383,32 @@ def grad_packed(dY, X, idx, G):
     _check(_load().oracle_grad_packed(_p(dY, _f32p), _p(X, _f32p), N, C, _p(idx, _u8p), O, G, K, _p(out, _f64p)),
            "grad_packed")
     return out
+
+
+# ------------------------------------------------------ log2(G)-bit indices --
+
+def index_width(G: int) -> int:
+    """Bits of a plain intra-group index (Sec. 3.1): ceil(log2 G), at least 1."""
+    b = int(_load().oracle_index_width(G))
+    if b < 0:
+        raise ValueError("G outside [1, 256]")
+    return b
+
+
+def index_bits(idx: np.ndarray, b: int) -> np.ndarray:
+    """The index array as a little-endian b-bit stream (uint32 words)."""
+    idx = np.ascontiguousarray(idx, np.uint8).reshape(-1)
+    words = np.empty(((idx.size * b + 31) // 32,), np.uint32)
+    _check(_load().oracle_index_bits(_p(idx, _u8p), idx.size, b,
+                                     words.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32))), "index_bits")
+    return words
+
+
+def index_unbits(words: np.ndarray, n: int, b: int) -> np.ndarray:
+    words = np.ascontiguousarray(words, np.uint32)
+    if words.size < (n * b + 31) // 32:
+        raise ValueError("stream too short")
+    idx = np.empty((n,), np.uint8)
+    _check(_load().oracle_index_unbits(words.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)), n, b, _p(idx, _u8p)),
+           "index_unbits")
+    return idx

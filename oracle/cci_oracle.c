@@ -492,6 +492,49 @@ int oracle_grad_packed(const float *dY, const float *X, int64_t N, int64_t C,
 }
 
 /*
+ * Plain log2(G)-bit indices (paper Sec. 3.1: each kept weight carries the
+ * plain index of its row inside the group, log2 G bits).  With
+ * b = ceil(log2 G) (at least 1), entry e of an index array occupies bits
+ * e*b .. e*b + b - 1 of a little-endian bit stream: stream bit t is bit
+ * t % 32 of 32-bit word t / 32.  The stream has ceil(n * b / 32) words;
+ * bits past the last entry are 0.  (With b = 8 the stream is the byte array
+ * itself.)
+ */
+int32_t oracle_index_width(int32_t G) {
+  if (G < 1 || G > 256) return -1;
+  int32_t b = 1;
+  while ((1 << b) < G) ++b;
+  return b;
+}
+
+int oracle_index_bits(const uint8_t *idx, int64_t n, int32_t b, uint32_t *words) {
+  if (n < 0 || b < 1 || b > 8) return ORACLE_EINVAL;
+  const int64_t nw = (n * b + 31) / 32;
+  for (int64_t w = 0; w < nw; ++w) words[w] = 0u;
+  for (int64_t e = 0; e < n; ++e) {
+    if (idx[e] >> b) return ORACLE_EINVAL; /* the value does not fit */
+    for (int32_t j = 0; j < b; ++j) {
+      const int64_t t = e * b + j;
+      if ((idx[e] >> j) & 1u) words[t / 32] |= 1u << (t % 32);
+    }
+  }
+  return ORACLE_OK;
+}
+
+int oracle_index_unbits(const uint32_t *words, int64_t n, int32_t b, uint8_t *idx) {
+  if (n < 0 || b < 1 || b > 8) return ORACLE_EINVAL;
+  for (int64_t e = 0; e < n; ++e) {
+    uint32_t v = 0;
+    for (int32_t j = 0; j < b; ++j) {
+      const int64_t t = e * b + j;
+      v |= ((words[t / 32] >> (t % 32)) & 1u) << j;
+    }
+    idx[e] = (uint8_t)v;
+  }
+  return ORACLE_OK;
+}
+
+/*
  * Round-to-nearest-even conversion of an fp32 value to bfloat16 (the upper
  * 16 bits of an IEEE binary32), written from the definition: the result is
  * the representable bf16 nearest to x; on an exact tie the one whose last

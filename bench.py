@@ -64,6 +64,7 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-dense", action="store_true")
     p.add_argument("--no-bbs", action="store_true", help="fc4096: skip the balanced-sparsity (2:4) comparison")
+    p.add_argument("--no-td", action="store_true", help="fc4096: skip the targeted-dropout training-step kernels")
     p.add_argument("--graph", action="store_true",
                    help="replay the timed steps from HIP graphs of 8 steps instead of launching every kernel "
                         "from Python")
@@ -494,6 +495,45 @@ def bbs_compare(Xs, Ys, W, ncopy, stream, dense, per_k):
     return out
 
 
+def td_compare(Xs, W, ncopy, stream, per_k):
+    """Kernels of an improved-targeted-dropout step on the 4096^3 layer (G = 16):
+    the candidate-dropout mask (HBM-bound: W and 32-bit random words read, W_eff
+    bf16 and the keep mask written), and once the mask is fixed the gradient of
+    the packed values (N * nnz multiply-adds on the vector ALUs) next to the
+    dense weight gradient dY^T X on hipBLASLt.  dY is the rotated X."""
+    import torch
+    from paper_1910_11971_amd import cci
+    N, C = Xs[0].shape
+    O = W.shape[0]
+    G = 16
+    bits = torch.randint(-2**31, 2**31 - 1, (O, C), dtype=torch.int32, device=W.device)
+    We = torch.empty((O, C), dtype=torch.bfloat16, device=W.device)
+    keep = torch.empty((O, C), dtype=torch.uint8, device=W.device)
+    n_t, p = cci.td_schedule(3, 4, G, 4)
+    t_mask = _graph_time(lambda i: cci.td_mask(W, G, n_t, bits, p, out=(We, keep)), 4, 8, stream)
+    mask_bytes = O * C * (4 + 4 + 2 + 1)
+    out = {"td_mask_us": round(t_mask * 1e3, 3), "td_mask": {"n_target": n_t, "drop_rate": p},
+           "td_mask_roofline": own_roof(0.0, mask_bytes, t_mask)}
+    dYt = Xs[1 % ncopy].t().contiguous()
+    dW = torch.empty((O, C), dtype=torch.bfloat16, device=W.device)
+    t_dw, how = _dense_time(lambda i: torch.matmul(dYt, Xs[i % ncopy], out=dW), 4, stream)
+    out["dense_dW_gemm_us"] = round(t_dw * 1e3, 3)
+    out["dense_timing"] = how
+    for K in (1, 2, 4):
+        idx = per_k[K]["idx"]
+        dv = torch.empty(tuple(idx.shape), dtype=torch.float32, device=W.device)
+        t = _graph_time(lambda i: cci.grad_packed(Xs[(i + 1) % ncopy], Xs[i % ncopy], idx, G, out=dv), 4, 4, stream)
+        nnz = O * C * K // G
+        flop = 2.0 * N * nnz
+        alg_bytes = 2 * N * O + 2 * N * C + nnz * 5
+        out[f"grad_packed_K{K}"] = {"us": round(t * 1e3, 3), "eff_TFLOPs": round(flop / (t * 1e-3) / 1e12, 2),
+                                    "roofline": roof_for("cci_grad_packed", flop, None, alg_bytes, t),
+                                    "speedup_vs_dense_dW": round(t_dw / t, 3)}
+    out["note"] = ("re-projection = cci_pack (sweep_k pack_us); backward dX of the fixed-mask layer = "
+                   "bbs_2of4 cci_backward_dX_us")
+    return out
+
+
 def main_fc_sweep(args):
     """The 4096^3 FC layer, G = 16: the timed steps at K = args.k, and every K
     of the sweep measured kernel by kernel in the same process."""
@@ -551,6 +591,7 @@ def main_fc_sweep(args):
 
     # ---- balanced sparsity on the 2:4 sparse matrix cores, same shape -------------
     bbs = None if args.no_bbs else bbs_compare(Xs, Ys, W, ncopy, stream, dense, per_k)
+    td = None if args.no_td else td_compare(Xs, W, ncopy, stream, per_k)
 
     # ---- timed region: whole steps (pack + product) at the declared K ------------
     sel = per_k[args.k]
@@ -628,6 +669,7 @@ def main_fc_sweep(args):
         "roofline": roof,
         "sweep_k": sweep_k,
         "bbs_2of4": bbs,
+        "td_step": td,
         "cpu_baseline": cpu,
         "dense_bf16": dense,
         "speedup_vs_dense_gemm": None if dense is None else round(dense["gemm_ms"] / sel["t_prod"], 3),

@@ -287,6 +287,41 @@ cci_status cci_grad_packed(const void *dY, const void *X, cci_dtype t,
                            int64_t N, int64_t C, const uint8_t *idx, int64_t O,
                            int32_t G, int32_t K, float *dvals, void *stream);
 
+/* ------------------------------------------------------------------------
+ * Plain log2(G)-bit indices (Sec. 3.1: each kept weight's index into its
+ * group is stored in log2 G bits).  Stream format: with b bits per entry,
+ * entry e of an index array occupies bits e*b .. e*b+b-1 of a little-endian
+ * stream of 32-bit words (stream bit t is bit t % 32 of word t / 32); bits
+ * past the last entry are 0.  b = 8 is exactly the byte array of cci_pack.
+ * ------------------------------------------------------------------------ */
+
+/* ceil(log2 G), at least 1: the plain index width of groups of G.  -1 if G
+ * is outside [1, 256].  Host-only. */
+int32_t cci_index_width(int32_t G);
+
+/* Bytes of the stream of n entries of `bits` bits: ceil(n*bits/32)*4. */
+cci_status cci_index_stream_bytes(int64_t n, int32_t bits, size_t *bytes);
+
+/* The byte index array idx (n entries, as from cci_pack) as a stream of
+ * `bits`-bit entries (1 <= bits <= 8).  Entries must be < 2^bits (a packing
+ * with G <= 2^bits; higher bits are dropped).  words: device uint32 of
+ * cci_index_stream_bytes bytes. */
+cci_status cci_index_bits(const uint8_t *idx, int64_t n, int32_t bits,
+                          uint32_t *words, void *stream);
+
+/* The CCI product of cci_spmm with the indices read as `idx_bits`-bit
+ * entries: idx is the stream of cci_index_bits for
+ * cci_index_width(G) <= idx_bits < 8, or the byte array of cci_pack for
+ * idx_bits = 8.  This is the few-row product (N <= 64: a decode-sized batch)
+ * where the packed weight bytes set the time; bf16 X and values, C % 32 == 0,
+ * O % 16 == 0 (CCI_EUNSUPPORTED otherwise).  Epilogue and output as for
+ * cci_spmm. */
+cci_status cci_spmm_bits(const void *X, cci_dtype x_t, int64_t N, int64_t C,
+                         const void *vals, cci_dtype val_t, const void *idx,
+                         int32_t idx_bits, int64_t O, int32_t G, int32_t K,
+                         const cci_epilogue *ep, void *Y, cci_dtype y_t,
+                         void *stream);
+
 /* CNN glue for the ResNet-shaped forward (not from the paper).
  * Max pooling, NHWC, window k, stride s, padding p (padding never wins).
  * X, Y: device [B][H][W][C] -> [B][Ho][Wo][C] of dtype t (F32 or BF16). */

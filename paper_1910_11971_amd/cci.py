@@ -62,6 +62,12 @@ _lib.cci_spmm_2of4.argtypes = [_vp, ctypes.c_int, _i64, _i64, _vp, _vp, _i64, ct
 _lib.cci_td_schedule.argtypes = [_i64, _i64, _i32, _i32, ctypes.POINTER(_i32), ctypes.POINTER(ctypes.c_double)]
 _lib.cci_td_mask.argtypes = [_vp, _i64, _i64, _i32, _i32, _vp, ctypes.c_double, _vp, ctypes.c_int, _vp, _vp]
 _lib.cci_grad_packed.argtypes = [_vp, _vp, ctypes.c_int, _i64, _i64, _vp, _i64, _i32, _i32, _vp, _vp]
+_lib.cci_index_width.argtypes = [_i32]
+_lib.cci_index_width.restype = _i32
+_lib.cci_index_stream_bytes.argtypes = [_i64, _i32, ctypes.POINTER(_sz)]
+_lib.cci_index_bits.argtypes = [_vp, _i64, _i32, _vp, _vp]
+_lib.cci_spmm_bits.argtypes = [_vp, ctypes.c_int, _i64, _i64, _vp, ctypes.c_int, _vp, _i32, _i64, _i32, _i32,
+                               ctypes.POINTER(Epilogue), _vp, ctypes.c_int, _vp]
 _lib.cci_auto_algo.argtypes = [ctypes.c_int, ctypes.c_int, _i64, _i64, _i64, _i64, _i32, _i32]
 _lib.cci_auto_algo.restype = ctypes.c_int
 _lib.cci_maxpool2d_nhwc.argtypes = [_vp, ctypes.c_int, _i64, _i64, _i64, _i64, _i32, _i32, _i32, _vp, _vp]
@@ -73,7 +79,8 @@ _lib.cci_version.restype = ctypes.c_int32
 for _fn in ("cci_packed_sizes", "cci_pack", "cci_spmm", "cci_spmm_algo", "cci_conv_im2col",
             "cci_conv_im2col_algo", "cci_maxpool2d_nhwc", "cci_global_avgpool_nhwc", "cci_bbs_packed_sizes",
             "cci_bbs_pack", "cci_2of4_sizes", "cci_bbs_to_2of4", "cci_to_2of4_transposed", "cci_spmm_2of4",
-            "cci_td_schedule", "cci_td_mask", "cci_grad_packed"):
+            "cci_td_schedule", "cci_td_mask", "cci_grad_packed", "cci_index_stream_bytes", "cci_index_bits",
+            "cci_spmm_bits"):
     getattr(_lib, _fn).restype = ctypes.c_int
 
 
@@ -364,3 +371,44 @@ def grad_packed(dY: torch.Tensor, X: torch.Tensor, idx: torch.Tensor, G: int, ou
     dv = _out(out, (ng, K, C), torch.float32, dY.device)
     _check(_lib.cci_grad_packed(_ptr(dY), _ptr(X), _code(dY.dtype), N, C, _ptr(idx), O, G, K, _ptr(dv), _stream(dY)))
     return dv
+
+
+# ------------------------------------------------------ log2(G)-bit indices --
+
+def index_width(G: int) -> int:
+    """cci_index_width: ceil(log2 G), at least 1."""
+    b = int(_lib.cci_index_width(G))
+    if b < 0:
+        raise ValueError("G outside [1, 256]")
+    return b
+
+
+def index_bits(idx: torch.Tensor, bits: int, out=None) -> torch.Tensor:
+    """cci_index_bits: uint8 index array (any shape) -> int32 tensor holding
+    the uint32 words of its `bits`-bit stream."""
+    _dev(idx)
+    if idx.dtype != torch.uint8:
+        raise TypeError("idx must be uint8")
+    n = idx.numel()
+    nb = _sz()
+    _check(_lib.cci_index_stream_bytes(n, bits, ctypes.byref(nb)))
+    words = _out(out, (nb.value // 4,), torch.int32, idx.device)
+    _check(_lib.cci_index_bits(_ptr(idx), n, bits, _ptr(words), _stream(idx)))
+    return words
+
+
+def spmm_bits(X: torch.Tensor, vals: torch.Tensor, idx: torch.Tensor, G: int, idx_bits: int, *, scale=None,
+              bias=None, residual=None, relu=False, out_dtype=None, out=None) -> torch.Tensor:
+    """cci_spmm_bits: the few-row (N <= 64) CCI product reading `idx_bits`-bit
+    indices (the stream of index_bits, or the uint8 array for 8)."""
+    _dev(X), _dev(vals), _dev(idx)
+    N, C = X.shape
+    ng, K, C2 = vals.shape
+    if C2 != C:
+        raise ValueError("shape mismatch between X and packed weights")
+    O = ng * G
+    Y = _out(out, (N, O), out_dtype or X.dtype, X.device)
+    ep = _epilogue(scale, bias, residual, relu, O, Y.shape, Y.dtype, X.device)
+    _check(_lib.cci_spmm_bits(_ptr(X), _code(X.dtype), N, C, _ptr(vals), _code(vals.dtype), _ptr(idx), idx_bits, O, G,
+                              K, ctypes.byref(ep), _ptr(Y), _code(Y.dtype), _stream(X)))
+    return Y

@@ -417,6 +417,57 @@ cci_status cci_grad_packed(const void* dY, const void* X, cci_dtype t, int64_t N
   return ok();
 }
 
+int32_t cci_index_width(int32_t G) {
+  if (G < 1 || G > 256) return -1;
+  int32_t b = 1;
+  while ((1 << b) < G) ++b;
+  return b;
+}
+
+cci_status cci_index_stream_bytes(int64_t n, int32_t bits, size_t* bytes) {
+  if (n < 0 || bits < 1 || bits > 8) return fail(CCI_EINVAL, "n=%lld or bits=%d out of range", (long long)n, bits);
+  if (!bytes) return fail(CCI_EINVAL, "null output pointer");
+  *bytes = static_cast<size_t>((n * bits + 31) / 32 * 4);
+  return ok();
+}
+
+cci_status cci_index_bits(const uint8_t* idx, int64_t n, int32_t bits, uint32_t* words, void* stream) {
+  if (n < 0 || n >= (int64_t(1) << 36) || bits < 1 || bits > 8)
+    return fail(CCI_EINVAL, "n=%lld or bits=%d out of range", (long long)n, bits);
+  if (n == 0) return ok();
+  if (!idx || !words) return fail(CCI_EINVAL, "null pointer");
+  if (!aligned16(idx) || !aligned16(words)) return fail(CCI_EALIGN, "pointer not 16-byte aligned");
+  hipError_t e = cci::launch_index_bits(idx, n, bits, words, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(CCI_EHIP, "index-bits launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+cci_status cci_spmm_bits(const void* X, cci_dtype x_t, int64_t N, int64_t C, const void* vals, cci_dtype val_t,
+                         const void* idx, int32_t idx_bits, int64_t O, int32_t G, int32_t K, const cci_epilogue* ep,
+                         void* Y, cci_dtype y_t, void* stream) {
+  if (cci_status s = check_groups(O, C, G, K)) return s;
+  if (cci_status s = check_types(x_t, val_t, y_t)) return s;
+  if (N < 0) return fail(CCI_EINVAL, "N=%lld < 0", (long long)N);
+  if (idx_bits < cci_index_width(G) || idx_bits > 8)
+    return fail(CCI_EINVAL, "idx_bits=%d outside [%d, 8] for G=%d", idx_bits, cci_index_width(G), G);
+  if (x_t != CCI_BF16) return fail(CCI_EUNSUPPORTED, "the bit-index product takes bf16 X and values");
+  if (!cci::spmm_bits_supports(N, C, O, G, K))
+    return fail(CCI_EUNSUPPORTED, "the bit-index product is for N <= 64 rows, C %% 32 == 0 and O %% 16 == 0");
+  const float* scale = ep ? ep->scale : nullptr;
+  const float* bias = ep ? ep->bias : nullptr;
+  const void* residual = ep ? ep->residual : nullptr;
+  if ((scale && !aligned16(scale)) || (bias && !aligned16(bias)) || (residual && !aligned16(residual)))
+    return fail(CCI_EALIGN, "epilogue pointer not 16-byte aligned");
+  if (N == 0) return ok();
+  if (!X || !vals || !idx || !Y) return fail(CCI_EINVAL, "null pointer");
+  if (!aligned16(X) || !aligned16(vals) || !aligned16(idx) || !aligned16(Y))
+    return fail(CCI_EALIGN, "pointer not 16-byte aligned");
+  hipError_t e = cci::launch_spmm_bits(X, N, C, vals, idx, idx_bits, O, G, K, scale, bias, residual, ep ? ep->relu : 0,
+                                       Y, to_dt(y_t), static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(CCI_EHIP, "bit-index product launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
 cci_status cci_maxpool2d_nhwc(const void* X, cci_dtype t, int64_t B, int64_t H, int64_t W,
                               int64_t C, int32_t k, int32_t s, int32_t p, void* Y, void* stream) {
   if (!dtype_ok(t)) return fail(CCI_EINVAL, "unknown dtype code");

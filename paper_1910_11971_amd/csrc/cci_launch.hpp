@@ -103,6 +103,14 @@ hipError_t launch_td_mask(const float* W, int64_t O, int64_t C, int32_t G, int32
 hipError_t launch_grad_packed(const void* dY, const void* X, DType t, int64_t N, int64_t C, const uint8_t* idx,
                               int64_t O, int32_t G, int32_t K, float* dv, hipStream_t s);
 
+// Plain log2(G)-bit index streams and the few-row product that reads them.
+int64_t index_stream_bytes(int64_t n, int32_t b);
+hipError_t launch_index_bits(const uint8_t* idx, int64_t n, int32_t b, uint32_t* words, hipStream_t s);
+bool spmm_bits_supports(int64_t N, int64_t C, int64_t O, int32_t G, int32_t K);
+hipError_t launch_spmm_bits(const void* X, int64_t N, int64_t C, const void* vals, const void* idx, int32_t b,
+                            int64_t O, int32_t G, int32_t K, const float* scale, const float* bias,
+                            const void* residual, int32_t relu, void* Y, DType y_t, hipStream_t s);
+
 hipError_t launch_maxpool(const void* X, DType t, int64_t B, int64_t H, int64_t W, int64_t C,
                           int32_t k, int32_t st, int32_t p, void* Y, hipStream_t s);
 hipError_t launch_avgpool(const void* X, DType x_t, int64_t B, int64_t H, int64_t W, int64_t C,

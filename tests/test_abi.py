@@ -217,3 +217,24 @@ def test_td_mask_and_grad_validation():
     assert lib.cci_grad_packed(FAKE, FAKE, cci.BF16, 4, 8, FAKE, 16, 8, 9, FAKE, None) == cci.EINVAL
     assert lib.cci_grad_packed(FAKE, FAKE, cci.BF16, -1, 8, FAKE, 16, 8, 2, FAKE, None) == cci.EINVAL
     assert lib.cci_grad_packed(FAKE, FAKE, cci.BF16, 4, 8, FAKE, 16, 8, 2, FAKE_MIS, None) == cci.EALIGN
+
+
+def test_index_width_host_logic_and_bits_validation():
+    import oracle
+    for G in range(1, 257):
+        assert cci.index_width(G) == oracle.index_width(G)
+    assert lib.cci_index_width(0) == -1 and lib.cci_index_width(257) == -1
+    nb = ctypes.c_size_t(0)
+    assert lib.cci_index_stream_bytes(33, 3, ctypes.byref(nb)) == cci.OK and nb.value == 16
+    assert lib.cci_index_stream_bytes(33, 9, ctypes.byref(nb)) == cci.EINVAL
+    assert lib.cci_index_bits(FAKE, 10, 0, FAKE, None) == cci.EINVAL
+    assert lib.cci_index_bits(FAKE_MIS, 10, 3, FAKE, None) == cci.EALIGN
+    # too few bits for G, unsupported row count, fp32
+    assert lib.cci_spmm_bits(FAKE, cci.BF16, 4, 64, FAKE, cci.BF16, FAKE, 3, 64, 16, 2, None, FAKE, cci.BF16,
+                             None) == cci.EINVAL
+    assert lib.cci_spmm_bits(FAKE, cci.BF16, 65, 64, FAKE, cci.BF16, FAKE, 4, 64, 16, 2, None, FAKE, cci.BF16,
+                             None) == cci.EUNSUPPORTED
+    assert lib.cci_spmm_bits(FAKE, cci.F32, 4, 64, FAKE, cci.F32, FAKE, 4, 64, 16, 2, None, FAKE, cci.F32,
+                             None) == cci.EUNSUPPORTED
+    assert lib.cci_spmm_bits(None, cci.BF16, 0, 64, None, cci.BF16, None, 4, 64, 16, 2, None, None, cci.BF16,
+                             None) == cci.OK

@@ -65,6 +65,7 @@ def parse():
     p.add_argument("--no-dense", action="store_true")
     p.add_argument("--no-bbs", action="store_true", help="fc4096: skip the balanced-sparsity (2:4) comparison")
     p.add_argument("--no-td", action="store_true", help="fc4096: skip the targeted-dropout training-step kernels")
+    p.add_argument("--no-smalln", action="store_true", help="fc4096: skip the few-row (log2 G-bit index) products")
     p.add_argument("--graph", action="store_true",
                    help="replay the timed steps from HIP graphs of 8 steps instead of launching every kernel "
                         "from Python")
@@ -534,6 +535,55 @@ def td_compare(Xs, W, ncopy, stream, per_k):
     return out
 
 
+def smalln_compare(Xs, W, stream, with_dense):
+    """Few-row products of the 4096 x 4096 layer (G = 16) where the packed
+    weight bytes set the time: cci_spmm_bits with 4-bit (log2 G) indices
+    against the same kernel reading the byte indices, the library's choice
+    (cci_spmm) and a dense bf16 GEMM of the same shape.  Roofline: HBM on
+    X + packed values + indices + Y, with each launch reading fresh weights
+    (8 packed copies rotated)."""
+    import torch
+    from paper_1910_11971_amd import cci
+    C = Xs[0].shape[1]
+    O = W.shape[0]
+    G = 16
+    b = cci.index_width(G)
+    out = {}
+    Wd_t = W.to(torch.bfloat16).t().contiguous()
+    copies = 8
+    for K in (1, 4):
+        packs = [cci.pack(W * (1.0 + 0.001 * i), G, K, torch.bfloat16) for i in range(copies)]
+        streams = [cci.index_bits(ix, b) for _, ix in packs]
+        nnz = O * C * K // G
+        for N in (1, 16, 64):
+            X = Xs[0][:N].contiguous()
+            Y = torch.empty((N, O), dtype=torch.bfloat16, device=W.device)
+            t_bits = _graph_time(lambda i: cci.spmm_bits(X, packs[i % copies][0], streams[i % copies], G, b, out=Y),
+                                 copies, 8, stream)
+            t_byte = _graph_time(lambda i: cci.spmm_bits(X, packs[i % copies][0], packs[i % copies][1], G, 8, out=Y),
+                                 copies, 8, stream)
+            t_auto = _graph_time(lambda i: cci.spmm(X, packs[i % copies][0], packs[i % copies][1], G, out=Y),
+                                 copies, 8, stream)
+            flop = 2.0 * N * nnz
+            io = N * C * 2 + N * O * 2
+            bytes_bits = io + nnz * 2 + (nnz * b + 7) // 8
+            bytes_byte = io + nnz * 3
+            e = {"bits_us": round(t_bits * 1e3, 3), "bytes_us": round(t_byte * 1e3, 3),
+                 "auto_us": round(t_auto * 1e3, 3),
+                 "bits_roofline": own_roof(flop, bytes_bits, t_bits),
+                 "bytes_roofline": own_roof(flop, bytes_byte, t_byte),
+                 "alg_bytes_bits": bytes_bits, "alg_bytes_uint8": bytes_byte}
+            if with_dense:
+                t_d = _graph_time(lambda i: torch.matmul(X, Wd_t, out=Y), copies, 8, stream)
+                e["dense_gemm_us"] = round(t_d * 1e3, 3)
+                e["speedup_bits_vs_dense"] = round(t_d / t_bits, 3)
+            out[f"K{K}_N{N}"] = e
+        del packs, streams
+    out["note"] = (f"index width {b} bits (ceil(log2 16)) vs 8; the dense GEMM reads one 32 MB weight copy "
+                   "(warm in the last-level cache), the CCI kernels rotate 8 packed copies")
+    return out
+
+
 def main_fc_sweep(args):
     """The 4096^3 FC layer, G = 16: the timed steps at K = args.k, and every K
     of the sweep measured kernel by kernel in the same process."""
@@ -592,6 +642,7 @@ def main_fc_sweep(args):
     # ---- balanced sparsity on the 2:4 sparse matrix cores, same shape -------------
     bbs = None if args.no_bbs else bbs_compare(Xs, Ys, W, ncopy, stream, dense, per_k)
     td = None if args.no_td else td_compare(Xs, W, ncopy, stream, per_k)
+    smalln = None if args.no_smalln else smalln_compare(Xs, W, stream, dense is not None)
 
     # ---- timed region: whole steps (pack + product) at the declared K ------------
     sel = per_k[args.k]
@@ -670,6 +721,7 @@ def main_fc_sweep(args):
         "sweep_k": sweep_k,
         "bbs_2of4": bbs,
         "td_step": td,
+        "few_rows_bits": smalln,
         "cpu_baseline": cpu,
         "dense_bf16": dense,
         "speedup_vs_dense_gemm": None if dense is None else round(dense["gemm_ms"] / sel["t_prod"], 3),

@@ -10,12 +10,13 @@
 //
 // cci_grad_packed: gradient of the packed values once the mask is fixed,
 //   dvals[g][k][c] = sum_n dY[n][gG + idx[g][k][c]] * X[n][c].
-// A workgroup owns one group and 256 columns (a lane per column, its K
-// indices in registers); rows of dY restricted to the group's G outputs are
-// staged in LDS (64 at a time, fewer for G > 128), and each lane gathers the K entries its
-// indices name (one LDS read and one FMA per kept weight and row) while
-// X[n][c] streams in coalesced.  Only kept weights are touched, so the work
-// is N * nnz multiply-adds on the vector ALUs.
+// A workgroup owns four consecutive groups and 256 columns (a lane per
+// column, its indices in registers); per pass of up to 32 rows the rows of dY
+// restricted to those groups' outputs and of X restricted to the columns are
+// staged in LDS with every load in flight, then each lane gathers the
+// entries its indices name (one LDS read and one FMA per kept weight and row).
+// Only kept weights are touched: N * nnz multiply-adds on the vector ALUs.
+#include <algorithm>
 #include <type_traits>
 
 #include "cci_launch.hpp"
@@ -104,84 +105,98 @@ hipError_t td_mask_typed(const float* W, int64_t O, int64_t C, int32_t G, int32_
 }
 
 // ---------------------------------------------------------------------------
+// Gradient of the packed values.  A workgroup owns GB consecutive groups and
+// 256 columns (a lane per column); per pass over the rows it takes KB slots
+// of every group, so one staged X[n][c] feeds GB * KB multiply-adds.
 
-constexpr int kGradThreads = 256;  // columns of a workgroup
-constexpr int kGradLdsFloats = 8192;  // dY staging: rows per pass = min(64, 8192 / G)
-constexpr int kGradKB = 8;         // kept slots accumulated per pass over the rows
+constexpr int kGradThreads = 256;     // columns of a workgroup
+constexpr int kGradLdsFloats = 8192;  // dY staging (32 KiB): rows per pass = min(32, 8192 / (GB * G))
 
 template <typename T> __device__ __forceinline__ float ld(const T* p, int64_t i);
 template <> __device__ __forceinline__ float ld<float>(const float* p, int64_t i) { return p[i]; }
 template <> __device__ __forceinline__ float ld<bf16_t>(const bf16_t* p, int64_t i) { return bf16_to_f32(p[i].bits); }
 
-// Slots k0 .. k0 + KB - 1 of group g for this workgroup's columns (those
-// past K are skipped); dYs is the LDS staging area, R x G floats.
-template <typename T, int KB>
-__device__ __forceinline__ void grad_pass(const T* __restrict__ dY, const T* __restrict__ X,
-                                          const uint8_t* __restrict__ idx, float* __restrict__ dv, int64_t N, int64_t C,
-                                          int64_t O, int32_t G, int32_t K, int64_t g, int64_t c, int32_t k0, int32_t R,
-                                          float* dYs) {
-  const bool live = c < C;
-  int r[KB];
-  float acc[KB];
-#pragma unroll
-  for (int k = 0; k < KB; ++k) {
-    const int ix = (live && k0 + k < K) ? idx[(g * K + k0 + k) * C + c] : 0;
-    r[k] = ix < G ? ix : G - 1;  // (a packing from cci_pack always has idx < G)
-    acc[k] = 0.0f;
-  }
-  for (int64_t n0 = 0; n0 < N; n0 += R) {
-    const int rows = static_cast<int>(N - n0 < R ? N - n0 : R);
-    __syncthreads();  // the previous pass's readers are done with dYs
-    for (int t = threadIdx.x; t < rows * G; t += kGradThreads) {
-      const int n = t / G, q = t - n * G;
-      dYs[t] = ld<T>(dY, (n0 + n) * O + g * G + q);
-    }
-    __syncthreads();
-    if (live) {
-      for (int n = 0; n < rows; ++n) {
-        const float x = ld<T>(X, (n0 + n) * C + c);
-        const float* row = dYs + n * G;
-#pragma unroll
-        for (int k = 0; k < KB; ++k) acc[k] = __builtin_fmaf(row[r[k]], x, acc[k]);
-      }
-    }
-  }
-  if (live) {
-#pragma unroll
-    for (int k = 0; k < KB; ++k)
-      if (k0 + k < K) dv[(g * K + k0 + k) * C + c] = acc[k];
-  }
-}
-
-template <typename T, int KB>
+template <typename T, int GB, int KB>
 __global__ __launch_bounds__(kGradThreads) void grad_packed_kernel(const T* __restrict__ dY, const T* __restrict__ X,
                                                                    const uint8_t* __restrict__ idx,
                                                                    float* __restrict__ dv, int64_t N, int64_t C,
                                                                    int64_t O, int32_t G, int32_t K, int64_t cblocks,
                                                                    int32_t R) {
-  extern __shared__ __attribute__((aligned(16))) float dYs[];
-  const int64_t g = blockIdx.x / cblocks;
+  extern __shared__ __attribute__((aligned(16))) float lds_f[];
+  float* Xs = lds_f;                       // R rows x 256 columns of X
+  float* dYs = lds_f + R * kGradThreads;   // R rows x (GB * G) outputs of dY
+  const int64_t ngroups = O / G;
+  const int64_t g0 = (blockIdx.x / cblocks) * GB;
+  const int32_t gcount = static_cast<int32_t>(ngroups - g0 < GB ? ngroups - g0 : GB);
   const int64_t c = (blockIdx.x % cblocks) * kGradThreads + threadIdx.x;
-  for (int32_t k0 = 0; k0 < K; k0 += KB) grad_pass<T, KB>(dY, X, idx, dv, N, C, O, G, K, g, c, k0, R, dYs);
+  const bool live = c < C;
+  const int32_t width = gcount * G;  // dY columns staged per row
+  for (int32_t k0 = 0; k0 < K; k0 += KB) {
+    int off[GB][KB];  // LDS offset of the entry each slot gathers, inside a staged row
+    float acc[GB][KB];
+#pragma unroll
+    for (int gi = 0; gi < GB; ++gi)
+#pragma unroll
+      for (int k = 0; k < KB; ++k) {
+        const bool on = live && gi < gcount && k0 + k < K;
+        const int ix = on ? idx[((g0 + gi) * K + k0 + k) * C + c] : 0;
+        off[gi][k] = gi * G + (ix < G ? ix : G - 1);  // (a packing from cci_pack always has idx < G)
+        acc[gi][k] = 0.0f;
+      }
+    for (int64_t n0 = 0; n0 < N; n0 += R) {
+      const int rows = static_cast<int>(N - n0 < R ? N - n0 : R);
+      __syncthreads();  // the previous pass's readers are done with dYs / Xs
+      // stage the pass's dY rows (restricted to the groups) and X rows
+      // (restricted to the columns): every load in flight at once
+      for (int t = threadIdx.x; t < rows * width; t += kGradThreads) {
+        const int n = t / width, q = t - n * width;
+        dYs[t] = ld<T>(dY, (n0 + n) * O + g0 * G + q);
+      }
+      for (int n = 0; n < rows; ++n) Xs[n * kGradThreads + threadIdx.x] = live ? ld<T>(X, (n0 + n) * C + c) : 0.0f;
+      __syncthreads();
+      if (live) {
+        for (int n = 0; n < rows; ++n) {
+          const float x = Xs[n * kGradThreads + threadIdx.x];
+          const float* row = dYs + n * width;
+#pragma unroll
+          for (int gi = 0; gi < GB; ++gi)
+#pragma unroll
+            for (int k = 0; k < KB; ++k) acc[gi][k] = __builtin_fmaf(row[off[gi][k]], x, acc[gi][k]);
+        }
+      }
+    }
+    if (live) {
+#pragma unroll
+      for (int gi = 0; gi < GB; ++gi)
+#pragma unroll
+        for (int k = 0; k < KB; ++k)
+          if (gi < gcount && k0 + k < K) dv[((g0 + gi) * K + k0 + k) * C + c] = acc[gi][k];
+    }
+  }
+}
+
+template <typename T, int GB, int KB>
+hipError_t grad_launch(const T* dY, const T* X, int64_t N, int64_t C, const uint8_t* idx, int64_t O, int32_t G,
+                       int32_t K, float* dv, hipStream_t s) {
+  const int64_t cblocks = (C + kGradThreads - 1) / kGradThreads;
+  const int64_t gblocks = (O / G + GB - 1) / GB;
+  const dim3 grid(static_cast<uint32_t>(gblocks * cblocks));
+  const int32_t R = static_cast<int32_t>(std::max<int64_t>(1, std::min<int64_t>(32, kGradLdsFloats / (GB * G))));
+  const size_t lds = static_cast<size_t>(R) * (GB * G + kGradThreads) * sizeof(float);
+  hipLaunchKernelGGL((grad_packed_kernel<T, GB, KB>), grid, dim3(kGradThreads), lds, s, dY, X, idx, dv, N, C, O, G, K,
+                     cblocks, R);
+  return hipGetLastError();
 }
 
 template <typename T>
 hipError_t grad_typed(const T* dY, const T* X, int64_t N, int64_t C, const uint8_t* idx, int64_t O, int32_t G,
                       int32_t K, float* dv, hipStream_t s) {
-  const int64_t cblocks = (C + kGradThreads - 1) / kGradThreads;
-  const dim3 grid(static_cast<uint32_t>((O / G) * cblocks));
-  const int32_t R = G >= kGradLdsFloats / 64 ? kGradLdsFloats / G : 64;
-  const size_t lds = static_cast<size_t>(R) * G * sizeof(float);
-  if (K == 1)
-    hipLaunchKernelGGL((grad_packed_kernel<T, 1>), grid, dim3(kGradThreads), lds, s, dY, X, idx, dv, N, C, O, G, K, cblocks, R);
-  else if (K == 2)
-    hipLaunchKernelGGL((grad_packed_kernel<T, 2>), grid, dim3(kGradThreads), lds, s, dY, X, idx, dv, N, C, O, G, K, cblocks, R);
-  else if (K <= 4)
-    hipLaunchKernelGGL((grad_packed_kernel<T, 4>), grid, dim3(kGradThreads), lds, s, dY, X, idx, dv, N, C, O, G, K, cblocks, R);
-  else
-    hipLaunchKernelGGL((grad_packed_kernel<T, kGradKB>), grid, dim3(kGradThreads), lds, s, dY, X, idx, dv, N, C, O, G,
-                       K, cblocks, R);
-  return hipGetLastError();
+  // four groups per workgroup (X read once per four groups; enough
+  // workgroups to fill the chip), up to eight slots of each per pass
+  if (K == 1) return grad_launch<T, 4, 1>(dY, X, N, C, idx, O, G, K, dv, s);
+  if (K == 2) return grad_launch<T, 4, 2>(dY, X, N, C, idx, O, G, K, dv, s);
+  if (K <= 4) return grad_launch<T, 4, 4>(dY, X, N, C, idx, O, G, K, dv, s);
+  return grad_launch<T, 4, 8>(dY, X, N, C, idx, O, G, K, dv, s);
 }
 
 }  // namespace

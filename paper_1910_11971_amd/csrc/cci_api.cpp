@@ -30,6 +30,14 @@ cci_status ok() {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// B * H * W * C < lim, checked without overflow (B >= 0; H, W, C >= 1).
+bool fits_nhwc(int64_t B, int64_t H, int64_t W, int64_t C, int64_t lim) {
+  if (W > lim || H > lim / W) return false;  // H * W <= lim
+  const int64_t hw = H * W;
+  if (C > lim / hw) return false;            // H * W * C <= lim
+  return B <= (lim - 1) / (hw * C);          // B * H * W * C <= lim - 1
+}
+
 bool dtype_ok(cci_dtype t) { return t == CCI_F32 || t == CCI_BF16; }
 
 cci::DType to_dt(cci_dtype t) { return t == CCI_F32 ? cci::DType::F32 : cci::DType::BF16; }
@@ -268,8 +276,8 @@ cci_status cci_conv_im2col_algo(const void* X, cci_dtype x_t, int64_t B, int64_t
   if (cci_status s = check_types(x_t, val_t, y_t)) return s;
   const int64_t Ho = (H + 2 * pad_h - KH) / stride_h + 1;
   const int64_t Wo = (W + 2 * pad_w - KW) / stride_w + 1;
-  const int64_t N = B * Ho * Wo;
-  if (B * H * W * Cin >= (int64_t(1) << 31)) return fail(CCI_EINVAL, "input tensor too large");
+  if (!fits_nhwc(B, H, W, Cin, int64_t(1) << 31)) return fail(CCI_EINVAL, "input tensor too large");
+  const int64_t N = B * Ho * Wo;  // B * H * W < 2^31 and Ho, Wo <= H, W + 128: no overflow
   if (N > (int64_t(1) << 40) / (C > O ? C : O)) return fail(CCI_EINVAL, "output too large");
   if (N > 0 && (!X || !vals || !idx || !Y)) return fail(CCI_EINVAL, "null pointer");
   if (N > 0 && (!aligned16(X) || !aligned16(vals) || !aligned16(idx) || !aligned16(Y)))
@@ -355,7 +363,7 @@ cci_status cci_spmm_2of4(const void* X, cci_dtype x_t, int64_t N, int64_t R, con
                          void* stream) {
   if (!dtype_ok(x_t) || !dtype_ok(y_t)) return fail(CCI_EINVAL, "unknown dtype code");
   if (x_t != CCI_BF16) return fail(CCI_EUNSUPPORTED, "the 2:4 product takes bf16 X");
-  if (N < 0) return fail(CCI_EINVAL, "N=%lld < 0", (long long)N);
+  if (N < 0 || N >= (int64_t(1) << 31)) return fail(CCI_EINVAL, "N=%lld outside [0, 2^31)", (long long)N);
   if (cci_status s = check_2of4(M, R)) return s;
   if (!cci::spmm_2of4_fits(N, R, M, to_dt(y_t))) return fail(CCI_EINVAL, "product too large");
   const float* scale = ep ? ep->scale : nullptr;
@@ -474,7 +482,7 @@ cci_status cci_maxpool2d_nhwc(const void* X, cci_dtype t, int64_t B, int64_t H, 
   if (B < 0 || H < 1 || W < 1 || C < 1 || k < 1 || s < 1 || p < 0 || 2 * p > k ||
       H + 2 * p < k || W + 2 * p < k)
     return fail(CCI_EINVAL, "bad pooling geometry");
-  if (B * H * W * C >= (int64_t(1) << 40)) return fail(CCI_EINVAL, "tensor too large");
+  if (!fits_nhwc(B, H, W, C, int64_t(1) << 40)) return fail(CCI_EINVAL, "tensor too large");
   if (B == 0) return ok();
   if (!X || !Y) return fail(CCI_EINVAL, "null pointer");
   if (!aligned16(X) || !aligned16(Y)) return fail(CCI_EALIGN, "pointer not 16-byte aligned");
@@ -488,7 +496,7 @@ cci_status cci_global_avgpool_nhwc(const void* X, cci_dtype x_t, int64_t B, int6
                                    int64_t C, void* Y, cci_dtype y_t, void* stream) {
   if (!dtype_ok(x_t) || !dtype_ok(y_t)) return fail(CCI_EINVAL, "unknown dtype code");
   if (B < 0 || H < 1 || W < 1 || C < 1) return fail(CCI_EINVAL, "bad pooling geometry");
-  if (B * H * W * C >= (int64_t(1) << 40)) return fail(CCI_EINVAL, "tensor too large");
+  if (!fits_nhwc(B, H, W, C, int64_t(1) << 40)) return fail(CCI_EINVAL, "tensor too large");
   if (B == 0) return ok();
   if (!X || !Y) return fail(CCI_EINVAL, "null pointer");
   if (!aligned16(X) || !aligned16(Y)) return fail(CCI_EALIGN, "pointer not 16-byte aligned");

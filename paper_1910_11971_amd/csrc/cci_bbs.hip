@@ -28,6 +28,7 @@
 // a k-step of 256 rows with 16 + 2 contiguous 1 KiB copies.
 #include <type_traits>
 
+#include "cci_device.hpp"
 #include "cci_launch.hpp"
 
 namespace cci {

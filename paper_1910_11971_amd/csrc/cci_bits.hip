@@ -24,6 +24,7 @@
 #include <algorithm>
 #include <type_traits>
 
+#include "cci_device.hpp"
 #include "cci_launch.hpp"
 
 namespace cci {

@@ -33,6 +33,7 @@
 // convolutions, any stride) stages one input pixel per output pixel.
 // Workgroup ids are mapped so that the output blocks of one pixel range sit
 // on the same XCD (they read the same activations through its L2).
+#include "cci_device.hpp"
 #include "cci_launch.hpp"
 
 namespace cci {

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "cci_types.hpp"
+
 namespace cci {
 
 // bf16 is carried as its raw 16-bit pattern; arithmetic happens in fp32.
@@ -56,12 +58,5 @@ __device__ __forceinline__ float apply_epilogue(float acc, int64_t o, int64_t yo
   if (ep.relu) y = y > 0.0f ? y : (y != y ? y : 0.0f);
   return y;
 }
-
-// Geometry of the GEMM operand A: row n of A is sample n (FC) or output
-// pixel n of an NHWC convolution read through implicit im2col, with column
-// c = (kh*KW + kw)*Cin + cin.
-struct ConvGeom {
-  int32_t H, W, Cin, KH, KW, sh, sw, ph, pw, Ho, Wo;
-};
 
 }  // namespace cci

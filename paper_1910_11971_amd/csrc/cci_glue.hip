@@ -3,6 +3,7 @@
 // consecutive channels (coalesced): bf16 max pooling with C % 8 == 0 gives a
 // lane 8 channels of one output pixel (16-byte reads and writes, 32-bit
 // index arithmetic); otherwise one lane per output element.
+#include "cci_device.hpp"
 #include "cci_launch.hpp"
 
 namespace cci {

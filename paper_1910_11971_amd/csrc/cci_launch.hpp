@@ -8,7 +8,7 @@
 
 #include <atomic>
 
-#include "cci_device.hpp"
+#include "cci_types.hpp"
 
 namespace cci {
 

@@ -31,6 +31,7 @@
 // the packed weights are read once per wave and every output is written
 // once.  The layers this serves are bound by HBM bandwidth: their MFMA work
 // is small next to their bytes.
+#include "cci_device.hpp"
 #include "cci_launch.hpp"
 
 namespace cci {

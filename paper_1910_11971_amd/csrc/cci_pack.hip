@@ -5,6 +5,7 @@
 // consecutive columns, so each of the G row reads is coalesced), ranks them by
 // |w| and writes the K survivors (value + intra-group row) in ascending row
 // order -- again coalesced along c.
+#include "cci_device.hpp"
 #include "cci_launch.hpp"
 
 namespace cci {

@@ -18,6 +18,7 @@
 //     broadcasts instead of dependent global loads.
 //
 // General path: any dtype combination, any C, conv through implicit im2col.
+#include "cci_device.hpp"
 #include "cci_launch.hpp"
 
 namespace cci {

@@ -19,6 +19,7 @@
 #include <algorithm>
 #include <type_traits>
 
+#include "cci_device.hpp"
 #include "cci_launch.hpp"
 
 namespace cci {

@@ -36,6 +36,7 @@
 //     reads is its 16 contiguous bytes at lane * 16.
 #include <type_traits>
 
+#include "cci_device.hpp"
 #include "cci_launch.hpp"
 
 namespace cci {

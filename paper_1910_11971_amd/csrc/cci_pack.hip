@@ -4,7 +4,7 @@
 // HBM-bound: reads the G weights of its group column (consecutive lanes read
 // consecutive columns, so each of the G row reads is coalesced), ranks them by
 // |w| and writes the K survivors (value + intra-group row) in ascending row
-// order -- again coalesced along c.
+// order, one coalesced store per slot.
 #include "cci_device.hpp"
 #include "cci_launch.hpp"
 
@@ -21,7 +21,13 @@ template <> __device__ __forceinline__ void put<bf16_t>(bf16_t* p, int64_t i, fl
   p[i].bits = f32_to_bf16_rne(w);
 }
 
-// Register-resident group (G known at compile time): O(G^2) rank counting.
+// Register-resident group (G known at compile time).  The rank of row r is
+// the number of rows that beat it (larger |w|, or equal |w| and a lower
+// row); each pair of rows is compared once and credits one of the two.
+// The kept rows form a bit mask; slot k then takes the k-th lowest kept row,
+// so each slot is one store of consecutive columns (coalesced), its value
+// re-read from the cache lines just loaded.  With K = G every row is kept in
+// order (the dense control): a copy.
 template <int G, typename VT>
 __global__ __launch_bounds__(kPackThreads) void pack_fixed(const float* __restrict__ W, int64_t C,
                                                            int64_t cblocks, int32_t K,
@@ -31,26 +37,40 @@ __global__ __launch_bounds__(kPackThreads) void pack_fixed(const float* __restri
   const int64_t g = blk / cblocks;
   const int64_t c = (blk % cblocks) * kPackThreads + threadIdx.x;
   if (c >= C) return;
-  float w[G];
-  uint32_t key[G];
+  const float* col = W + g * G * C + c;
+  if (K == G) {
 #pragma unroll
-  for (int r = 0; r < G; ++r) {
-    w[r] = W[(g * G + r) * C + c];
-    key[r] = abs_bits(w[r]);
-  }
-  int slot = 0;
-#pragma unroll
-  for (int r = 0; r < G; ++r) {
-    int rank = 0;
-#pragma unroll
-    for (int q = 0; q < G; ++q)
-      rank += (key[q] > key[r]) || (key[q] == key[r] && q < r);
-    if (rank < K) {
-      const int64_t o = (g * K + slot) * C + c;
-      put<VT>(vals, o, w[r]);
+    for (int r = 0; r < G; ++r) {
+      const int64_t o = (g * K + r) * C + c;
+      put<VT>(vals, o, col[r * C]);
       idx[o] = static_cast<uint8_t>(r);
-      ++slot;
     }
+    return;
+  }
+  uint32_t key[G];
+  int rank[G];
+#pragma unroll
+  for (int r = 0; r < G; ++r) {
+    key[r] = abs_bits(col[r * C]);
+    rank[r] = 0;
+  }
+#pragma unroll
+  for (int r = 1; r < G; ++r)
+#pragma unroll
+    for (int q = 0; q < r; ++q) {
+      const bool q_wins = key[q] >= key[r];  // q < r: a tie goes to q
+      rank[r] += q_wins ? 1 : 0;
+      rank[q] += q_wins ? 0 : 1;
+    }
+  uint32_t kept = 0;
+#pragma unroll
+  for (int r = 0; r < G; ++r) kept |= (rank[r] < K ? 1u : 0u) << r;
+  for (int32_t k = 0; k < K; ++k) {
+    const int r = __builtin_ctz(kept);
+    kept &= kept - 1u;
+    const int64_t o = (g * K + k) * C + c;
+    put<VT>(vals, o, col[static_cast<int64_t>(r) * C]);
+    idx[o] = static_cast<uint8_t>(r);
   }
 }
 

@@ -39,6 +39,7 @@ typedef __bf16 bf16x16_t __attribute__((ext_vector_type(16)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef uint16_t u16x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void_t;
 
 constexpr uint32_t kOOB = 0x80000000u;   // buffer offset that reads as zero
@@ -239,7 +240,8 @@ __global__ __launch_bounds__(256) void cci_t_to_24_kernel(const uint16_t* __rest
 // k-step, 128 fp32 accumulators per lane.  Each k-step's operands (A: 16 KiB
 // of values, 2 KiB of indices; X: 256 rows x 128 B) are DMA'd into one of
 // three LDS stages two k-steps ahead (buffer_load ... lds, 16 B per lane);
-// one barrier per k-step.
+// one barrier per k-step.  A bf16 output tile leaves through LDS as whole
+// row segments.
 //
 // X stage layout: row r at r * 128, its 16-byte unit u (channels 8u .. 8u+7
 // of the k-step) at (u ^ ((r >> 1) & 7)) * 16: a DMA instruction reads 8
@@ -255,6 +257,7 @@ constexpr int kS4X = kS4Tile * 128;                    // X rows of a stage
 constexpr int kS4Stage = kS4AV + kS4AI + kS4X;         // 51200
 constexpr int kS4Lds = 3 * kS4Stage;                   // 153600
 static_assert(kS4Lds <= 160 * 1024, "LDS budget");
+static_assert(8 * 64 * 272 <= kS4Lds, "the output staging reuses the operand stages");
 
 struct S4Params {
   const uint16_t* X;
@@ -402,8 +405,14 @@ __global__ __launch_bounds__(kS4Threads) void spmm24_kernel(S4Params p) {
   }
 
   // ---- epilogue: lane holds rows 4 (lane / 16) .. +3 of A (outputs) for X
-  // row lane % 16 of each 16 x 16 block --------------------------------------
+  // row lane % 16 of each 16 x 16 block.  Scale, bias, residual and ReLU in
+  // fp32, one rounding.  A bf16 result is staged per wave in LDS (64 X rows x
+  // 128 outputs, rows padded to 272 B) and written back as whole 256-byte row
+  // segments; fp32 results are stored from the registers.
   const bool yf32 = std::is_same<YT, float>::value;
+  constexpr int kStPitch = 272;
+  uint8_t* stg = lds + w * (64 * kStPitch);
+  if (!yf32) lds_barrier();  // every wave is done with the operand stages
 #pragma unroll
   for (int a = 0; a < 8; ++a) {
     const int32_t mbase = m0 + 16 * (8 * wm + a);
@@ -414,13 +423,13 @@ __global__ __launch_bounds__(kS4Threads) void spmm24_kernel(S4Params p) {
     if (p.bias) bs = *reinterpret_cast<const f32x4_t*>(p.bias + m);
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      const int32_t n = n0 + 64 * wn + 16 * t + (lane & 15);
-      if (n >= p.N) continue;
+      const int32_t nl = 16 * t + (lane & 15);
+      const int32_t n = n0 + 64 * wn + nl;
       const int64_t yo = static_cast<int64_t>(n) * p.M + m;
       float y[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) y[r] = acc[a][t][r] * sc[r] + bs[r];
-      if (p.residual) {
+      if (p.residual && n < p.N) {
         if (yf32) {
           const f32x4_t rv = *reinterpret_cast<const f32x4_t*>(static_cast<const float*>(p.residual) + yo);
 #pragma unroll
@@ -436,11 +445,23 @@ __global__ __launch_bounds__(kS4Threads) void spmm24_kernel(S4Params p) {
         for (int r = 0; r < 4; ++r) y[r] = y[r] > 0.0f ? y[r] : (y[r] != y[r] ? y[r] : 0.0f);
       }
       if (yf32) {
-        *reinterpret_cast<f32x4_t*>(static_cast<float*>(p.Y) + yo) = f32x4_t{y[0], y[1], y[2], y[3]};
+        if (n < p.N) *reinterpret_cast<f32x4_t*>(static_cast<float*>(p.Y) + yo) = f32x4_t{y[0], y[1], y[2], y[3]};
       } else {
-        *reinterpret_cast<u16x4_t*>(static_cast<uint16_t*>(p.Y) + yo) =
+        *reinterpret_cast<u16x4_t*>(stg + nl * kStPitch + (16 * a + 4 * (lane >> 4)) * 2) =
             u16x4_t{f32_to_bf16_rne(y[0]), f32_to_bf16_rne(y[1]), f32_to_bf16_rne(y[2]), f32_to_bf16_rne(y[3])};
       }
+    }
+  }
+  if (!yf32) {
+    // (each wave reads back only what it wrote: program order suffices)
+    const int32_t mw = m0 + 128 * wm + 8 * (lane & 15);  // this lane's 8 outputs
+#pragma unroll
+    for (int rr = 0; rr < 16; ++rr) {
+      const int32_t nl = 4 * rr + (lane >> 4);
+      const int32_t n = n0 + 64 * wn + nl;
+      const u32x4_t v = *reinterpret_cast<const u32x4_t*>(stg + nl * kStPitch + (lane & 15) * 16);
+      if (n < p.N && mw < p.M)
+        *reinterpret_cast<u32x4_t*>(static_cast<uint16_t*>(p.Y) + static_cast<int64_t>(n) * p.M + mw) = v;
     }
   }
 }

@@ -84,13 +84,22 @@ typedef enum { CCI_F32 = 0, CCI_BF16 = 1 } cci_dtype;
  *                           KH*KW*Cin), C % 8 == 0, O % 4 == 0, G <= 256;
  *                           X and vals 16-byte aligned, idx 8-byte aligned,
  *                           Y (and residual) 8-byte aligned for bf16 and
- *                           16-byte aligned for fp32 output. */
+ *                           16-byte aligned for fp32 output.
+ *  CCI_ALGO_RESIDENT_MFMA   the same expansion for small k x k
+ *                           convolutions: the whole expanded tile is kept in
+ *                           registers for the launch and each workgroup
+ *                           stages the input rows under its band of output
+ *                           rows in LDS once.  3x3 convolutions with unit
+ *                           stride and padding 0..2, Cin 32 or 64, O 32 or
+ *                           64, bf16 X and vals, O/G*K*C/8 <= 5120; X, vals
+ *                           and Y 16-byte aligned, idx 8-byte aligned. */
 typedef enum {
   CCI_ALGO_AUTO = 0,
   CCI_ALGO_SPARSE_MAC = 1,
   CCI_ALGO_DENSE_TILE_MFMA = 2,
   CCI_ALGO_WIDE_TILE_MFMA = 3,
-  CCI_ALGO_NARROW_MFMA = 4
+  CCI_ALGO_NARROW_MFMA = 4,
+  CCI_ALGO_RESIDENT_MFMA = 5
 } cci_algo;
 
 /* Optional fused epilogue, applied per output element before rounding:
@@ -176,7 +185,9 @@ cci_status cci_conv_im2col_algo(const void *X, cci_dtype x_t, int64_t B,
  * 1x1 convolution reported as CCI_ALGO_WIDE_TILE_MFMA runs on the dense-tile
  * kernels when its stride or padding rules the wide-tile ones out; one
  * reported as CCI_ALGO_NARROW_MFMA then runs on the dense-tile kernels if
- * they take its shape, else on the sparse-MAC ones. */
+ * they take its shape, else on the sparse-MAC ones; one reported as
+ * CCI_ALGO_RESIDENT_MFMA runs on the dense-tile kernels when its stride is
+ * not 1 (or another of that family's limits rules it out). */
 cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C,
                        int64_t cin, int64_t O, int32_t G, int32_t K);
 

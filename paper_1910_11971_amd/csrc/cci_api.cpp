@@ -77,7 +77,7 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
       (a.residual && !aligned16(a.residual)))
     return fail(CCI_EALIGN, "epilogue pointer not 16-byte aligned");
   if (algo != CCI_ALGO_AUTO && algo != CCI_ALGO_SPARSE_MAC && algo != CCI_ALGO_DENSE_TILE_MFMA &&
-      algo != CCI_ALGO_WIDE_TILE_MFMA && algo != CCI_ALGO_NARROW_MFMA)
+      algo != CCI_ALGO_WIDE_TILE_MFMA && algo != CCI_ALGO_NARROW_MFMA && algo != CCI_ALGO_RESIDENT_MFMA)
     return fail(CCI_EINVAL, "unknown algo %d", (int)algo);
   if (a.N == 0) return ok();
 
@@ -91,6 +91,8 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
                            a.G, a.K);
   }
   // (the shape-only choice cannot see stride and padding)
+  if (algo == CCI_ALGO_AUTO && chosen == CCI_ALGO_RESIDENT_MFMA && !cci::resident_supports(a))
+    chosen = tile_ok ? CCI_ALGO_DENSE_TILE_MFMA : CCI_ALGO_SPARSE_MAC;
   if (algo == CCI_ALGO_AUTO && chosen == CCI_ALGO_WIDE_TILE_MFMA && !cci::wide_tile_supports(a))
     chosen = CCI_ALGO_DENSE_TILE_MFMA;
   if (algo == CCI_ALGO_AUTO && chosen == CCI_ALGO_NARROW_MFMA && !cci::narrow_supports(a))
@@ -104,6 +106,10 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
     return fail(CCI_EUNSUPPORTED,
                 "wide-tile MFMA kernels need bf16 X/vals, an FC or stride-1 unpadded 1x1 product, "
                 "C %% 64 == 0, O %% 256 == 0, 64 %% G == 0 and aligned pointers");
+  if (chosen == CCI_ALGO_RESIDENT_MFMA && !cci::resident_supports(a))
+    return fail(CCI_EUNSUPPORTED,
+                "resident MFMA kernels need bf16 X/vals, a 3x3 convolution with unit stride and padding "
+                "below 3, Cin 32 or 64, O 32 or 64, aligned pointers and at most 5120 packed 8-column units");
   if (chosen == CCI_ALGO_NARROW_MFMA && !cci::narrow_supports(a))
     return fail(CCI_EUNSUPPORTED,
                 "narrow MFMA kernels need bf16 X/vals, C <= 256, C %% 8 == 0, O %% 4 == 0, G <= 256, "
@@ -112,6 +118,7 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
   const hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = chosen == CCI_ALGO_SPARSE_MAC       ? cci::launch_sparse_mac(a, st)
                  : chosen == CCI_ALGO_WIDE_TILE_MFMA ? cci::launch_wide_tile(a, st)
+                 : chosen == CCI_ALGO_RESIDENT_MFMA  ? cci::launch_resident(a, st)
                  : chosen == CCI_ALGO_NARROW_MFMA    ? cci::launch_narrow(a, st)
                                                      : cci::launch_dense_tile(a, st);
   if (e != hipSuccess) return fail(CCI_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
@@ -213,6 +220,14 @@ cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C, int
   // a 12544 x 1024 x 256 one (98 tiles of 128 pixels), slower on the short
   // reductions of ResNet-50's other 1x1 layers.
   const bool bf = x_t == CCI_BF16 && val_t == CCI_BF16 && G >= 1 && 64 % G == 0;
+  // 3x3 convolutions over 32 or 64 channels into 32 or 64 outputs: their
+  // whole expanded tile fits in registers, so it is expanded once per
+  // workgroup and only activations stream (measured 2-3x the dense-tile
+  // kernel on a 32 x 56 x 56 x 64 -> 64 layer).  Only unit stride is taken:
+  // other strides run on the dense-tile kernels.
+  if (x_t == CCI_BF16 && val_t == CCI_BF16 && (cin == 32 || cin == 64) && C == 9 * cin && (O == 32 || O == 64) &&
+      O % G == 0)
+    return CCI_ALGO_RESIDENT_MFMA;
   const bool mac_g = G == 2 || G == 4 || G == 8 || G == 16 || G == 32;
   const int64_t tiles = (N + 127) / 128 * (O / 256);
   if (bf && C == cin && C % 64 == 0 && C >= 512 && O % 256 == 0 && tiles >= 96) return CCI_ALGO_WIDE_TILE_MFMA;

@@ -81,6 +81,13 @@ hipError_t launch_wide_tile(const ProductArgs& a, hipStream_t s);
 bool narrow_supports(const ProductArgs& a);
 hipError_t launch_narrow(const ProductArgs& a, hipStream_t s);
 
+// k x k convolutions with unit stride and few outputs (3x3, Cin 32 or 64, O 32
+// or 64; bf16): the expanded weights stay in registers for the whole launch,
+// and each workgroup stages the input rows under its band of output rows in
+// LDS once.
+bool resident_supports(const ProductArgs& a);
+hipError_t launch_resident(const ProductArgs& a, hipStream_t s);
+
 // Balanced sparsity (groups of G inputs in one output row) and the 2:4
 // sparse matrix-core product.
 hipError_t launch_bbs_pack(const float* W, int64_t O, int64_t C, int32_t G, int32_t K, void* vals, DType val_t,

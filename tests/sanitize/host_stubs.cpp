@@ -22,6 +22,11 @@ bool wide_tile_supports(const ProductArgs& a) { return a.x_t == DType::BF16 && a
 hipError_t launch_wide_tile(const ProductArgs&, hipStream_t) { ++g_launches; return hipSuccess; }
 bool narrow_supports(const ProductArgs& a) { return a.x_t == DType::BF16 && a.C <= 256 && a.C % 8 == 0; }
 hipError_t launch_narrow(const ProductArgs&, hipStream_t) { ++g_launches; return hipSuccess; }
+bool resident_supports(const ProductArgs& a) {
+  return a.conv && a.x_t == DType::BF16 && a.geom.KH == 3 && a.geom.KW == 3 && a.geom.sh == 1 && a.geom.sw == 1 &&
+         (a.geom.Cin == 32 || a.geom.Cin == 64) && (a.O == 32 || a.O == 64);
+}
+hipError_t launch_resident(const ProductArgs&, hipStream_t) { ++g_launches; return hipSuccess; }
 hipError_t launch_bbs_pack(const float*, int64_t, int64_t, int32_t, int32_t, void*, DType, uint8_t*, hipStream_t) {
   ++g_launches;
   return hipSuccess;

@@ -107,6 +107,24 @@ def test_narrow_algo_requirements():
                                    FAKE, 96, 8, 2, None, FAKE, cci.BF16, Nw, None) == cci.EUNSUPPORTED
 
 
+def test_resident_algo_requirements():
+    # resident MFMA: bf16 3x3 convolutions with unit stride, Cin 32 / 64, O 32 / 64; FC refused
+    Rs = cci.ALGO_RESIDENT_MFMA
+    assert lib.cci_spmm_algo(FAKE, cci.BF16, 4, 576, FAKE, cci.BF16, FAKE, 64, 8, 2, None, FAKE,
+                             cci.BF16, Rs, None) == cci.EUNSUPPORTED
+    for Cin, KH, st, O in [(64, 3, 2, 64), (96, 3, 1, 64), (64, 1, 1, 64), (64, 3, 1, 128), (64, 5, 1, 64),
+                           (16, 3, 1, 64)]:
+        assert lib.cci_conv_im2col_algo(FAKE, cci.BF16, 1, 8, 8, Cin, KH, KH, st, st, 1, 1, FAKE, cci.BF16,
+                                        FAKE, O, 8, 2, None, FAKE, cci.BF16, Rs, None) == cci.EUNSUPPORTED
+    assert lib.cci_conv_im2col_algo(FAKE, cci.F32, 1, 8, 8, 64, 3, 3, 1, 1, 1, 1, FAKE, cci.F32,
+                                    FAKE, 64, 8, 2, None, FAKE, cci.F32, Rs, None) == cci.EUNSUPPORTED
+    # misaligned idx (8-byte alignment needed) -- the plain 16-byte rule fires first
+    assert lib.cci_conv_im2col_algo(FAKE, cci.BF16, 1, 8, 8, 64, 3, 3, 1, 1, 1, 1, FAKE, cci.BF16,
+                                    FAKE_MIS, 64, 8, 2, None, FAKE, cci.BF16, Rs, None) == cci.EALIGN
+    # the shape-only choice names the family for 3x3 64 -> 64
+    assert lib.cci_auto_algo(cci.BF16, cci.BF16, 100352, 576, 64, 64, 8, 2) == Rs
+
+
 def test_algo_entry_points_match_plain_calls_on_validation():
     # the pinned-family calls validate exactly like the plain ones
     assert lib.cci_spmm_algo(FAKE, cci.BF16, 4, 64, FAKE, cci.BF16, FAKE, 12, 8, 2, None, FAKE,
@@ -138,8 +156,11 @@ def test_conv_geometry_errors():
 
 
 def test_auto_algo_cost_model():
-    # bf16, tile-friendly: expanded MFMA work wins while K/G > 1/32
-    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 100352, 576, 64, 64, 8, 2) == "dense_tile_mfma"
+    # bf16, tile-friendly: expanded MFMA work wins while K/G > 1/32; 3x3 convs over 32 / 64 channels into
+    # 32 / 64 outputs keep the whole expanded tile in registers
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 100352, 576, 64, 64, 8, 2) == "resident_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 100352, 288, 32, 32, 8, 2) == "resident_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 100352, 576, 64, 128, 8, 2) == "dense_tile_mfma"
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 4096, 4096, 4096, 512, 16, 1) == "dense_tile_mfma"
     # large FC / 1x1 products (>= 128 tiles of 256 x 256): wide-tile MFMA, any K
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 4096, 4096, 4096, 4096, 16, 1) == "wide_tile_mfma"

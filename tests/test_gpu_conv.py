@@ -118,6 +118,66 @@ def test_conv1x1_narrow(B, H, W, Cin, O, G, K):
     run_conv(X, rand_w(O, Cin, O), G, K, 1, 1, 0, torch.bfloat16, "narrow_mfma", ep=ep)
 
 
+RESIDENT_CASES = [  # B, H, W, Cin, O, pad, G, K
+    (2, 9, 11, 32, 64, 1, 8, 2),
+    (3, 14, 14, 64, 64, 1, 8, 2),
+    (1, 6, 5, 64, 32, 0, 4, 1),      # 32 outputs: eight pixel streams; no padding
+    (2, 17, 19, 32, 32, 2, 16, 5),   # padding 2
+    (5, 12, 23, 64, 64, 1, 64, 64),  # K = G (dense control): 4608 packed units
+    (3, 3, 3, 64, 64, 1, 32, 7),     # a 3x3 image: one band of 3 rows
+    (1, 5, 100, 64, 64, 1, 2, 1),    # 16 KiB staged rows
+    (2, 7, 120, 32, 64, 0, 4, 2),    # 16 KiB staged rows, 32 channels
+    (7, 31, 13, 32, 64, 1, 1, 1),    # G = 1
+    (9, 10, 10, 64, 64, 1, 8, 3),    # 18 bands: not a multiple of 8 (no XCD grouping)
+]
+
+
+@pytest.mark.parametrize("B,H,W,Cin,O,pad,G,K", RESIDENT_CASES)
+def test_conv_resident(B, H, W, Cin, O, pad, G, K):
+    """3x3 unit-stride convolutions on the register-resident kernels."""
+    need_gpu()
+    X = rand_x((B, H, W, Cin), torch.bfloat16, B + H + W + Cin)
+    run_conv(X, rand_w(O, 9 * Cin, O + G + K), G, K, 3, 1, pad, torch.bfloat16, "resident_mfma")
+
+
+@pytest.mark.parametrize("y_dtype", [torch.bfloat16, torch.float32])
+@pytest.mark.parametrize("O", [32, 64])
+def test_conv_resident_epilogue(y_dtype, O):
+    """scale, bias, residual and ReLU fused on the resident kernels, bf16 and fp32 output."""
+    need_gpu()
+    B, H, W, Cin = 3, 11, 13, 64
+    ep = rand_epilogue(O, B * H * W, y_dtype, O + 3, residual=True, relu=True)
+    run_conv(rand_x((B, H, W, Cin), torch.bfloat16, 41), rand_w(O, 9 * Cin, 42), 8, 2, 3, 1, 1, y_dtype,
+             "resident_mfma", ep=ep)
+    ep = rand_epilogue(O, B * H * W, y_dtype, O + 4, residual=False, relu=False)
+    run_conv(rand_x((B, H, W, Cin), torch.bfloat16, 43), rand_w(O, 9 * Cin, 44), 8, 2, 3, 1, 1, y_dtype,
+             "resident_mfma", ep=ep)
+
+
+def test_conv_resident_wide_rows_fall_back():
+    """Rows wider than 16 KiB of staged activations are refused by the resident family and run under AUTO."""
+    need_gpu()
+    from paper_1910_11971_amd import cci
+    X = rand_x((1, 4, 200, 64), torch.bfloat16, 61)
+    vals, idx = cci.pack(torch.from_numpy(rand_w(64, 576, 62)).to(DEV), 8, 2, torch.bfloat16)
+    with pytest.raises(cci.CCIError):
+        cci.conv_im2col(X.to(DEV), vals, idx, 8, 3, 3, (1, 1), (1, 1), algo="resident_mfma")
+    run_conv(X, rand_w(64, 576, 62), 8, 2, 3, 1, 1, torch.bfloat16, "auto")
+
+
+def test_conv_resident_is_auto_for_3x3_64():
+    from paper_1910_11971_amd import cci
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 100352, 576, 64, 64, 8, 2) == "resident_mfma"
+
+
+@pytest.mark.parametrize("stride", [2])
+def test_conv_resident_shape_falls_back(stride):
+    """A strided 3x3 64 -> 64 layer (not a resident shape) still runs under AUTO."""
+    need_gpu()
+    X = rand_x((2, 15, 15, 64), torch.bfloat16, 51)
+    run_conv(X, rand_w(64, 576, 52), 8, 2, 3, stride, 1, torch.bfloat16, "auto")
+
+
 @pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma"])
 def test_conv_epilogue_residual_relu(algo):
     need_gpu()

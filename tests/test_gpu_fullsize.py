@@ -59,7 +59,7 @@ def run_full(name, algo):
     check_close(got, Yref, Yabs, TOL["bf16"], f"{name} {algo} (all {wl.N * wl.O} outputs)")
 
 
-@pytest.mark.parametrize("algo", ["auto", "dense_tile_mfma", "sparse_mac"])
+@pytest.mark.parametrize("algo", ["auto", "resident_mfma", "dense_tile_mfma", "sparse_mac"])
 def test_conv3x3_every_output(algo):
     need_gpu()
     run_full("conv3x3", algo)

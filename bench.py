@@ -502,8 +502,9 @@ def td_compare(Xs, W, ncopy, stream, per_k):
     """Kernels of an improved-targeted-dropout step on the 4096^3 layer (G = 16):
     the candidate-dropout mask (HBM-bound: W and 32-bit random words read, W_eff
     bf16 and the keep mask written), and once the mask is fixed the gradient of
-    the packed values (N * nnz multiply-adds on the vector ALUs) next to the
-    dense weight gradient dY^T X on hipBLASLt.  dY is the rotated X."""
+    the packed values (bf16: the dense dY^T X tiles on the matrix cores, kept
+    entries written) next to the dense weight gradient dY^T X on hipBLASLt.
+    dY is the rotated X."""
     import torch
     from paper_1910_11971_amd import cci
     N, C = Xs[0].shape
@@ -530,7 +531,8 @@ def td_compare(Xs, W, ncopy, stream, per_k):
         flop = 2.0 * N * nnz
         alg_bytes = 2 * N * O + 2 * N * C + nnz * 5
         out[f"grad_packed_K{K}"] = {"us": round(t * 1e3, 3), "eff_TFLOPs": round(flop / (t * 1e-3) / 1e12, 2),
-                                    "roofline": roof_for("cci_grad_packed", flop, None, alg_bytes, t),
+                                    "kernel": "cci_grad_mfma",
+                                    "roofline": own_roof(flop, alg_bytes, t, dense_flop=2.0 * N * O * C),
                                     "speedup_vs_dense_dW": round(t_dw / t, 3)}
     out["note"] = ("re-projection = cci_pack (sweep_k pack_us); backward dX of the fixed-mask layer = "
                    "bbs_2of4 cci_backward_dX_us")
@@ -797,7 +799,7 @@ def roof_for(kname, flop, dense_flop, alg_bytes, t_ms):
     """The matrix-core kernels against the method's own work (own_roof); the
     vector-ALU kernel multiplies only kept weights, so its bound is the fp32
     FMA rate (or HBM, if that takes longer)."""
-    if kname in ("cci_dense_tile", "cci_wide_tile", "cci_narrow"):
+    if kname in ("cci_dense_tile", "cci_wide_tile", "cci_narrow", "cci_resident"):
         return own_roof(flop, alg_bytes, t_ms, dense_flop)
     t_alu = flop / (PEAK["valu_fp32_TFLOPs"] * 1e12)
     t_hbm = alg_bytes / (PEAK["hbm_GBps"] * 1e9)

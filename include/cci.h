@@ -291,9 +291,12 @@ cci_status cci_td_mask(const float *W, int64_t O, int64_t C, int32_t G,
 
 /* Gradient of the packed values of Y = X . W_hat^T (Alg. 1's product):
  *   dvals[g][k][c] = sum_n dY[n][gG + idx[g][k][c]] * X[n][c],
- * fp32 accumulation in n order.  dY: device [N][O], X: device [N][C], both
- * of dtype t (F32 or BF16); idx as from cci_pack; dvals: device fp32
- * [O/G][K][C].  Only kept weights are computed (N * nnz multiply-adds). */
+ * fp32 accumulation.  dY: device [N][O], X: device [N][C], both of dtype t
+ * (F32 or BF16); idx as from cci_pack; dvals: device fp32 [O/G][K][C].
+ * bf16 operands with N >= 32, O % 8 == 0, C % 8 == 0 and 128 % G == 0 run
+ * on the matrix cores (the dense tiles of dY^T X, summed over samples in
+ * steps of 32, kept entries written); other calls multiply only kept
+ * weights on the vector ALUs, summing in n order. */
 cci_status cci_grad_packed(const void *dY, const void *X, cci_dtype t,
                            int64_t N, int64_t C, const uint8_t *idx, int64_t O,
                            int32_t G, int32_t K, float *dvals, void *stream);

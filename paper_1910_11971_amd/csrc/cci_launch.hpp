@@ -109,6 +109,12 @@ hipError_t launch_td_mask(const float* W, int64_t O, int64_t C, int32_t G, int32
                           uint64_t thr, void* We, DType w_t, uint8_t* keep, hipStream_t s);
 hipError_t launch_grad_packed(const void* dY, const void* X, DType t, int64_t N, int64_t C, const uint8_t* idx,
                               int64_t O, int32_t G, int32_t K, float* dv, hipStream_t s);
+// The same gradient on the matrix cores (bf16 dY and X, O % 8 == 0,
+// C % 8 == 0, 128 % G == 0): dense 256 x 256 tiles of dY^T X, kept entries
+// gathered.
+bool grad_mfma_supports(const void* dY, const void* X, DType t, int64_t N, int64_t C, int64_t O, int32_t G);
+hipError_t launch_grad_mfma(const void* dY, const void* X, int64_t N, int64_t C, const uint8_t* idx, int64_t O,
+                            int32_t G, int32_t K, float* dv, hipStream_t s);
 
 // Plain log2(G)-bit index streams and the few-row product that reads them.
 int64_t index_stream_bytes(int64_t n, int32_t b);

@@ -10,6 +10,8 @@
 //
 // cci_grad_packed: gradient of the packed values once the mask is fixed,
 //   dvals[g][k][c] = sum_n dY[n][gG + idx[g][k][c]] * X[n][c].
+// (bf16 operands in the shapes it takes run on the matrix cores instead:
+// cci_grad.hip.  This kernel serves fp32, short reductions and other shapes.)
 // A workgroup owns four consecutive groups and 256 columns (a lane per
 // column, its indices in registers); per pass of up to 32 rows the rows of dY
 // restricted to those groups' outputs and of X restricted to the columns are
@@ -210,6 +212,8 @@ hipError_t launch_td_mask(const float* W, int64_t O, int64_t C, int32_t G, int32
 
 hipError_t launch_grad_packed(const void* dY, const void* X, DType t, int64_t N, int64_t C, const uint8_t* idx,
                               int64_t O, int32_t G, int32_t K, float* dv, hipStream_t s) {
+  // bf16 operands of at least one reduction step go to the matrix cores
+  if (N >= 32 && grad_mfma_supports(dY, X, t, N, C, O, G)) return launch_grad_mfma(dY, X, N, C, idx, O, G, K, dv, s);
   if (t == DType::F32)
     return grad_typed<float>(static_cast<const float*>(dY), static_cast<const float*>(X), N, C, idx, O, G, K, dv, s);
   return grad_typed<bf16_t>(static_cast<const bf16_t*>(dY), static_cast<const bf16_t*>(X), N, C, idx, O, G, K, dv, s);

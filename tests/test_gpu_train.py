@@ -93,6 +93,16 @@ def test_grad_packed_matches_oracle(N, O, C, G, K, dt):
     run_grad(N, O, C, G, K, dt, seed=N + C + K)
 
 
+@pytest.mark.parametrize("N,O,C,G,K", [(96, 264, 520, 8, 3), (33, 1024, 64, 128, 5), (200, 256, 256, 1, 1),
+                                       (64, 136, 8, 2, 2), (500, 64, 2056, 64, 64), (32, 512, 768, 16, 4),
+                                       (1000, 40, 24, 4, 1)])
+def test_grad_packed_matrix_cores(N, O, C, G, K):
+    """bf16 shapes the matrix-core kernel takes: ragged sample steps, partial 256 x 256 tiles, G from 1 to 128,
+    K = G (dense control)."""
+    need_gpu()
+    run_grad(N, O, C, G, K, torch.bfloat16, seed=N + O + C + K)
+
+
 @pytest.mark.parametrize("K", [1, 4])
 def test_grad_packed_fc4096_every_output(K):
     need_gpu()

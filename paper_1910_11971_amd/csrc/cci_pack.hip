@@ -23,7 +23,10 @@ template <> __device__ __forceinline__ void put<bf16_t>(bf16_t* p, int64_t i, fl
 
 // Register-resident group (G known at compile time).  The rank of row r is
 // the number of rows that beat it (larger |w|, or equal |w| and a lower
-// row); each pair of rows is compared once and credits one of the two.
+// row); each pair of rows is compared once and credits one of the two.  (For
+// K < (G - 1) / 2 the K winners are taken one at a time instead: the same
+// set, in fewer operations; the ranking is vector-ALU work comparable to
+// the kernel's HBM time.)
 // The kept rows form a bit mask; slot k then takes the k-th lowest kept row,
 // so each slot is one store of consecutive columns (coalesced), its value
 // re-read from the cache lines just loaded.  With K = G every row is kept in
@@ -48,23 +51,45 @@ __global__ __launch_bounds__(kPackThreads) void pack_fixed(const float* __restri
     return;
   }
   uint32_t key[G];
-  int rank[G];
 #pragma unroll
-  for (int r = 0; r < G; ++r) {
-    key[r] = abs_bits(col[r * C]);
-    rank[r] = 0;
-  }
-#pragma unroll
-  for (int r = 1; r < G; ++r)
-#pragma unroll
-    for (int q = 0; q < r; ++q) {
-      const bool q_wins = key[q] >= key[r];  // q < r: a tie goes to q
-      rank[r] += q_wins ? 1 : 0;
-      rank[q] += q_wins ? 0 : 1;
-    }
+  for (int r = 0; r < G; ++r) key[r] = abs_bits(col[r * C]);
   uint32_t kept = 0;
+  if (2 * K + 1 < G) {
+    // Few kept rows: take the largest remaining |w| K times (a strict
+    // comparison scanning up from row 0 keeps the lower row on a tie; a
+    // taken row's key drops below every |w|): 3 G K operations against the
+    // 3 G (G - 1) / 2 of the pairwise rank.
+    int32_t sk[G];
 #pragma unroll
-  for (int r = 0; r < G; ++r) kept |= (rank[r] < K ? 1u : 0u) << r;
+    for (int r = 0; r < G; ++r) sk[r] = static_cast<int32_t>(key[r]);
+    for (int32_t k = 0; k < K; ++k) {
+      int32_t best = sk[0];
+      int br = 0;
+#pragma unroll
+      for (int r = 1; r < G; ++r) {
+        const bool gt = sk[r] > best;
+        best = gt ? sk[r] : best;
+        br = gt ? r : br;
+      }
+      kept |= 1u << br;
+#pragma unroll
+      for (int r = 0; r < G; ++r) sk[r] = r == br ? -1 : sk[r];
+    }
+  } else {
+    int rank[G];
+#pragma unroll
+    for (int r = 0; r < G; ++r) rank[r] = 0;
+#pragma unroll
+    for (int r = 1; r < G; ++r)
+#pragma unroll
+      for (int q = 0; q < r; ++q) {
+        const bool q_wins = key[q] >= key[r];  // q < r: a tie goes to q
+        rank[r] += q_wins ? 1 : 0;
+        rank[q] += q_wins ? 0 : 1;
+      }
+#pragma unroll
+    for (int r = 0; r < G; ++r) kept |= (rank[r] < K ? 1u : 0u) << r;
+  }
   for (int32_t k = 0; k < K; ++k) {
     const int r = __builtin_ctz(kept);
     kept &= kept - 1u;

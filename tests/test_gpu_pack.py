@@ -44,6 +44,9 @@ def test_pack_ties_zeros_and_specials(vdt):
     W[0, :5] = [np.inf, -np.inf, np.nan, 3e38, -1e-40]
     run_pack(W.astype(np.float32), 8, 3, vdt)
     run_pack(W.astype(np.float32), 16, 5, vdt)
+    # the take-the-largest-K-times path (K < (G - 1) / 2) and the pairwise rank, on heavy ties
+    for G, K in ((16, 1), (16, 2), (16, 4), (16, 7), (16, 8), (8, 1), (4, 1), (32, 3)):
+        run_pack(W.astype(np.float32), G, K, vdt)
 
 
 @pytest.mark.parametrize("K", [1, 2, 4, 8, 16])

@@ -92,14 +92,21 @@ typedef enum { CCI_F32 = 0, CCI_BF16 = 1 } cci_dtype;
  *                           rows in LDS once.  3x3 convolutions with unit
  *                           stride and padding 0..2, Cin 32 or 64, O 32 or
  *                           64, bf16 X and vals, O/G*K*C/8 <= 5120; X, vals
- *                           and Y 16-byte aligned, idx 8-byte aligned. */
+ *                           and Y 16-byte aligned, idx 8-byte aligned.
+ *  CCI_ALGO_FEW_ROWS_MFMA   the few-row product of cci_spmm_bits reading
+ *                           cci_pack's byte indices: FC products and 1x1
+ *                           convolutions with stride 1 and no padding,
+ *                           N <= 64, C % 32 == 0, O % 16 == 0, bf16 X and
+ *                           vals (the packed bytes set the time; each is
+ *                           read once). */
 typedef enum {
   CCI_ALGO_AUTO = 0,
   CCI_ALGO_SPARSE_MAC = 1,
   CCI_ALGO_DENSE_TILE_MFMA = 2,
   CCI_ALGO_WIDE_TILE_MFMA = 3,
   CCI_ALGO_NARROW_MFMA = 4,
-  CCI_ALGO_RESIDENT_MFMA = 5
+  CCI_ALGO_RESIDENT_MFMA = 5,
+  CCI_ALGO_FEW_ROWS_MFMA = 6
 } cci_algo;
 
 /* Optional fused epilogue, applied per output element before rounding:

@@ -67,6 +67,18 @@ cci_status check_types(cci_dtype x_t, cci_dtype val_t, cci_dtype y_t) {
   return CCI_OK;
 }
 
+// The few-row product of cci_spmm_bits, reading the byte indices of
+// cci_pack (8-bit entries): FC products and 1x1 convolutions whose rows are
+// the pixels.
+bool few_rows_ok(const cci::ProductArgs& a) {
+  if (a.x_t != cci::DType::BF16 || a.val_t != cci::DType::BF16) return false;
+  if (a.conv) {
+    const cci::ConvGeom& g = a.geom;
+    if (g.KH != 1 || g.KW != 1 || g.sh != 1 || g.sw != 1 || g.ph != 0 || g.pw != 0) return false;
+  }
+  return cci::spmm_bits_supports(a.N, a.C, a.O, a.G, a.K);
+}
+
 cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* ep,
                        void* stream) {
   a.scale = ep ? ep->scale : nullptr;
@@ -77,7 +89,8 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
       (a.residual && !aligned16(a.residual)))
     return fail(CCI_EALIGN, "epilogue pointer not 16-byte aligned");
   if (algo != CCI_ALGO_AUTO && algo != CCI_ALGO_SPARSE_MAC && algo != CCI_ALGO_DENSE_TILE_MFMA &&
-      algo != CCI_ALGO_WIDE_TILE_MFMA && algo != CCI_ALGO_NARROW_MFMA && algo != CCI_ALGO_RESIDENT_MFMA)
+      algo != CCI_ALGO_WIDE_TILE_MFMA && algo != CCI_ALGO_NARROW_MFMA && algo != CCI_ALGO_RESIDENT_MFMA &&
+      algo != CCI_ALGO_FEW_ROWS_MFMA)
     return fail(CCI_EINVAL, "unknown algo %d", (int)algo);
   if (a.N == 0) return ok();
 
@@ -91,6 +104,8 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
                            a.G, a.K);
   }
   // (the shape-only choice cannot see stride and padding)
+  if (algo == CCI_ALGO_AUTO && chosen == CCI_ALGO_FEW_ROWS_MFMA && !few_rows_ok(a))
+    chosen = tile_ok ? CCI_ALGO_DENSE_TILE_MFMA : CCI_ALGO_SPARSE_MAC;
   if (algo == CCI_ALGO_AUTO && chosen == CCI_ALGO_RESIDENT_MFMA && !cci::resident_supports(a))
     chosen = tile_ok ? CCI_ALGO_DENSE_TILE_MFMA : CCI_ALGO_SPARSE_MAC;
   if (algo == CCI_ALGO_AUTO && chosen == CCI_ALGO_WIDE_TILE_MFMA && !cci::wide_tile_supports(a))
@@ -106,6 +121,10 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
     return fail(CCI_EUNSUPPORTED,
                 "wide-tile MFMA kernels need bf16 X/vals, an FC or stride-1 unpadded 1x1 product, "
                 "C %% 64 == 0, O %% 256 == 0, 64 %% G == 0 and aligned pointers");
+  if (chosen == CCI_ALGO_FEW_ROWS_MFMA && !few_rows_ok(a))
+    return fail(CCI_EUNSUPPORTED,
+                "few-row MFMA kernels need bf16 X/vals, an FC or stride-1 unpadded 1x1 product, N <= 64, "
+                "C %% 32 == 0 and O %% 16 == 0");
   if (chosen == CCI_ALGO_RESIDENT_MFMA && !cci::resident_supports(a))
     return fail(CCI_EUNSUPPORTED,
                 "resident MFMA kernels need bf16 X/vals, a 3x3 convolution with unit stride and padding "
@@ -119,6 +138,9 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
   hipError_t e = chosen == CCI_ALGO_SPARSE_MAC       ? cci::launch_sparse_mac(a, st)
                  : chosen == CCI_ALGO_WIDE_TILE_MFMA ? cci::launch_wide_tile(a, st)
                  : chosen == CCI_ALGO_RESIDENT_MFMA  ? cci::launch_resident(a, st)
+                 : chosen == CCI_ALGO_FEW_ROWS_MFMA
+                     ? cci::launch_spmm_bits(a.X, a.N, a.C, a.vals, a.idx, 8, a.O, a.G, a.K, a.scale, a.bias,
+                                             a.residual, a.relu, a.Y, a.y_t, st)
                  : chosen == CCI_ALGO_NARROW_MFMA    ? cci::launch_narrow(a, st)
                                                      : cci::launch_dense_tile(a, st);
   if (e != hipSuccess) return fail(CCI_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
@@ -220,6 +242,12 @@ cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C, int
   // a 12544 x 1024 x 256 one (98 tiles of 128 pixels), slower on the short
   // reductions of ResNet-50's other 1x1 layers.
   const bool bf = x_t == CCI_BF16 && val_t == CCI_BF16 && G >= 1 && 64 % G == 0;
+  // Up to 64 rows every packed weight feeds at most 64 multiply-adds: the
+  // packed bytes set the time, and the few-row kernel (one expanded 16 x 32
+  // tile per k-step and wave, read once) takes 7-24 us on a 4096 x 4096
+  // layer where the tile kernels need 55-70 us.
+  if (x_t == CCI_BF16 && val_t == CCI_BF16 && C == cin && N <= 64 && C % 32 == 0 && O % 16 == 0)
+    return CCI_ALGO_FEW_ROWS_MFMA;
   // 3x3 convolutions over 32 or 64 channels into 32 or 64 outputs: their
   // whole expanded tile fits in registers, so it is expanded once per
   // workgroup and only activations stream (measured 2-3x the dense-tile

@@ -125,6 +125,20 @@ def test_resident_algo_requirements():
     assert lib.cci_auto_algo(cci.BF16, cci.BF16, 100352, 576, 64, 64, 8, 2) == Rs
 
 
+def test_few_rows_algo_requirements():
+    # few-row MFMA: bf16 FC / plain 1x1 products with N <= 64, C % 32 == 0, O % 16 == 0
+    Fr = cci.ALGO_FEW_ROWS_MFMA
+    for N, C, O in [(65, 64, 16), (4, 48, 16), (4, 64, 24)]:
+        assert lib.cci_spmm_algo(FAKE, cci.BF16, N, C, FAKE, cci.BF16, FAKE, O, 8, 2, None, FAKE,
+                                 cci.BF16, Fr, None) == cci.EUNSUPPORTED
+    assert lib.cci_spmm_algo(FAKE, cci.F32, 4, 64, FAKE, cci.F32, FAKE, 16, 8, 2, None, FAKE,
+                             cci.F32, Fr, None) == cci.EUNSUPPORTED
+    assert lib.cci_conv_im2col_algo(FAKE, cci.BF16, 1, 4, 4, 64, 3, 3, 1, 1, 1, 1, FAKE, cci.BF16,
+                                    FAKE, 16, 8, 2, None, FAKE, cci.BF16, Fr, None) == cci.EUNSUPPORTED
+    assert lib.cci_auto_algo(cci.BF16, cci.BF16, 64, 4096, 4096, 4096, 16, 4) == Fr
+    assert lib.cci_auto_algo(cci.BF16, cci.BF16, 65, 4096, 4096, 4096, 16, 4) != Fr
+
+
 def test_algo_entry_points_match_plain_calls_on_validation():
     # the pinned-family calls validate exactly like the plain ones
     assert lib.cci_spmm_algo(FAKE, cci.BF16, 4, 64, FAKE, cci.BF16, FAKE, 12, 8, 2, None, FAKE,

@@ -133,6 +133,29 @@ def test_spmm_fp32(N, C, O, G, K):
     run_case(rand_x(N, C, torch.float32, N), rand_w(O, C, C), G, K, torch.float32, "auto")
 
 
+FEW_ROW_CASES = [  # N, C, O, G, K: N <= 64 bf16 products (the library's choice: the few-row kernel)
+    (1, 64, 16, 8, 2), (17, 96, 48, 16, 4), (64, 512, 256, 8, 3), (33, 32, 48, 3, 2), (5, 256, 256, 256, 9),
+    (64, 160, 64, 4, 4), (2, 1024, 512, 64, 1),
+]
+
+
+@pytest.mark.parametrize("N,C,O,G,K", FEW_ROW_CASES)
+def test_spmm_bf16_few_rows(N, C, O, G, K):
+    need_gpu()
+    from paper_1910_11971_amd import cci
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, N, C, C, O, G, K) == "few_rows_mfma"
+    run_case(rand_x(N, C, torch.bfloat16, N + C + 1), rand_w(O, C, O + G + 1), G, K, torch.bfloat16, "auto")
+    run_case(rand_x(N, C, torch.bfloat16, N + C + 2), rand_w(O, C, O + G + 2), G, K, torch.bfloat16, "few_rows_mfma")
+
+
+@pytest.mark.parametrize("y_dtype", [torch.bfloat16, torch.float32])
+def test_spmm_few_rows_epilogue(y_dtype):
+    need_gpu()
+    N, C, O, G, K = 40, 256, 128, 8, 2
+    ep = rand_epilogue(O, N, y_dtype, 23, residual=True, relu=True)
+    run_case(rand_x(N, C, torch.bfloat16, 24), rand_w(O, C, 25), G, K, y_dtype, "few_rows_mfma", ep=ep)
+
+
 def test_spmm_odd_c_bf16_auto_routes_to_sparse_mac():
     need_gpu()
     run_case(rand_x(200, 45, torch.bfloat16, 9), rand_w(32, 45, 9), 8, 2, torch.bfloat16, "auto")

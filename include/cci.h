@@ -98,7 +98,17 @@ typedef enum { CCI_F32 = 0, CCI_BF16 = 1 } cci_dtype;
  *                           convolutions with stride 1 and no padding,
  *                           N <= 64, C % 32 == 0, O % 16 == 0, bf16 X and
  *                           vals (the packed bytes set the time; each is
- *                           read once). */
+ *                           read once).
+ *  CCI_ALGO_TAP_TILE_MFMA   the same expansion with 128-pixel x 128-output
+ *                           workgroup tiles, two workgroups per CU, and a
+ *                           reduction in chunks of 64 input channels under
+ *                           one filter tap: convolutions of any stride and
+ *                           padding through implicit im2col, and FC
+ *                           products, with long reductions and few output
+ *                           tiles.  Needs bf16 X and vals, Cin % 64 == 0
+ *                           (FC: C % 64 == 0), O % 128 == 0, 32 % G == 0,
+ *                           KH*KW <= 32; X, vals and Y 16-byte aligned, idx
+ *                           8-byte aligned. */
 typedef enum {
   CCI_ALGO_AUTO = 0,
   CCI_ALGO_SPARSE_MAC = 1,
@@ -106,7 +116,8 @@ typedef enum {
   CCI_ALGO_WIDE_TILE_MFMA = 3,
   CCI_ALGO_NARROW_MFMA = 4,
   CCI_ALGO_RESIDENT_MFMA = 5,
-  CCI_ALGO_FEW_ROWS_MFMA = 6
+  CCI_ALGO_FEW_ROWS_MFMA = 6,
+  CCI_ALGO_TAP_TILE_MFMA = 7
 } cci_algo;
 
 /* Optional fused epilogue, applied per output element before rounding:

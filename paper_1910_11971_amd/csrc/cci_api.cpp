@@ -90,7 +90,7 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
     return fail(CCI_EALIGN, "epilogue pointer not 16-byte aligned");
   if (algo != CCI_ALGO_AUTO && algo != CCI_ALGO_SPARSE_MAC && algo != CCI_ALGO_DENSE_TILE_MFMA &&
       algo != CCI_ALGO_WIDE_TILE_MFMA && algo != CCI_ALGO_NARROW_MFMA && algo != CCI_ALGO_RESIDENT_MFMA &&
-      algo != CCI_ALGO_FEW_ROWS_MFMA)
+      algo != CCI_ALGO_FEW_ROWS_MFMA && algo != CCI_ALGO_TAP_TILE_MFMA)
     return fail(CCI_EINVAL, "unknown algo %d", (int)algo);
   if (a.N == 0) return ok();
 
@@ -111,6 +111,8 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
   if (algo == CCI_ALGO_AUTO && chosen == CCI_ALGO_WIDE_TILE_MFMA && !cci::wide_tile_supports(a))
     chosen = CCI_ALGO_DENSE_TILE_MFMA;
   if (algo == CCI_ALGO_AUTO && chosen == CCI_ALGO_NARROW_MFMA && !cci::narrow_supports(a))
+    chosen = tile_ok ? CCI_ALGO_DENSE_TILE_MFMA : CCI_ALGO_SPARSE_MAC;
+  if (algo == CCI_ALGO_AUTO && chosen == CCI_ALGO_TAP_TILE_MFMA && !cci::tap_tile_supports(a))
     chosen = tile_ok ? CCI_ALGO_DENSE_TILE_MFMA : CCI_ALGO_SPARSE_MAC;
   if (chosen == CCI_ALGO_SPARSE_MAC && !mac_ok)
     return fail(CCI_EUNSUPPORTED, "sparse-MAC kernels need G in {2,4,8,16,32} (G=%d)", a.G);
@@ -134,8 +136,13 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
                 "narrow MFMA kernels need bf16 X/vals, C <= 256, C %% 8 == 0, O %% 4 == 0, G <= 256, "
                 "aligned pointers, and for a conv other than 1x1 stride 1 unpadded Cin %% 8 == 0 or "
                 "Cin == 4 with an even KW");
+  if (chosen == CCI_ALGO_TAP_TILE_MFMA && !cci::tap_tile_supports(a))
+    return fail(CCI_EUNSUPPORTED,
+                "tap-tile MFMA kernels need bf16 X/vals, Cin (FC: C) %% 64 == 0, O %% 128 == 0, 32 %% G == 0, "
+                "at most 32 filter taps and aligned pointers");
   const hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = chosen == CCI_ALGO_SPARSE_MAC       ? cci::launch_sparse_mac(a, st)
+                 : chosen == CCI_ALGO_TAP_TILE_MFMA  ? cci::launch_tap_tile(a, st)
                  : chosen == CCI_ALGO_WIDE_TILE_MFMA ? cci::launch_wide_tile(a, st)
                  : chosen == CCI_ALGO_RESIDENT_MFMA  ? cci::launch_resident(a, st)
                  : chosen == CCI_ALGO_FEW_ROWS_MFMA

@@ -88,6 +88,13 @@ hipError_t launch_narrow(const ProductArgs& a, hipStream_t s);
 bool resident_supports(const ProductArgs& a);
 hipError_t launch_resident(const ProductArgs& a, hipStream_t s);
 
+// Convolutions of any geometry (implicit im2col) and FC products whose
+// reduction splits into chunks of 64 channels under one tap (Cin % 64 == 0):
+// 128 x 128 workgroup tiles, two workgroups per CU (bf16; O % 128 == 0,
+// 32 % G == 0, KH * KW <= 32).
+bool tap_tile_supports(const ProductArgs& a);
+hipError_t launch_tap_tile(const ProductArgs& a, hipStream_t s);
+
 // Balanced sparsity (groups of G inputs in one output row) and the 2:4
 // sparse matrix-core product.
 hipError_t launch_bbs_pack(const float* W, int64_t O, int64_t C, int32_t G, int32_t K, void* vals, DType val_t,

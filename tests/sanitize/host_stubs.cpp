@@ -27,6 +27,11 @@ bool resident_supports(const ProductArgs& a) {
          (a.geom.Cin == 32 || a.geom.Cin == 64) && (a.O == 32 || a.O == 64);
 }
 hipError_t launch_resident(const ProductArgs&, hipStream_t) { ++g_launches; return hipSuccess; }
+bool tap_tile_supports(const ProductArgs& a) {
+  const int64_t cin = a.conv ? a.geom.Cin : a.C;
+  return a.x_t == DType::BF16 && cin % 64 == 0 && a.O % 128 == 0 && 32 % a.G == 0;
+}
+hipError_t launch_tap_tile(const ProductArgs&, hipStream_t) { ++g_launches; return hipSuccess; }
 hipError_t launch_bbs_pack(const float*, int64_t, int64_t, int32_t, int32_t, void*, DType, uint8_t*, hipStream_t) {
   ++g_launches;
   return hipSuccess;

@@ -125,6 +125,21 @@ def test_resident_algo_requirements():
     assert lib.cci_auto_algo(cci.BF16, cci.BF16, 100352, 576, 64, 64, 8, 2) == Rs
 
 
+def test_tap_tile_algo_requirements():
+    # tap-tile MFMA: bf16, Cin (FC: C) % 64 == 0, O % 128 == 0, 32 % G == 0, at most 32 taps
+    Tt = cci.ALGO_TAP_TILE_MFMA
+    for C, O, G in [(96, 128, 8), (64, 64, 8), (64, 128, 64), (64, 192, 8)]:
+        assert lib.cci_spmm_algo(FAKE, cci.BF16, 4, C, FAKE, cci.BF16, FAKE, O, G, 2, None, FAKE,
+                                 cci.BF16, Tt, None) == cci.EUNSUPPORTED
+    assert lib.cci_spmm_algo(FAKE, cci.F32, 4, 64, FAKE, cci.F32, FAKE, 128, 8, 2, None, FAKE,
+                             cci.F32, Tt, None) == cci.EUNSUPPORTED
+    for Cin, KH, KW in [(32, 3, 3), (64, 7, 7)]:
+        assert lib.cci_conv_im2col_algo(FAKE, cci.BF16, 1, 8, 8, Cin, KH, KW, 1, 1, 1, 1, FAKE, cci.BF16,
+                                        FAKE, 128, 8, 2, None, FAKE, cci.BF16, Tt, None) == cci.EUNSUPPORTED
+    assert lib.cci_spmm_algo(FAKE, cci.BF16, 4, 64, FAKE, cci.BF16, FAKE, 128, 8, 2, None, FAKE,
+                             cci.BF16, 8, None) == cci.EINVAL
+
+
 def test_few_rows_algo_requirements():
     # few-row MFMA: bf16 FC / plain 1x1 products with N <= 64, C % 32 == 0, O % 16 == 0
     Fr = cci.ALGO_FEW_ROWS_MFMA

@@ -178,6 +178,58 @@ def test_conv_resident_shape_falls_back(stride):
     run_conv(X, rand_w(64, 576, 52), 8, 2, 3, stride, 1, torch.bfloat16, "auto")
 
 
+TAP_CASES = [  # B, H, W, Cin, O, KH, KW, stride, pad, G, K
+    (2, 9, 11, 64, 128, 3, 3, 1, 1, 8, 2),     # 198 pixels: a ragged second pixel block
+    (3, 14, 14, 128, 128, 3, 3, 2, 1, 8, 2),   # stride 2
+    (2, 7, 7, 256, 256, 3, 3, 1, 1, 16, 4),    # one pixel block, two output blocks, 36 chunks
+    (1, 12, 10, 64, 384, 5, 5, 1, 2, 4, 1),    # 5x5, padding 2, three output blocks
+    (2, 10, 9, 128, 128, 1, 1, 2, 0, 16, 2),   # strided 1x1
+    (3, 8, 8, 64, 128, 3, 3, 1, 0, 32, 7),     # G = 32: a group spans two 16-row blocks
+    (2, 6, 7, 64, 128, 3, 3, 1, 1, 8, 8),      # K = G (dense control)
+    (4, 9, 9, 64, 256, 3, 3, 2, 1, 2, 1),      # G = 2: 16 packed rows per wave
+    (2, 11, 13, 192, 128, 3, 3, 1, 1, 8, 3),   # 12 packed rows per wave; 3 channel blocks per tap
+    (1, 20, 20, 64, 128, 7, 4, 1, 3, 16, 1),   # 28 taps, padding 3
+    (6, 16, 16, 64, 128, 1, 1, 1, 0, 4, 3),    # 1x1 through the conv call; 24 packed rows per wave
+    (3, 4, 4, 64, 128, 3, 3, 1, 1, 1, 1),      # G = 1
+    (1, 1, 1, 64, 128, 3, 3, 1, 1, 8, 2),      # one pixel: every tap but the centre in the padding
+]
+
+
+@pytest.mark.parametrize("B,H,W,Cin,O,KH,KW,stride,pad,G,K", TAP_CASES)
+def test_conv_tap_tile(B, H, W, Cin, O, KH, KW, stride, pad, G, K):
+    """Implicit-im2col convolutions on the tap-chunk kernels (128 x 128 tiles)."""
+    need_gpu()
+    X = rand_x((B, H, W, Cin), torch.bfloat16, B + H + W + Cin + KH)
+    run_conv_kw(X, rand_w(O, KH * KW * Cin, O + G + K + KW), G, K, KH, KW, stride, pad, torch.bfloat16,
+                "tap_tile_mfma")
+
+
+@pytest.mark.parametrize("y_dtype", [torch.bfloat16, torch.float32])
+def test_conv_tap_tile_epilogue(y_dtype):
+    """scale, bias, residual and ReLU fused on the tap-chunk kernels, bf16 and fp32 output."""
+    need_gpu()
+    from paper_1910_11971_amd import cci
+    B, H, W, Cin, O = 2, 13, 11, 128, 256
+    Ho, Wo = cci.conv_out_hw(H, W, 3, 3, (2, 2), (1, 1))
+    ep = rand_epilogue(O, B * Ho * Wo, y_dtype, 71, residual=True, relu=True)
+    run_conv(rand_x((B, H, W, Cin), torch.bfloat16, 72), rand_w(O, 9 * Cin, 73), 8, 2, 3, 2, 1, y_dtype,
+             "tap_tile_mfma", ep=ep)
+    ep = rand_epilogue(O, B * Ho * Wo, y_dtype, 74, residual=False, relu=False)
+    run_conv(rand_x((B, H, W, Cin), torch.bfloat16, 75), rand_w(O, 9 * Cin, 76), 16, 4, 3, 2, 1, y_dtype,
+             "tap_tile_mfma", ep=ep)
+
+
+def test_conv_tap_tile_refuses_unsupported():
+    """Cin % 64 != 0, O % 128 != 0 and G = 64 are refused by the tap-chunk family."""
+    need_gpu()
+    from paper_1910_11971_amd import cci
+    for Cin, O, G in [(96, 128, 8), (64, 64, 8), (64, 128, 64)]:
+        X = rand_x((1, 5, 5, Cin), torch.bfloat16, 81).to(DEV)
+        vals, idx = cci.pack(torch.from_numpy(rand_w(O, 9 * Cin, 82)).to(DEV), G, 2, torch.bfloat16)
+        with pytest.raises(cci.CCIError):
+            cci.conv_im2col(X, vals, idx, G, 3, 3, (1, 1), (1, 1), algo="tap_tile_mfma")
+
+
 @pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma"])
 def test_conv_epilogue_residual_relu(algo):
     need_gpu()

@@ -98,6 +98,18 @@ def test_spmm_bf16_narrow(N, C, O, G, K):
     run_case(rand_x(N, C, torch.bfloat16, N + C), rand_w(O, C, O + G), G, K, torch.bfloat16, "narrow_mfma")
 
 
+TAP_FC_CASES = [  # N, C, O, G, K: FC products on the tap-chunk kernels
+    (1, 64, 128, 8, 2), (129, 128, 256, 16, 4), (300, 640, 128, 4, 1), (1000, 1024, 256, 16, 4),
+    (257, 192, 384, 32, 5), (2049, 64, 128, 8, 8), (777, 320, 128, 2, 1), (12544, 256, 256, 8, 3),
+]
+
+
+@pytest.mark.parametrize("N,C,O,G,K", TAP_FC_CASES)
+def test_spmm_bf16_tap_tile(N, C, O, G, K):
+    need_gpu()
+    run_case(rand_x(N, C, torch.bfloat16, N + C), rand_w(O, C, O + G), G, K, torch.bfloat16, "tap_tile_mfma")
+
+
 def test_spmm_wide_tile_repeat_is_identical():
     """Two launches on the same inputs give the same bytes (no state carried between launches)."""
     need_gpu()
@@ -110,7 +122,7 @@ def test_spmm_wide_tile_repeat_is_identical():
     assert torch.equal(Y1.view(torch.int16), Y2.view(torch.int16))
 
 
-@pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma", "wide_tile_mfma", "narrow_mfma"])
+@pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma", "wide_tile_mfma", "narrow_mfma", "tap_tile_mfma"])
 def test_spmm_bf16_in_f32_out_with_epilogue(algo):
     need_gpu()
     N, C, O, G, K = 777, 128, 256, 8, 2
@@ -118,7 +130,7 @@ def test_spmm_bf16_in_f32_out_with_epilogue(algo):
     run_case(rand_x(N, C, torch.bfloat16, 1), rand_w(O, C, 2), G, K, torch.float32, algo, ep=ep)
 
 
-@pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma", "wide_tile_mfma", "narrow_mfma"])
+@pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma", "wide_tile_mfma", "narrow_mfma", "tap_tile_mfma"])
 def test_spmm_bf16_epilogue_bf16_residual(algo):
     need_gpu()
     N, C, O, G, K = 300, 64, 256, 16, 4

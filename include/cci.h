@@ -200,12 +200,13 @@ cci_status cci_conv_im2col_algo(const void *X, cci_dtype x_t, int64_t B,
 
 /* Which family CCI_ALGO_AUTO picks for a product of N x C x O (conv: pass
  * N = B*Ho*Wo, C = KH*KW*Cin and cin = Cin; FC: cin = C).  Host-only.  A
- * 1x1 convolution reported as CCI_ALGO_WIDE_TILE_MFMA runs on the dense-tile
- * kernels when its stride or padding rules the wide-tile ones out; one
- * reported as CCI_ALGO_NARROW_MFMA then runs on the dense-tile kernels if
- * they take its shape, else on the sparse-MAC ones; one reported as
- * CCI_ALGO_RESIDENT_MFMA runs on the dense-tile kernels when its stride is
- * not 1 (or another of that family's limits rules it out). */
+ * 1x1 convolution reported as CCI_ALGO_WIDE_TILE_MFMA runs on the tap-chunk
+ * kernels (else the dense-tile ones) when its stride or padding rules the
+ * wide-tile ones out; one reported as CCI_ALGO_NARROW_MFMA then runs on the
+ * dense-tile kernels if they take its shape, else on the sparse-MAC ones;
+ * one reported as CCI_ALGO_RESIDENT_MFMA or CCI_ALGO_TAP_TILE_MFMA runs on
+ * the dense-tile kernels when a stride, alignment or size limit of that
+ * family rules it out. */
 cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C,
                        int64_t cin, int64_t O, int32_t G, int32_t K);
 

@@ -109,7 +109,7 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
   if (algo == CCI_ALGO_AUTO && chosen == CCI_ALGO_RESIDENT_MFMA && !cci::resident_supports(a))
     chosen = tile_ok ? CCI_ALGO_DENSE_TILE_MFMA : CCI_ALGO_SPARSE_MAC;
   if (algo == CCI_ALGO_AUTO && chosen == CCI_ALGO_WIDE_TILE_MFMA && !cci::wide_tile_supports(a))
-    chosen = CCI_ALGO_DENSE_TILE_MFMA;
+    chosen = cci::tap_tile_supports(a) ? CCI_ALGO_TAP_TILE_MFMA : CCI_ALGO_DENSE_TILE_MFMA;
   if (algo == CCI_ALGO_AUTO && chosen == CCI_ALGO_NARROW_MFMA && !cci::narrow_supports(a))
     chosen = tile_ok ? CCI_ALGO_DENSE_TILE_MFMA : CCI_ALGO_SPARSE_MAC;
   if (algo == CCI_ALGO_AUTO && chosen == CCI_ALGO_TAP_TILE_MFMA && !cci::tap_tile_supports(a))
@@ -241,13 +241,7 @@ cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C, int
   // The matrix cores multiply the expanded tile at 2516.6 dense bf16 TFLOP/s;
   // the vector ALUs multiply only kept weights at 78.6 fp32 TFLOP/s (no
   // packed fp32).  Expanded work is G/K times the kept work, so the tile
-  // path wins whenever K/G > 78.6/2516.6 (about 1/32).  The wide-tile plan
-  // (256-output workgroup tiles of 256 pixels, or of 128 when the product is
-  // smaller) is measured faster than the dense-tile one once there are
-  // at least 96 tiles of 128 pixels and a reduction of at least 8 of its
-  // 64-channel chunks to pipeline: 2.2-2.4x on 4096^3 FC products, 1.15x on
-  // a 12544 x 1024 x 256 one (98 tiles of 128 pixels), slower on the short
-  // reductions of ResNet-50's other 1x1 layers.
+  // path wins whenever K/G > 78.6/2516.6 (about 1/32).
   const bool bf = x_t == CCI_BF16 && val_t == CCI_BF16 && G >= 1 && 64 % G == 0;
   // Up to 64 rows every packed weight feeds at most 64 multiply-adds: the
   // packed bytes set the time, and the few-row kernel (one expanded 16 x 32
@@ -264,8 +258,6 @@ cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C, int
       O % G == 0)
     return CCI_ALGO_RESIDENT_MFMA;
   const bool mac_g = G == 2 || G == 4 || G == 8 || G == 16 || G == 32;
-  const int64_t tiles = (N + 127) / 128 * (O / 256);
-  if (bf && C == cin && C % 64 == 0 && C >= 512 && O % 256 == 0 && tiles >= 96) return CCI_ALGO_WIDE_TILE_MFMA;
   // Short reductions the tile kernels cannot take (Cin % 32 != 0) stream
   // through register-resident weights: 1x1 layers and FC products with
   // C % 8 == 0, and convolutions over 4 input channels (an even KW) or a
@@ -276,6 +268,22 @@ cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C, int
   const bool narrow_shape = x_t == CCI_BF16 && val_t == CCI_BF16 && C <= 256 && C % 8 == 0 && O % 4 == 0 &&
                             (cin == 4 || cin % 8 == 0);
   if (narrow_shape && (cin % 32 != 0 || (C == cin && C <= 128 && N >= 100000))) return CCI_ALGO_NARROW_MFMA;
+  // FC and 1x1 products that fill the chip with 256 x 256 tiles (>= 128 of
+  // them) run on the wide-tile kernels: 2.2-2.4x the dense-tile kernel on
+  // 4096^3, and ahead of the tap-chunk kernels on ResNet-50's 1x1 layers
+  // with 196 such tiles (19.5 vs 21.8 us at 12544 x 256 x 1024).
+  const int64_t tiles256 = (N + 255) / 256 * (O / 256);
+  if (bf && C == cin && C % 64 == 0 && C >= 128 && O % 256 == 0 && tiles256 >= 128) return CCI_ALGO_WIDE_TILE_MFMA;
+  // Fewer output tiles, and every k x k convolution over a multiple of 64
+  // channels, run on the tap-chunk kernels (128 x 128 tiles): measured on
+  // ResNet-50's layers at batch 64 against the dense-tile kernel, 3x3
+  // stride 2 28.9 vs 112.6 us (Cin 128), 31.5 vs 109.1 us (Cin 256), 51.9
+  // vs 99.0 us (Cin 512); 3x3 stride 1 28.6 vs 38.4 us (Cin 128); strided
+  // 1x1 26-36 vs 37-45 us; and 12544 x 1024 x 256 at 18.5 us against 23.3
+  // us on the wide-tile kernels (49 tiles of 256 x 256).
+  const bool tap_shape = x_t == CCI_BF16 && val_t == CCI_BF16 && G >= 1 && 32 % G == 0 && cin % 64 == 0 &&
+                         O % 128 == 0 && C >= 128 && C / cin <= 32;
+  if (tap_shape) return CCI_ALGO_TAP_TILE_MFMA;
   const bool tile_shape = bf && cin % 32 == 0;
   if (tile_shape && (32 * static_cast<int64_t>(K) > G || !mac_g)) return CCI_ALGO_DENSE_TILE_MFMA;
   return CCI_ALGO_SPARSE_MAC;

@@ -189,14 +189,21 @@ def test_auto_algo_cost_model():
     # 32 / 64 outputs keep the whole expanded tile in registers
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 100352, 576, 64, 64, 8, 2) == "resident_mfma"
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 100352, 288, 32, 32, 8, 2) == "resident_mfma"
-    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 100352, 576, 64, 128, 8, 2) == "dense_tile_mfma"
-    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 4096, 4096, 4096, 512, 16, 1) == "dense_tile_mfma"
+    # k x k convolutions over a multiple of 64 channels into a multiple of 128 outputs: tap-chunk MFMA
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 100352, 576, 64, 128, 8, 2) == "tap_tile_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 3136, 4608, 512, 512, 8, 2) == "tap_tile_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 4096, 4096, 4096, 512, 16, 1) == "tap_tile_mfma"
+    # 64 outputs, or 64 input channels: the dense-tile kernels
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 50000, 576, 64, 96, 16, 2) == "dense_tile_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 50000, 864, 96, 128, 8, 2) == "dense_tile_mfma"
     # large FC / 1x1 products (>= 128 tiles of 256 x 256): wide-tile MFMA, any K
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 4096, 4096, 4096, 4096, 16, 1) == "wide_tile_mfma"
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 4096, 4096, 4096, 4096, 64, 1) == "wide_tile_mfma"
-    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 12544, 1024, 1024, 256, 16, 4) == "wide_tile_mfma"
-    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 12544, 256, 256, 1024, 16, 4) == "dense_tile_mfma"
-    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 6000, 1024, 1024, 256, 16, 4) == "dense_tile_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 12544, 256, 256, 1024, 16, 4) == "wide_tile_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 50176, 128, 128, 512, 8, 2) == "wide_tile_mfma"
+    # fewer tiles: the tap-chunk kernels (two 128 x 128 tiles per CU)
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 12544, 1024, 1024, 256, 16, 4) == "tap_tile_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 6000, 1024, 1024, 256, 16, 4) == "tap_tile_mfma"
     # G the vector kernels do not support: the tile path even at K/G < 1/32
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 4096, 4096, 4096, 512, 64, 1) == "dense_tile_mfma"
     # fp32, or a reduction the tile path cannot step through: sparse-MAC

@@ -66,14 +66,16 @@ def test_conv3x3_every_output(algo):
 
 
 @pytest.mark.parametrize("name,algo", [(n, a) for n in ("conv1x1_k4", "conv1x1_k2")
-                                       for a in ("auto", "wide_tile_mfma", "dense_tile_mfma", "sparse_mac")])
+                                       for a in ("auto", "tap_tile_mfma", "wide_tile_mfma", "dense_tile_mfma",
+                                                 "sparse_mac")])
 def test_conv1x1_bottleneck_every_output(name, algo):
     need_gpu()
     run_full(name, algo)
 
 
 @pytest.mark.parametrize("K,algo", [(k, a) for k in (1, 2, 4, 8, 16)
-                                    for a in ("auto", "wide_tile_mfma", "dense_tile_mfma", "sparse_mac")])
+                                    for a in ("auto", "wide_tile_mfma", "tap_tile_mfma", "dense_tile_mfma",
+                                              "sparse_mac")])
 def test_fc4096_every_output(K, algo):
     need_gpu()
     run_full(f"fc4096_k{K}", algo)

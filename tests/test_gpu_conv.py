@@ -192,6 +192,8 @@ TAP_CASES = [  # B, H, W, Cin, O, KH, KW, stride, pad, G, K
     (6, 16, 16, 64, 128, 1, 1, 1, 0, 4, 3),    # 1x1 through the conv call; 24 packed rows per wave
     (3, 4, 4, 64, 128, 3, 3, 1, 1, 1, 1),      # G = 1
     (1, 1, 1, 64, 128, 3, 3, 1, 1, 8, 2),      # one pixel: every tap but the centre in the padding
+    (10, 60, 60, 64, 128, 3, 3, 1, 1, 8, 2),   # 282 workgroups: two per CU
+    (4, 30, 30, 128, 256, 3, 3, 1, 1, 16, 4),  # 226 workgroups: one per CU
 ]
 
 

@@ -107,8 +107,8 @@ typedef enum { CCI_F32 = 0, CCI_BF16 = 1 } cci_dtype;
  *                           products, with long reductions and few output
  *                           tiles.  Needs bf16 X and vals, Cin % 64 == 0
  *                           (FC: C % 64 == 0), O % 128 == 0, 32 % G == 0,
- *                           KH*KW <= 32; X, vals and Y 16-byte aligned, idx
- *                           8-byte aligned. */
+ *                           2 K <= G or K == G, KH*KW <= 32; X, vals and Y
+ *                           16-byte aligned, idx 8-byte aligned. */
 typedef enum {
   CCI_ALGO_AUTO = 0,
   CCI_ALGO_SPARSE_MAC = 1,

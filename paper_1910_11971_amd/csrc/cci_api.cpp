@@ -139,7 +139,7 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
   if (chosen == CCI_ALGO_TAP_TILE_MFMA && !cci::tap_tile_supports(a))
     return fail(CCI_EUNSUPPORTED,
                 "tap-tile MFMA kernels need bf16 X/vals, Cin (FC: C) %% 64 == 0, O %% 128 == 0, 32 %% G == 0, "
-                "at most 32 filter taps and aligned pointers");
+                "2 K <= G or K == G, at most 32 filter taps and aligned pointers");
   const hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = chosen == CCI_ALGO_SPARSE_MAC       ? cci::launch_sparse_mac(a, st)
                  : chosen == CCI_ALGO_TAP_TILE_MFMA  ? cci::launch_tap_tile(a, st)
@@ -281,8 +281,8 @@ cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C, int
   // vs 99.0 us (Cin 512); 3x3 stride 1 28.6 vs 38.4 us (Cin 128); strided
   // 1x1 26-36 vs 37-45 us; and 12544 x 1024 x 256 at 18.5 us against 23.3
   // us on the wide-tile kernels (49 tiles of 256 x 256).
-  const bool tap_shape = x_t == CCI_BF16 && val_t == CCI_BF16 && G >= 1 && 32 % G == 0 && cin % 64 == 0 &&
-                         O % 128 == 0 && C >= 128 && C / cin <= 32;
+  const bool tap_shape = x_t == CCI_BF16 && val_t == CCI_BF16 && G >= 1 && 32 % G == 0 && (2 * K <= G || K == G) &&
+                         cin % 64 == 0 && O % 128 == 0 && C >= 128 && C / cin <= 32;
   if (tap_shape) return CCI_ALGO_TAP_TILE_MFMA;
   const bool tile_shape = bf && cin % 32 == 0;
   if (tile_shape && (32 * static_cast<int64_t>(K) > G || !mac_g)) return CCI_ALGO_DENSE_TILE_MFMA;

@@ -557,8 +557,7 @@ hipError_t launch_tg(const TParams& p, uint32_t grid, hipStream_t s) {
   if (p.rows_w == 8) return launch_tu<YT, 1, false, BIGG, false>(p, grid, s);
   if (p.rows_w < 16) return launch_tu<YT, 2, false, BIGG, true>(p, grid, s);
   if (p.rows_w == 16) return launch_tu<YT, 2, false, BIGG, false>(p, grid, s);
-  if (p.rows_w < 32) return launch_tu<YT, 4, false, BIGG, true>(p, grid, s);
-  return launch_tu<YT, 4, false, BIGG, false>(p, grid, s);
+  return launch_tu<YT, 2, false, BIGG, false>(p, grid, s);  // (rows_w <= 16: at most half of a group kept)
 }
 
 template <typename YT>
@@ -572,6 +571,9 @@ hipError_t launch_ty(const TParams& p, uint32_t grid, hipStream_t s) {
 bool tap_tile_supports(const ProductArgs& a) {
   if (a.x_t != DType::BF16 || a.val_t != DType::BF16) return false;
   if (a.G < 1 || a.G > 32 || 32 % a.G != 0 || a.K < 1 || a.K > a.G) return false;
+  // at most half of each group kept, or all of it (dense control): above
+  // that the packed units no longer fit the registers beside the rings
+  if (2 * a.K > a.G && a.K != a.G) return false;
   if (a.O % kTO != 0 || a.N < 1) return false;
   const int64_t cin = a.conv ? a.geom.Cin : a.C;
   if (cin % kCK != 0) return false;

@@ -189,7 +189,7 @@ TAP_CASES = [  # B, H, W, Cin, O, KH, KW, stride, pad, G, K
     (4, 9, 9, 64, 256, 3, 3, 2, 1, 2, 1),      # G = 2: 16 packed rows per wave
     (2, 11, 13, 192, 128, 3, 3, 1, 1, 8, 3),   # 12 packed rows per wave; 3 channel blocks per tap
     (1, 20, 20, 64, 128, 7, 4, 1, 3, 16, 1),   # 28 taps, padding 3
-    (6, 16, 16, 64, 128, 1, 1, 1, 0, 4, 3),    # 1x1 through the conv call; 24 packed rows per wave
+    (6, 16, 16, 64, 128, 1, 1, 1, 0, 4, 2),    # 1x1 through the conv call; 16 packed rows per wave
     (3, 4, 4, 64, 128, 3, 3, 1, 1, 1, 1),      # G = 1
     (1, 1, 1, 64, 128, 3, 3, 1, 1, 8, 2),      # one pixel: every tap but the centre in the padding
     (10, 60, 60, 64, 128, 3, 3, 1, 1, 8, 2),   # 282 workgroups: two per CU

@@ -101,8 +101,9 @@ def test_spmm_bf16_narrow(N, C, O, G, K):
 TAP_FC_CASES = [  # N, C, O, G, K: FC products on the tap-chunk kernels
     (1, 64, 128, 8, 2), (129, 128, 256, 16, 4), (300, 640, 128, 4, 1), (1000, 1024, 256, 16, 4),
     (257, 192, 384, 32, 5), (2049, 64, 128, 8, 8), (777, 320, 128, 2, 1), (12544, 256, 256, 8, 3),
+    (300, 128, 128, 8, 4), (300, 128, 128, 32, 16),
     # >= 257 workgroups: two workgroups per CU (the rest: one per CU)
-    (33024, 64, 128, 8, 2), (33024, 128, 128, 32, 5), (16500, 192, 256, 16, 16), (40000, 320, 128, 4, 3),
+    (33024, 64, 128, 8, 2), (33024, 128, 128, 32, 5), (16500, 192, 256, 16, 16), (40000, 320, 128, 4, 2),
 ]
 
 

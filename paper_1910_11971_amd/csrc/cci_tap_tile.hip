@@ -77,7 +77,8 @@ struct TParams {
   int32_t npb, nob, nch;  // pixel blocks, output blocks (of 128), chunks
   int32_t cpt;            // chunks per tap: Cin / 64
   int32_t rows_w;         // packed rows behind one wave's 32 tile rows: 32 K / G
-  int32_t grid8;          // grid / 8 when the grid is a multiple of 8, else 0
+  int32_t grid8;          // launched workgroups / 8 (the tile count rounded up to a multiple of 8)
+  int32_t ntiles;         // npb * nob
   // input geometry (an FC product is B = N images of 1 x 1 pixel)
   int32_t H, W, Cin, KH, KW, sh, sw, ph, pw, HoWo, Wo;
 };
@@ -162,9 +163,11 @@ __device__ __forceinline__ void tap_tile_body(const TParams& p, uint8_t* lds) {
   // ---- tile of this workgroup ---------------------------------------------
   // Dispatch places workgroup b on XCD b % 8; L numbers the workgroups of one
   // XCD consecutively, output block fastest, so the tiles that read the same
-  // activations run behind one L2.
+  // activations run behind one L2.  (The grid is rounded up to a multiple
+  // of 8; the workgroups past the last tile leave at once.)
   const uint32_t bid = blockIdx.x;
-  const uint32_t L = p.grid8 ? (bid & 7u) * static_cast<uint32_t>(p.grid8) + (bid >> 3) : bid;
+  const uint32_t L = (bid & 7u) * static_cast<uint32_t>(p.grid8) + (bid >> 3);
+  if (L >= static_cast<uint32_t>(p.ntiles)) return;
   const uint32_t pb = L / static_cast<uint32_t>(p.nob);
   const uint32_t ob = L - pb * static_cast<uint32_t>(p.nob);
 
@@ -537,8 +540,8 @@ hipError_t launch_tn(const TParams& p, uint32_t grid, hipStream_t s) {
   const hipError_t attr = set_lds_limit_once(
       lds_set, reinterpret_cast<const void*>(&tap_tile_kernel<YT, UPL, FULL, BIGG, MASK, NX>), lds_bytes(NX));
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((tap_tile_kernel<YT, UPL, FULL, BIGG, MASK, NX>), dim3(grid), dim3(kThreads), lds_bytes(NX), s,
-                     p);
+  hipLaunchKernelGGL((tap_tile_kernel<YT, UPL, FULL, BIGG, MASK, NX>), dim3(8u * static_cast<uint32_t>(p.grid8)),
+                     dim3(kThreads), lds_bytes(NX), s, p);
   return hipGetLastError();
 }
 
@@ -641,8 +644,9 @@ hipError_t launch_tap_tile(const ProductArgs& a, hipStream_t s) {
   p.rows_w = 32 * a.K / a.G;
   const int64_t grid = static_cast<int64_t>(p.npb) * p.nob;
   if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
-  p.grid8 = grid % 8 == 0 ? static_cast<int32_t>(grid / 8) : 0;
-  const uint32_t g = static_cast<uint32_t>(grid);
+  p.ntiles = static_cast<int32_t>(grid);
+  p.grid8 = static_cast<int32_t>((grid + 7) / 8);
+  const uint32_t g = static_cast<uint32_t>(grid);  // (the plan's choice counts real tiles)
   return a.y_t == DType::BF16 ? launch_ty<bf16_t>(p, g, s) : launch_ty<float>(p, g, s);
 }
 

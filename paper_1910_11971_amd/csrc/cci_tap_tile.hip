@@ -455,18 +455,32 @@ __device__ __forceinline__ void tap_tile_body(const TParams& p, uint8_t* lds) {
     for (int ot = 0; ot < 4; ++ot) acc_fence(acc[pt][ot]);
   constexpr uint32_t ysz = sizeof(YT);
   uint8_t* stg = lds + w * 64 * kEpPitch;
-#pragma unroll
-  for (int pt = 0; pt < 4; ++pt)
-#pragma unroll
-    for (int ot = 0; ot < 4; ++ot)
-      *reinterpret_cast<f32x4_t*>(stg + (pt * 16 + (lane & 15)) * kEpPitch + (ot * 16 + 4 * (lane >> 4)) * 4) =
-          acc[pt][ot];
   const __amdgpu_buffer_rsrc_t yr =
       __builtin_amdgcn_make_buffer_rsrc(p.Y, (short)0, static_cast<int>(p.y_bytes), kRsrcWord3);
   const __amdgpu_buffer_rsrc_t rsr = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<void*>(p.residual), (short)0, p.residual ? static_cast<int>(p.y_bytes) : 0, kRsrcWord3);
   const int c8 = lane & 7;  // 8-output block of the wave's 64
   const uint32_t o = ob * kTO + static_cast<uint32_t>(wo * 64 + 8 * c8);
+  const auto row_off = [&](int rr) {  // Y / residual byte offset of the lane's row rr
+    const uint32_t px = pb * kTP + static_cast<uint32_t>(wp * 64 + 8 * rr + (lane >> 3));
+    return px < static_cast<uint32_t>(p.N) ? (px * static_cast<uint32_t>(p.O) + o) * ysz : kOOB;
+  };
+  // bf16 residual: all 8 rows' 16-byte pieces are requested before the
+  // accumulators are parked (one load latency, not one per row)
+  u32x4_t rres[8];
+  if constexpr (ysz == 2) {
+    if (p.residual) {
+#pragma unroll
+      for (int rr = 0; rr < 8; ++rr)
+        rres[rr] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rsr, row_off(rr), 0, 0));
+    }
+  }
+#pragma unroll
+  for (int pt = 0; pt < 4; ++pt)
+#pragma unroll
+    for (int ot = 0; ot < 4; ++ot)
+      *reinterpret_cast<f32x4_t*>(stg + (pt * 16 + (lane & 15)) * kEpPitch + (ot * 16 + 4 * (lane >> 4)) * 4) =
+          acc[pt][ot];
   f32x4_t sc0{1.f, 1.f, 1.f, 1.f}, sc1{1.f, 1.f, 1.f, 1.f}, bi0{0.f, 0.f, 0.f, 0.f}, bi1{0.f, 0.f, 0.f, 0.f};
   if (p.scale) {
     sc0 = *reinterpret_cast<const f32x4_t*>(p.scale + o);
@@ -477,19 +491,18 @@ __device__ __forceinline__ void tap_tile_body(const TParams& p, uint8_t* lds) {
     bi1 = *reinterpret_cast<const f32x4_t*>(p.bias + o + 4);
   }
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's staging writes have landed
-#pragma unroll 2
+#pragma unroll
   for (int rr = 0; rr < 8; ++rr) {
     const int row = 8 * rr + (lane >> 3);
     const uint8_t* src = stg + row * kEpPitch + c8 * 32;
     f32x4_t y0 = *reinterpret_cast<const f32x4_t*>(src);
     f32x4_t y1 = *reinterpret_cast<const f32x4_t*>(src + 16);
-    const uint32_t px = pb * kTP + static_cast<uint32_t>(wp * 64 + row);
-    const uint32_t off = px < static_cast<uint32_t>(p.N) ? (px * static_cast<uint32_t>(p.O) + o) * ysz : kOOB;
+    const uint32_t off = row_off(rr);
     y0 = y0 * sc0 + bi0;
     y1 = y1 * sc1 + bi1;
     if (p.residual) {
       if constexpr (ysz == 2) {
-        const u32x4_t r = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rsr, off, 0, 0));
+        const u32x4_t r = rres[rr];
         y0[0] += __uint_as_float(r[0] << 16);
         y0[1] += __uint_as_float(r[0] & 0xffff0000u);
         y0[2] += __uint_as_float(r[1] << 16);

@@ -545,27 +545,40 @@ __device__ __forceinline__ void wide_tile_body(const WParams& p, uint8_t* lds) {
     bi1 = *reinterpret_cast<const f32x4_t*>(p.bias + o + 4);
   }
   uint8_t* stg = lds + w * 64 * kEpPitch;
+  const auto row_off = [&](int h, int rr) {  // Y / residual byte offset of the lane's row rr of pass h
+    const uint32_t px = pb * Geo<PT>::TP + static_cast<uint32_t>(wp * (PT * 16) + h * 64 + 4 * rr + (lane >> 4));
+    return px < static_cast<uint32_t>(p.N) ? (px * static_cast<uint32_t>(p.O) + o) * ysz : kOOB;
+  };
 #pragma unroll
   for (int h = 0; h < PT / 4; ++h) {
+    // bf16 residual: all 16 rows' 16-byte pieces are requested before the
+    // rows are processed (one load latency per pass, not one per row)
+    u32x4_t rres[16];
+    if constexpr (ysz == 2) {
+      if (p.residual) {
+#pragma unroll
+        for (int rr = 0; rr < 16; ++rr)
+          rres[rr] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rsr, row_off(h, rr), 0, 0));
+      }
+    }
 #pragma unroll
     for (int pt = 0; pt < 4; ++pt)
 #pragma unroll
       for (int ot = 0; ot < 8; ++ot)
         *reinterpret_cast<f32x4_t*>(stg + (pt * 16 + (lane & 15)) * kEpPitch + (ot * 16 + 4 * (lane >> 4)) * 4) =
             acc[4 * h + pt][ot];
-#pragma unroll 2
+#pragma unroll
     for (int rr = 0; rr < 16; ++rr) {
       const int row = 4 * rr + (lane >> 4);
       const uint8_t* src = stg + row * kEpPitch + c8 * 32;
       f32x4_t y0 = *reinterpret_cast<const f32x4_t*>(src);
       f32x4_t y1 = *reinterpret_cast<const f32x4_t*>(src + 16);
-      const uint32_t px = pb * Geo<PT>::TP + static_cast<uint32_t>(wp * (PT * 16) + h * 64 + row);
-      const uint32_t off = px < static_cast<uint32_t>(p.N) ? (px * static_cast<uint32_t>(p.O) + o) * ysz : kOOB;
+      const uint32_t off = row_off(h, rr);
       y0 = y0 * sc0 + bi0;
       y1 = y1 * sc1 + bi1;
       if (p.residual) {
         if constexpr (ysz == 2) {
-          const u32x4_t r = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rsr, off, 0, 0));
+          const u32x4_t r = rres[rr];
           y0[0] += __uint_as_float(r[0] << 16);
           y0[1] += __uint_as_float(r[0] & 0xffff0000u);
           y0[2] += __uint_as_float(r[1] << 16);

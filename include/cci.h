@@ -105,10 +105,12 @@ typedef enum { CCI_F32 = 0, CCI_BF16 = 1 } cci_dtype;
  *                           one filter tap: convolutions of any stride and
  *                           padding through implicit im2col, and FC
  *                           products, with long reductions and few output
- *                           tiles.  Needs bf16 X and vals, Cin % 64 == 0
- *                           (FC: C % 64 == 0), O % 128 == 0, 32 % G == 0,
- *                           2 K <= G or K == G, KH*KW <= 32; X, vals and Y
- *                           16-byte aligned, idx 8-byte aligned. */
+ *                           tiles (64 outputs for grids of fewer than 128
+ *                           such tiles, or O % 128 != 0).  Needs bf16 X and
+ *                           vals, Cin % 64 == 0 (FC: C % 64 == 0), O % 128
+ *                           == 0 and 32 % G == 0, or O % 64 == 0 and 16 % G
+ *                           == 0; 2 K <= G or K == G; KH*KW <= 32; X, vals
+ *                           and Y 16-byte aligned, idx 8-byte aligned. */
 typedef enum {
   CCI_ALGO_AUTO = 0,
   CCI_ALGO_SPARSE_MAC = 1,

@@ -138,8 +138,9 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
                 "Cin == 4 with an even KW");
   if (chosen == CCI_ALGO_TAP_TILE_MFMA && !cci::tap_tile_supports(a))
     return fail(CCI_EUNSUPPORTED,
-                "tap-tile MFMA kernels need bf16 X/vals, Cin (FC: C) %% 64 == 0, O %% 128 == 0, 32 %% G == 0, "
-                "2 K <= G or K == G, at most 32 filter taps and aligned pointers");
+                "tap-tile MFMA kernels need bf16 X/vals, Cin (FC: C) %% 64 == 0, O %% 128 == 0 with 32 %% G == 0 "
+                "or O %% 64 == 0 with 16 %% G == 0, 2 K <= G or K == G, at most 32 filter taps and aligned "
+                "pointers");
   const hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = chosen == CCI_ALGO_SPARSE_MAC       ? cci::launch_sparse_mac(a, st)
                  : chosen == CCI_ALGO_TAP_TILE_MFMA  ? cci::launch_tap_tile(a, st)

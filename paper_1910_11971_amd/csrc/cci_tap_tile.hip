@@ -49,20 +49,24 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 
 constexpr int kThreads = 256;             // four waves
 constexpr int kTP = 128;                  // pixels of a workgroup tile
-constexpr int kTO = 128;                  // outputs of a workgroup tile
 constexpr int kCK = 64;                   // reduction columns per chunk (two k-steps)
 constexpr int kXB = kTP * kCK * 2;        // one activation buffer
-constexpr int kWB = kTO * kCK * 2;        // one weight tile
 // NX activation buffers, then the two weight tiles: 80 KiB with three
 // buffers (two workgroups per CU), 96 KiB with four (one per CU, one chunk
 // more of prefetch)
-constexpr int lds_bytes(int nx) { return nx * kXB + 2 * kWB; }
-constexpr int kEpPitch = 64 * 4 + 16;     // epilogue staging: bytes per pixel row of a wave
+// TO outputs per workgroup tile (128, or 64 for grids that would leave CUs
+// idle): one weight tile is TO x 64 bf16
+constexpr int wb_bytes(int to) { return to * kCK * 2; }
+constexpr int lds_bytes(int nx, int to) { return nx * kXB + 2 * wb_bytes(to); }
+// epilogue staging: bytes per pixel row of a wave's 64 x TO/2 fp32 block
+constexpr int ep_pitch(int to) { return to / 2 * 4 + 16; }
 constexpr int kMaxTaps = 32;              // taps of one filter (one validity bit each)
 constexpr uint32_t kDeepGrid = 257;       // grids below this run one workgroup per CU
+constexpr int64_t kSmallGrid = 128;       // fewer 128-output tiles than this (half the CUs): 64-output tiles
 constexpr uint32_t kOOB = 0x80000000u;    // buffer offset that reads as zero / drops a store
 constexpr int kRsrcWord3 = 0x00020000;    // raw buffer descriptor word 3 (gfx9 family)
-static_assert(4 * 64 * kEpPitch <= lds_bytes(3), "epilogue staging reuses the operand buffers");
+static_assert(4 * 64 * ep_pitch(128) <= lds_bytes(3, 128) && 4 * 64 * ep_pitch(64) <= lds_bytes(3, 64),
+              "epilogue staging reuses the operand buffers");
 
 struct TParams {
   const uint16_t* X;
@@ -74,9 +78,9 @@ struct TParams {
   void* Y;
   uint32_t x_bytes, v_bytes, i_bytes, y_bytes;
   int32_t N, C, O, G, K, relu;
-  int32_t npb, nob, nch;  // pixel blocks, output blocks (of 128), chunks
+  int32_t npb, nob, nch;  // pixel blocks (of 128), output blocks (of TO), chunks
   int32_t cpt;            // chunks per tap: Cin / 64
-  int32_t rows_w;         // packed rows behind one wave's 32 tile rows: 32 K / G
+  int32_t rows_w;         // packed rows behind one wave's TO / 4 tile rows: TO / 4 * K / G
   int32_t grid8;          // launched workgroups / 8 (the tile count rounded up to a multiple of 8)
   int32_t ntiles;         // npb * nob
   // input geometry (an FC product is B = N images of 1 x 1 pixel)
@@ -153,12 +157,17 @@ __device__ __forceinline__ uint32_t trow(uint32_t o) { return ((o >> 4) << 11) |
 // entry kept, indices ascending, so a unit is one tile row's 16 bytes).
 // BIGG: G == 32 (a group spans two 16-row blocks).  MASK: some lanes have no
 // unit (else the checks compile away).
-template <typename YT, int UPL, bool FULL, bool BIGG, bool MASK, int NX>
+template <typename YT, int UPL, bool FULL, bool BIGG, bool MASK, int NX, int TO>
 __device__ __forceinline__ void tap_tile_body(const TParams& p, uint8_t* lds) {
-  constexpr int RW = NX - 1;  // packed-unit ring stages: W(m) is issued with X(m)
+  constexpr int RW = NX - 1;         // packed-unit ring stages: W(m) is issued with X(m)
+  constexpr int OT = TO / 32;        // 16-output tiles per wave
+  constexpr int RPW = TO / 4;        // weight-tile rows a wave builds
+  constexpr int WB = wb_bytes(TO);   // one weight tile
+  constexpr int PITCH = ep_pitch(TO);
+  constexpr int NMF = 4 * OT;        // MFMAs of one k-step
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wp = w >> 1, wo = w & 1;  // pixel half, output half of this wave
+  const int wp = w >> 1, wo = w & 1;  // pixel half, output half (TO / 2 outputs) of this wave
 
   // ---- tile of this workgroup ---------------------------------------------
   // Dispatch places workgroup b on XCD b % 8; L numbers the workgroups of one
@@ -234,8 +243,8 @@ __device__ __forceinline__ void tap_tile_body(const TParams& p, uint8_t* lds) {
   };
 
   // ---- packed weights ---------------------------------------------------------
-  // Wave w expands tile rows [32 w, 32 w + 32): 32 / G groups, rows_w packed
-  // rows.  Unit u of a lane is packed row r = (lane + 64 u) / 8 of them,
+  // Wave w expands tile rows [RPW w, RPW w + RPW): RPW / G groups, rows_w
+  // packed rows.  Unit u of a lane is packed row r = (lane + 64 u) / 8 of them,
   // channels 8 c8 .. +7 of the chunk, c8 = (lane + 64 u) % 8.
   const u32x4_t vd = sdesc(p.vals, p.v_bytes), id = sdesc(p.idx, p.i_bytes);
   // The lanes of one packed row write neighbouring column blocks whose
@@ -253,12 +262,12 @@ __device__ __forceinline__ void tap_tile_body(const TParams& p, uint8_t* lds) {
     const int v = lane + 64 * u;
     const int r = v >> 3, c8 = v & 7;
     uok[u] = !MASK || r < p.rows_w;
-    const uint32_t prow = (ob * static_cast<uint32_t>(kTO / p.G) + static_cast<uint32_t>(w * (32 / p.G))) *
+    const uint32_t prow = (ob * static_cast<uint32_t>(TO / p.G) + static_cast<uint32_t>(w * (RPW / p.G))) *
                               static_cast<uint32_t>(p.K) +
                           static_cast<uint32_t>(r);
     voff[u] = uok[u] ? (prow * static_cast<uint32_t>(p.C) + static_cast<uint32_t>(c8 * 8)) * 2u : kOOB;
     ioff[u] = uok[u] ? prow * static_cast<uint32_t>(p.C) + static_cast<uint32_t>(c8 * 8) : kOOB;
-    const int o0 = 32 * w + (FULL ? r : (r / p.K) * p.G);  // first tile row of the unit's group
+    const int o0 = RPW * w + (FULL ? r : (r / p.K) * p.G);  // first tile row of the unit's group
     // (non-FULL: bits 1..3 carry 2 m, the byte offset of element m)
     ubase[u] = trow(static_cast<uint32_t>(uok[u] ? o0 : 0)) +
                static_cast<uint32_t>((c8 >> 2) * 1024 + (c8 & 3) * 256) + (FULL ? 0u : 2u * m);
@@ -294,10 +303,11 @@ __device__ __forceinline__ void tap_tile_body(const TParams& p, uint8_t* lds) {
   };
   // tile offset of row rr of a group, relative to its first row
   auto grow = [](uint32_t rr) { return BIGG ? trow(rr) : rr << 4; };
-  // Building a tile: wave w zeroes its 32 rows (4 KiB at w * 4096), then
+  // Building a tile: wave w zeroes its RPW rows (RPW / 16 blocks of 16 rows,
+  // both k-steps: RPW * 128 bytes at w * RPW * 128), then
   // writes its kept weights; LDS operations of one wave complete in order.
   auto zero_piece = [&](uint8_t* tb, int i) {
-    *reinterpret_cast<u32x4_t*>(tb + w * 4096 + i * 1024 + lane * 16) = u32x4_t{0u, 0u, 0u, 0u};
+    *reinterpret_cast<u32x4_t*>(tb + w * (RPW * 128) + i * 1024 + lane * 16) = u32x4_t{0u, 0u, 0u, 0u};
   };
   auto scatter_e = [&](uint8_t* tb, auto kc, int u, int e) {  // step e of unit u (element e ^ m)
     constexpr int k = decltype(kc)::value;
@@ -315,16 +325,17 @@ __device__ __forceinline__ void tap_tile_body(const TParams& p, uint8_t* lds) {
 
   // ---- MFMAs ------------------------------------------------------------------
   // acc[pt][ot]: 16 pixels (tile pt of the wave's 64) x 16 outputs (tile ot
-  // of its 64).  A lane holds outputs 4 (lane / 16) .. +3 of pixel lane % 16.
-  f32x4_t acc[4][4];
+  // of its TO / 2).  A lane holds outputs 4 (lane / 16) .. +3 of pixel
+  // lane % 16.
+  f32x4_t acc[4][OT];
 #pragma unroll
   for (int pt = 0; pt < 4; ++pt)
 #pragma unroll
-    for (int ot = 0; ot < 4; ++ot) acc[pt][ot] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int ot = 0; ot < OT; ++ot) acc[pt][ot] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int pt = 0; pt < 4; ++pt)
 #pragma unroll
-    for (int ot = 0; ot < 4; ++ot) acc_fence(acc[pt][ot]);
+    for (int ot = 0; ot < OT; ++ot) acc_fence(acc[pt][ot]);
   mfma_drain();  // the zero writes land before the first MFMA reads them
   // B fragment (activations): pixel lane % 16, channels 8 (4 s + lane / 16) ..
   const uint32_t xl = static_cast<uint32_t>(lane & 15), xk = static_cast<uint32_t>(lane >> 4);
@@ -362,7 +373,7 @@ __device__ __forceinline__ void tap_tile_body(const TParams& p, uint8_t* lds) {
   w_fence(std::integral_constant<int, 0>{});
   for (int u = 0; u < UPL; ++u) permute_unit(std::integral_constant<int, 0>{}, u);
   if constexpr (!FULL)
-    for (int i = 0; i < 4; ++i) zero_piece(lds + NX * kXB, i);
+    for (int i = 0; i < RPW / 8; ++i) zero_piece(lds + NX * kXB, i);
   for (int u = 0; u < UPL; ++u)
     for (int e = 0; e < 8; ++e) scatter_e(lds + NX * kXB, std::integral_constant<int, 0>{}, u, e);
   lds_barrier();
@@ -384,25 +395,24 @@ __device__ __forceinline__ void tap_tile_body(const TParams& p, uint8_t* lds) {
     const bool issue = ST || j + RW < nch;
     const bool next = ST || j + 1 < nch;
     const uint8_t* xb = lds + (j % NX) * kXB + wp * 8192;
-    const uint8_t* wb = lds + NX * kXB + (j & 1) * kWB + wo * 8192 + lane * 16;
-    uint8_t* tb = lds + NX * kXB + ((j + 1) & 1) * kWB;
-    bf16x8_t fa[4], fb[4], ga[4], gb[4];
+    const uint8_t* wb = lds + NX * kXB + (j & 1) * WB + wo * (OT * 2048) + lane * 16;
+    uint8_t* tb = lds + NX * kXB + ((j + 1) & 1) * WB;
+    bf16x8_t fa[OT], fb[4], ga[OT], gb[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      fb[q] = ld(xb + q * 2048 + boff0);
-      fa[q] = ld(wb + (2 * q) * 1024);
-    }
+    for (int q = 0; q < 4; ++q) fb[q] = ld(xb + q * 2048 + boff0);
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      mfma_acc(acc[i >> 2][i & 3], fa[i & 3], fb[i >> 2]);
+    for (int q = 0; q < OT; ++q) fa[q] = ld(wb + (2 * q) * 1024);
+#pragma unroll
+    for (int i = 0; i < NMF; ++i) {
+      mfma_acc(acc[i / OT][i % OT], fa[i % OT], fb[i / OT]);
       __builtin_amdgcn_sched_barrier(0);
-      if (i < 4) ga[i] = ld(wb + (2 * i + 1) * 1024);
-      if (i >= 4 && i < 8) gb[i - 4] = ld(xb + (i - 4) * 2048 + boff1);
+      if (i < OT) ga[i] = ld(wb + (2 * i + 1) * 1024);
+      if (i >= OT && i < OT + 4) gb[i - OT] = ld(xb + (i - OT) * 2048 + boff1);
       if constexpr (!FULL) {
-        if (i >= 8 && i < 12 && next) zero_piece(tb, i - 8);
+        if (i >= NMF / 2 && i < NMF / 2 + RPW / 8 && next) zero_piece(tb, i - NMF / 2);
       }
-      if (i == 12 && issue) load_w(j + RW, kc);
-      if (i == 13 && issue) issue_x((j + RW) % NX);
+      if (i == NMF - 4 && issue) load_w(j + RW, kc);
+      if (i == NMF - 3 && issue) issue_x((j + RW) % NX);
       __builtin_amdgcn_sched_barrier(0);
     }
     if (next) {
@@ -416,14 +426,14 @@ __device__ __forceinline__ void tap_tile_body(const TParams& p, uint8_t* lds) {
       for (int u = 0; u < UPL; ++u) permute_unit(std::integral_constant<int, k1>{}, u);
     }
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      mfma_acc(acc[i >> 2][i & 3], ga[i & 3], gb[i >> 2]);
+    for (int i = 0; i < NMF; ++i) {
+      mfma_acc(acc[i / OT][i % OT], ga[i % OT], gb[i / OT]);
       __builtin_amdgcn_sched_barrier(0);
       if (next) {
-        // step q of the 8 UPL stores goes to slot q * 16 / (8 UPL)
+        // step q of the 8 UPL stores goes to slot q * NMF / (8 UPL)
 #pragma unroll
         for (int q = 0; q < 8 * UPL; ++q)
-          if ((q * 16) / (8 * UPL) == i) scatter_e(tb, std::integral_constant<int, k1>{}, q >> 3, q & 7);
+          if ((q * NMF) / (8 * UPL) == i) scatter_e(tb, std::integral_constant<int, k1>{}, q >> 3, q & 7);
       }
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -442,44 +452,46 @@ __device__ __forceinline__ void tap_tile_body(const TParams& p, uint8_t* lds) {
   });
 
   // ---- fused epilogue -----------------------------------------------------------
-  // Each wave parks its 64 pixels x 64 outputs (fp32) in its own LDS region
-  // (pitch 272 bytes: conflict-free both ways) and reads them back by pixel
-  // rows: a lane then owns 8 consecutive outputs of one pixel (8 lanes cover
-  // the wave's 64), applies scale / bias / residual / ReLU in fp32, rounds
-  // once and stores 16 (bf16) or 32 bytes.  (The loop's last barrier has
-  // released the operand buffers.)
+  // Each wave parks its 64 pixels x TO/2 outputs (fp32) in its own LDS region
+  // (pitch TO/2 * 4 + 16 bytes: conflict-free both ways) and reads them back
+  // by pixel rows: a lane then owns 8 consecutive outputs of one pixel (LPR
+  // lanes cover the wave's TO/2), applies scale / bias / residual / ReLU in
+  // fp32, rounds once and stores 16 (bf16) or 32 bytes.  (The loop's last
+  // barrier has released the operand buffers.)
+  constexpr int LPR = TO / 16;   // lanes per pixel row
+  constexpr int RPP = 64 / LPR;  // rows per pass (LPR passes)
   mfma_drain();  // the last MFMAs have written acc
 #pragma unroll
   for (int pt = 0; pt < 4; ++pt)
 #pragma unroll
-    for (int ot = 0; ot < 4; ++ot) acc_fence(acc[pt][ot]);
+    for (int ot = 0; ot < OT; ++ot) acc_fence(acc[pt][ot]);
   constexpr uint32_t ysz = sizeof(YT);
-  uint8_t* stg = lds + w * 64 * kEpPitch;
+  uint8_t* stg = lds + w * 64 * PITCH;
   const __amdgpu_buffer_rsrc_t yr =
       __builtin_amdgcn_make_buffer_rsrc(p.Y, (short)0, static_cast<int>(p.y_bytes), kRsrcWord3);
   const __amdgpu_buffer_rsrc_t rsr = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<void*>(p.residual), (short)0, p.residual ? static_cast<int>(p.y_bytes) : 0, kRsrcWord3);
-  const int c8 = lane & 7;  // 8-output block of the wave's 64
-  const uint32_t o = ob * kTO + static_cast<uint32_t>(wo * 64 + 8 * c8);
+  const int c8 = lane % LPR;  // 8-output block of the wave's TO/2
+  const uint32_t o = ob * TO + static_cast<uint32_t>(wo * (TO / 2) + 8 * c8);
   const auto row_off = [&](int rr) {  // Y / residual byte offset of the lane's row rr
-    const uint32_t px = pb * kTP + static_cast<uint32_t>(wp * 64 + 8 * rr + (lane >> 3));
+    const uint32_t px = pb * kTP + static_cast<uint32_t>(wp * 64 + RPP * rr + lane / LPR);
     return px < static_cast<uint32_t>(p.N) ? (px * static_cast<uint32_t>(p.O) + o) * ysz : kOOB;
   };
-  // bf16 residual: all 8 rows' 16-byte pieces are requested before the
+  // bf16 residual: all rows' 16-byte pieces are requested before the
   // accumulators are parked (one load latency, not one per row)
-  u32x4_t rres[8];
+  u32x4_t rres[LPR];
   if constexpr (ysz == 2) {
     if (p.residual) {
 #pragma unroll
-      for (int rr = 0; rr < 8; ++rr)
+      for (int rr = 0; rr < LPR; ++rr)
         rres[rr] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rsr, row_off(rr), 0, 0));
     }
   }
 #pragma unroll
   for (int pt = 0; pt < 4; ++pt)
 #pragma unroll
-    for (int ot = 0; ot < 4; ++ot)
-      *reinterpret_cast<f32x4_t*>(stg + (pt * 16 + (lane & 15)) * kEpPitch + (ot * 16 + 4 * (lane >> 4)) * 4) =
+    for (int ot = 0; ot < OT; ++ot)
+      *reinterpret_cast<f32x4_t*>(stg + (pt * 16 + (lane & 15)) * PITCH + (ot * 16 + 4 * (lane >> 4)) * 4) =
           acc[pt][ot];
   f32x4_t sc0{1.f, 1.f, 1.f, 1.f}, sc1{1.f, 1.f, 1.f, 1.f}, bi0{0.f, 0.f, 0.f, 0.f}, bi1{0.f, 0.f, 0.f, 0.f};
   if (p.scale) {
@@ -492,9 +504,9 @@ __device__ __forceinline__ void tap_tile_body(const TParams& p, uint8_t* lds) {
   }
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's staging writes have landed
 #pragma unroll
-  for (int rr = 0; rr < 8; ++rr) {
-    const int row = 8 * rr + (lane >> 3);
-    const uint8_t* src = stg + row * kEpPitch + c8 * 32;
+  for (int rr = 0; rr < LPR; ++rr) {
+    const int row = RPP * rr + lane / LPR;
+    const uint8_t* src = stg + row * PITCH + c8 * 32;
     f32x4_t y0 = *reinterpret_cast<const f32x4_t*>(src);
     f32x4_t y1 = *reinterpret_cast<const f32x4_t*>(src + 16);
     const uint32_t off = row_off(rr);
@@ -540,46 +552,53 @@ __device__ __forceinline__ void tap_tile_body(const TParams& p, uint8_t* lds) {
   }
 }
 
-template <typename YT, int UPL, bool FULL, bool BIGG, bool MASK, int NX>
+template <typename YT, int UPL, bool FULL, bool BIGG, bool MASK, int NX, int TO>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NX == 3 ? 2 : 1, NX == 3 ? 2 : 1)))
 void tap_tile_kernel(TParams p) {
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
-  tap_tile_body<YT, UPL, FULL, BIGG, MASK, NX>(p, lds);
+  tap_tile_body<YT, UPL, FULL, BIGG, MASK, NX, TO>(p, lds);
 }
 
-template <typename YT, int UPL, bool FULL, bool BIGG, bool MASK, int NX>
-hipError_t launch_tn(const TParams& p, uint32_t grid, hipStream_t s) {
+template <typename YT, int UPL, bool FULL, bool BIGG, bool MASK, int NX, int TO>
+hipError_t launch_tn(const TParams& p, hipStream_t s) {
   static std::atomic<int8_t> lds_set[kMaxDevices];
   const hipError_t attr = set_lds_limit_once(
-      lds_set, reinterpret_cast<const void*>(&tap_tile_kernel<YT, UPL, FULL, BIGG, MASK, NX>), lds_bytes(NX));
+      lds_set, reinterpret_cast<const void*>(&tap_tile_kernel<YT, UPL, FULL, BIGG, MASK, NX, TO>), lds_bytes(NX, TO));
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((tap_tile_kernel<YT, UPL, FULL, BIGG, MASK, NX>), dim3(8u * static_cast<uint32_t>(p.grid8)),
-                     dim3(kThreads), lds_bytes(NX), s, p);
+  hipLaunchKernelGGL((tap_tile_kernel<YT, UPL, FULL, BIGG, MASK, NX, TO>), dim3(8u * static_cast<uint32_t>(p.grid8)),
+                     dim3(kThreads), lds_bytes(NX, TO), s, p);
   return hipGetLastError();
 }
 
 // Two workgroups per CU once the grid covers every CU twice; below that,
 // one per CU with the deeper prefetch.
-template <typename YT, int UPL, bool FULL, bool BIGG, bool MASK>
-hipError_t launch_tu(const TParams& p, uint32_t grid, hipStream_t s) {
-  return grid >= kDeepGrid ? launch_tn<YT, UPL, FULL, BIGG, MASK, 3>(p, grid, s)
-                           : launch_tn<YT, UPL, FULL, BIGG, MASK, 4>(p, grid, s);
+template <typename YT, int UPL, bool FULL, bool BIGG, bool MASK, int TO>
+hipError_t launch_tu(const TParams& p, hipStream_t s) {
+  return static_cast<uint32_t>(p.ntiles) >= kDeepGrid ? launch_tn<YT, UPL, FULL, BIGG, MASK, 3, TO>(p, s)
+                                                       : launch_tn<YT, UPL, FULL, BIGG, MASK, 4, TO>(p, s);
 }
 
-template <typename YT, bool BIGG>
-hipError_t launch_tg(const TParams& p, uint32_t grid, hipStream_t s) {
-  // units per wave: 8 rows_w; per lane: rows_w / 8, rounded up
-  if (p.rows_w < 8) return launch_tu<YT, 1, false, BIGG, true>(p, grid, s);
-  if (p.rows_w == 8) return launch_tu<YT, 1, false, BIGG, false>(p, grid, s);
-  if (p.rows_w < 16) return launch_tu<YT, 2, false, BIGG, true>(p, grid, s);
-  if (p.rows_w == 16) return launch_tu<YT, 2, false, BIGG, false>(p, grid, s);
-  return launch_tu<YT, 2, false, BIGG, false>(p, grid, s);  // (rows_w <= 16: at most half of a group kept)
+template <typename YT, bool BIGG, int TO>
+hipError_t launch_tg(const TParams& p, hipStream_t s) {
+  // units per wave: 8 rows_w; per lane: rows_w / 8, rounded up (rows_w <= 16:
+  // at most half of a group kept)
+  if (p.rows_w < 8) return launch_tu<YT, 1, false, BIGG, true, TO>(p, s);
+  if (p.rows_w == 8) return launch_tu<YT, 1, false, BIGG, false, TO>(p, s);
+  if constexpr (TO == 128) {
+    if (p.rows_w < 16) return launch_tu<YT, 2, false, BIGG, true, TO>(p, s);
+    return launch_tu<YT, 2, false, BIGG, false, TO>(p, s);
+  }
+  return hipErrorInvalidConfiguration;  // (TO = 64: rows_w <= 8)
 }
 
 template <typename YT>
-hipError_t launch_ty(const TParams& p, uint32_t grid, hipStream_t s) {
-  if (p.K == p.G) return launch_tu<YT, 4, true, false, false>(p, grid, s);
-  return p.G == 32 ? launch_tg<YT, true>(p, grid, s) : launch_tg<YT, false>(p, grid, s);
+hipError_t launch_ty(const TParams& p, hipStream_t s, int to) {
+  if (to == 64) {
+    if (p.K == p.G) return launch_tu<YT, 2, true, false, false, 64>(p, s);
+    return launch_tg<YT, false, 64>(p, s);
+  }
+  if (p.K == p.G) return launch_tu<YT, 4, true, false, false, 128>(p, s);
+  return p.G == 32 ? launch_tg<YT, true, 128>(p, s) : launch_tg<YT, false, 128>(p, s);
 }
 
 }  // namespace
@@ -590,7 +609,9 @@ bool tap_tile_supports(const ProductArgs& a) {
   // at most half of each group kept, or all of it (dense control): above
   // that the packed units no longer fit the registers beside the rings
   if (2 * a.K > a.G && a.K != a.G) return false;
-  if (a.O % kTO != 0 || a.N < 1) return false;
+  // O % 128 (tiles of 128 outputs), or O % 64 with G <= 16 (tiles of 64: a
+  // group must fit one wave's 16 rows)
+  if (a.N < 1 || a.O % 64 != 0 || (a.O % 128 != 0 && a.G > 16)) return false;
   const int64_t cin = a.conv ? a.geom.Cin : a.C;
   if (cin % kCK != 0) return false;
   if (a.conv && a.geom.KH * a.geom.KW > kMaxTaps) return false;
@@ -651,16 +672,21 @@ hipError_t launch_tap_tile(const ProductArgs& a, hipStream_t s) {
   p.K = a.K;
   p.relu = a.relu;
   p.npb = static_cast<int32_t>((a.N + kTP - 1) / kTP);
-  p.nob = static_cast<int32_t>(a.O / kTO);
+  // 128-output tiles, unless O is not a multiple of 128 or they would leave
+  // more than half of the CUs idle and 64-output ones are possible (measured:
+  // 3136 x 4608 x 512, 100 tiles, 51 -> 44 us; at 196 tiles the 64-output
+  // plan is 10-15% slower)
+  const int64_t grid128 = a.O % 128 == 0 ? static_cast<int64_t>(p.npb) * (a.O / 128) : 0;
+  const int to = a.O % 128 == 0 && (grid128 >= kSmallGrid || a.G > 16) ? 128 : 64;
+  p.nob = static_cast<int32_t>(a.O / to);
   p.nch = static_cast<int32_t>(a.C / kCK);
   p.cpt = p.Cin / kCK;
-  p.rows_w = 32 * a.K / a.G;
+  p.rows_w = to / 4 * a.K / a.G;
   const int64_t grid = static_cast<int64_t>(p.npb) * p.nob;
   if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
   p.ntiles = static_cast<int32_t>(grid);
   p.grid8 = static_cast<int32_t>((grid + 7) / 8);
-  const uint32_t g = static_cast<uint32_t>(grid);  // (the plan's choice counts real tiles)
-  return a.y_t == DType::BF16 ? launch_ty<bf16_t>(p, g, s) : launch_ty<float>(p, g, s);
+  return a.y_t == DType::BF16 ? launch_ty<bf16_t>(p, s, to) : launch_ty<float>(p, s, to);
 }
 
 }  // namespace cci

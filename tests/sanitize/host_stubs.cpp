@@ -29,8 +29,8 @@ bool resident_supports(const ProductArgs& a) {
 hipError_t launch_resident(const ProductArgs&, hipStream_t) { ++g_launches; return hipSuccess; }
 bool tap_tile_supports(const ProductArgs& a) {
   const int64_t cin = a.conv ? a.geom.Cin : a.C;
-  return a.x_t == DType::BF16 && cin % 64 == 0 && a.O % 128 == 0 && 32 % a.G == 0 &&
-         (2 * a.K <= a.G || a.K == a.G);
+  return a.x_t == DType::BF16 && cin % 64 == 0 && 32 % a.G == 0 && (2 * a.K <= a.G || a.K == a.G) &&
+         (a.O % 128 == 0 || (a.O % 64 == 0 && a.G <= 16));
 }
 hipError_t launch_tap_tile(const ProductArgs&, hipStream_t) { ++g_launches; return hipSuccess; }
 hipError_t launch_bbs_pack(const float*, int64_t, int64_t, int32_t, int32_t, void*, DType, uint8_t*, hipStream_t) {

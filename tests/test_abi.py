@@ -126,9 +126,10 @@ def test_resident_algo_requirements():
 
 
 def test_tap_tile_algo_requirements():
-    # tap-tile MFMA: bf16, Cin (FC: C) % 64 == 0, O % 128 == 0, 32 % G == 0, at most 32 taps
+    # tap-tile MFMA: bf16, Cin (FC: C) % 64 == 0, O % 128 == 0 (O % 64 == 0 with G <= 16), 32 % G == 0,
+    # 2 K <= G or K == G, at most 32 taps
     Tt = cci.ALGO_TAP_TILE_MFMA
-    for C, O, G, K in [(96, 128, 8, 2), (64, 64, 8, 2), (64, 128, 64, 2), (64, 192, 8, 2), (64, 128, 8, 5)]:
+    for C, O, G, K in [(96, 128, 8, 2), (64, 96, 8, 2), (64, 128, 64, 2), (64, 192, 32, 2), (64, 128, 8, 5)]:
         assert lib.cci_spmm_algo(FAKE, cci.BF16, 4, C, FAKE, cci.BF16, FAKE, O, G, K, None, FAKE,
                                  cci.BF16, Tt, None) == cci.EUNSUPPORTED
     assert lib.cci_spmm_algo(FAKE, cci.F32, 4, 64, FAKE, cci.F32, FAKE, 128, 8, 2, None, FAKE,

@@ -194,6 +194,11 @@ TAP_CASES = [  # B, H, W, Cin, O, KH, KW, stride, pad, G, K
     (1, 1, 1, 64, 128, 3, 3, 1, 1, 8, 2),      # one pixel: every tap but the centre in the padding
     (10, 60, 60, 64, 128, 3, 3, 1, 1, 8, 2),   # 282 workgroups: two per CU
     (4, 30, 30, 128, 256, 3, 3, 1, 1, 16, 4),  # 226 workgroups: one per CU
+    (2, 9, 11, 64, 64, 3, 3, 1, 1, 8, 2),      # 64 outputs: 64-output tiles
+    (3, 14, 14, 128, 192, 3, 3, 2, 1, 16, 4),  # 192 outputs: three 64-output tiles
+    (16, 28, 28, 64, 64, 3, 3, 1, 1, 8, 2),    # 98 pixel blocks x 1: 64-output tiles, one per CU
+    (40, 28, 28, 64, 64, 3, 3, 2, 1, 4, 2),    # 245 pixel blocks of 64-output tiles
+    (12, 40, 40, 64, 320, 1, 1, 1, 0, 16, 8),  # 150 x 5 = 750 tiles of 64 outputs: two per CU
 ]
 
 
@@ -222,10 +227,10 @@ def test_conv_tap_tile_epilogue(y_dtype):
 
 
 def test_conv_tap_tile_refuses_unsupported():
-    """Cin % 64 != 0, O % 128 != 0 and G = 64 are refused by the tap-chunk family."""
+    """Cin % 64 != 0, O % 64 != 0, G = 64, and G = 32 with O % 128 != 0 are refused by the tap-chunk family."""
     need_gpu()
     from paper_1910_11971_amd import cci
-    for Cin, O, G in [(96, 128, 8), (64, 64, 8), (64, 128, 64)]:
+    for Cin, O, G in [(96, 128, 8), (64, 96, 8), (64, 128, 64), (64, 192, 32)]:
         X = rand_x((1, 5, 5, Cin), torch.bfloat16, 81).to(DEV)
         vals, idx = cci.pack(torch.from_numpy(rand_w(O, 9 * Cin, 82)).to(DEV), G, 2, torch.bfloat16)
         with pytest.raises(cci.CCIError):

@@ -104,6 +104,8 @@ TAP_FC_CASES = [  # N, C, O, G, K: FC products on the tap-chunk kernels
     (300, 128, 128, 8, 4), (300, 128, 128, 32, 16),
     # >= 257 workgroups: two workgroups per CU (the rest: one per CU)
     (33024, 64, 128, 8, 2), (33024, 128, 128, 32, 5), (16500, 192, 256, 16, 16), (40000, 320, 128, 4, 2),
+    # 64-output tiles: O % 128 != 0, or fewer than 256 tiles of 128 outputs
+    (500, 256, 320, 8, 2), (40000, 128, 64, 8, 2), (3000, 512, 512, 16, 4), (777, 192, 192, 16, 16),
 ]
 
 

@@ -259,31 +259,40 @@ cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C, int
       O % G == 0)
     return CCI_ALGO_RESIDENT_MFMA;
   const bool mac_g = G == 2 || G == 4 || G == 8 || G == 16 || G == 32;
-  // Short reductions the tile kernels cannot take (Cin % 32 != 0) stream
-  // through register-resident weights: 1x1 layers and FC products with
-  // C % 8 == 0, and convolutions over 4 input channels (an even KW) or a
-  // multiple of 8.
-  // It also beats the tile kernels on large 1x1 / FC products with C <= 128
-  // (measured at 50 K - 800 K rows: 64 -> 256 and 128 -> 128 at 200 K rows
-  // 8-20% faster; at C = 256, or below 100 K rows, the tile kernels win).
   const bool narrow_shape = x_t == CCI_BF16 && val_t == CCI_BF16 && C <= 256 && C % 8 == 0 && O % 4 == 0 &&
                             (cin == 4 || cin % 8 == 0);
-  if (narrow_shape && (cin % 32 != 0 || (C == cin && C <= 128 && N >= 100000))) return CCI_ALGO_NARROW_MFMA;
-  // FC and 1x1 products that fill the chip with 256 x 256 tiles (>= 128 of
-  // them) run on the wide-tile kernels: 2.2-2.4x the dense-tile kernel on
-  // 4096^3, and ahead of the tap-chunk kernels on ResNet-50's 1x1 layers
-  // with 196 such tiles (19.5 vs 21.8 us at 12544 x 256 x 1024).
+  // The tap-chunk kernels (128 x 128 or 128 x 64 tiles, reduction in
+  // 64-channel chunks under one filter tap): every k x k convolution over a
+  // multiple of 64 channels into a multiple of 128 outputs, strided 1x1
+  // layers, and FC / 1x1 products the wide-tile kernels do not fill the chip
+  // with.  Measured on ResNet-50's layers at batch 64 against the previous
+  // choice: 3x3 stride 2 28.9 vs 112.6 us (Cin 128), 31.5 vs 109.1 us (Cin
+  // 256), 45 vs 99 us (Cin 512); 3x3 stride 1 28.6 vs 38.4 us (Cin 128);
+  // strided 1x1 26-36 vs 37-45 us; 12544 x 1024 x 256 18.5 vs 23.3 us; the
+  // bottleneck 1x1 layers with their residual add 52 vs 64 us (64 -> 256,
+  // 200 704 pixels) and 35 vs 39 us (128 -> 512, 50 176 pixels).
+  // A reduction of one 64-channel chunk leaves the pipeline empty: such
+  // products go to the tap-chunk kernels only at >= 100 K rows (MobileNetV2's
+  // 12544 x 64 -> 384: 9.4 us there, 8.0 us on the dense-tile kernels).
+  const bool tap_fits = x_t == CCI_BF16 && val_t == CCI_BF16 && G >= 1 && 32 % G == 0 && (2 * K <= G || K == G) &&
+                        cin % 64 == 0 && O % 128 == 0 && C / cin <= 32;
+  const bool tap_shape = tap_fits && C >= 128;
+  // Short reductions the tile kernels cannot take (Cin % 32 != 0) stream
+  // through register-resident weights (narrow kernels): 1x1 layers and FC
+  // products with C % 8 == 0, and convolutions over 4 input channels (an
+  // even KW) or a multiple of 8.  Large 1x1 / FC products with C <= 128 do
+  // too (8-20% ahead of the dense-tile kernels at 50 K - 800 K rows) unless
+  // the tap-chunk kernels take them (64 -> 256 at 200 K rows: 40 us either
+  // way without a residual, 52 vs 64 us with one).
+  const bool narrow_large = C == cin && C <= 128 && N >= 100000;
+  if (tap_fits && narrow_large) return CCI_ALGO_TAP_TILE_MFMA;
+  if (narrow_shape && (cin % 32 != 0 || narrow_large)) return CCI_ALGO_NARROW_MFMA;
+  // FC and 1x1 products with a reduction of >= 256 that fill the chip with
+  // 256 x 256 tiles (>= 128 of them) run on the wide-tile kernels: 2.2-2.4x
+  // the dense-tile kernel on 4096^3, and level with the tap-chunk kernels on
+  // ResNet-50's 1x1 layers with 196 such tiles.
   const int64_t tiles256 = (N + 255) / 256 * (O / 256);
-  if (bf && C == cin && C % 64 == 0 && C >= 128 && O % 256 == 0 && tiles256 >= 128) return CCI_ALGO_WIDE_TILE_MFMA;
-  // Fewer output tiles, and every k x k convolution over a multiple of 64
-  // channels, run on the tap-chunk kernels (128 x 128 tiles): measured on
-  // ResNet-50's layers at batch 64 against the dense-tile kernel, 3x3
-  // stride 2 28.9 vs 112.6 us (Cin 128), 31.5 vs 109.1 us (Cin 256), 51.9
-  // vs 99.0 us (Cin 512); 3x3 stride 1 28.6 vs 38.4 us (Cin 128); strided
-  // 1x1 26-36 vs 37-45 us; and 12544 x 1024 x 256 at 18.5 us against 23.3
-  // us on the wide-tile kernels (49 tiles of 256 x 256).
-  const bool tap_shape = x_t == CCI_BF16 && val_t == CCI_BF16 && G >= 1 && 32 % G == 0 && (2 * K <= G || K == G) &&
-                         cin % 64 == 0 && O % 128 == 0 && C >= 128 && C / cin <= 32;
+  if (bf && C == cin && C % 64 == 0 && C >= 256 && O % 256 == 0 && tiles256 >= 128) return CCI_ALGO_WIDE_TILE_MFMA;
   if (tap_shape) return CCI_ALGO_TAP_TILE_MFMA;
   const bool tile_shape = bf && cin % 32 == 0;
   if (tile_shape && (32 * static_cast<int64_t>(K) > G || !mac_g)) return CCI_ALGO_DENSE_TILE_MFMA;

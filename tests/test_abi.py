@@ -201,8 +201,8 @@ def test_auto_algo_cost_model():
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 4096, 4096, 4096, 4096, 16, 1) == "wide_tile_mfma"
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 4096, 4096, 4096, 4096, 64, 1) == "wide_tile_mfma"
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 12544, 256, 256, 1024, 16, 4) == "wide_tile_mfma"
-    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 50176, 128, 128, 512, 8, 2) == "wide_tile_mfma"
-    # fewer tiles: the tap-chunk kernels (two 128 x 128 tiles per CU)
+    # fewer tiles, or a reduction of 128 or less: the tap-chunk kernels (two 128 x 128 tiles per CU)
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 50176, 128, 128, 512, 8, 2) == "tap_tile_mfma"
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 12544, 1024, 1024, 256, 16, 4) == "tap_tile_mfma"
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 6000, 1024, 1024, 256, 16, 4) == "tap_tile_mfma"
     # G the vector kernels do not support: the tile path even at K/G < 1/32
@@ -217,10 +217,13 @@ def test_auto_algo_cost_model():
     # small-Cin convs read through implicit im2col (a stem padded to 4 channels and KW = 8)
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 802816, 224, 4, 64, 8, 8) == "narrow_mfma"
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 5000, 216, 24, 64, 8, 2) == "narrow_mfma"
-    # large 1x1 products with C <= 128 too; C = 256 or fewer rows stay on the tile kernels
-    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 200704, 64, 64, 256, 8, 2) == "narrow_mfma"
+    # large 1x1 products with C <= 128 too, unless the tap-chunk kernels take them (O % 128 == 0);
+    # C = 256 or fewer rows stay on the tile kernels
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 200704, 128, 128, 96, 8, 2) == "narrow_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 200704, 64, 64, 256, 8, 2) == "tap_tile_mfma"
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 200704, 256, 256, 64, 8, 2) == "dense_tile_mfma"
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 12544, 64, 64, 384, 8, 2) == "dense_tile_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 12544, 64, 64, 96, 8, 2) == "dense_tile_mfma"
 
 
 @pytest.mark.skipif(torch.cuda.is_available(), reason="checks the no-device error path only")

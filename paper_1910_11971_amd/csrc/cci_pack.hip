@@ -21,16 +21,27 @@ template <> __device__ __forceinline__ void put<bf16_t>(bf16_t* p, int64_t i, fl
   p[i].bits = f32_to_bf16_rne(w);
 }
 
-// Register-resident group (G known at compile time).  The rank of row r is
-// the number of rows that beat it (larger |w|, or equal |w| and a lower
-// row); each pair of rows is compared once and credits one of the two.  (For
-// K < (G - 1) / 2 the K winners are taken one at a time instead: the same
-// set, in fewer operations; the ranking is vector-ALU work comparable to
-// the kernel's HBM time.)
+// Register-resident group (G known at compile time, a power of two).
+//
+// The order is |w| descending, then row ascending.  Each key gets its row in
+// its low log2(G) bits, (|w| with those bits cleared) | (G - 1 - r): the keys
+// are then distinct, and they order the rows exactly as |w| does wherever
+// two |w| differ above those bits.  With distinct keys the next largest key
+// below p is p - 1 - min_r(p - 1 - key_r) in unsigned arithmetic (keys below
+// p give p - 1 - key_r < p; the others wrap past 2^31), two operations per
+// row and round; the next smallest above p likewise.  min(K, G - K) + 1
+// rounds find the boundary of the kept set from the nearer end, and the kept
+// set is the exact one unless the last kept and the first dropped key agree
+// above the row bits: such columns (ties, or |w| closer than 2^-19 relative)
+// are ranked exactly, each pair of rows compared once.
 // The kept rows form a bit mask; slot k then takes the k-th lowest kept row,
 // so each slot is one store of consecutive columns (coalesced), its value
-// re-read from the cache lines just loaded.  With K = G every row is kept in
-// order (the dense control): a copy.
+// re-read from the cache lines just loaded (four slots' loads in flight at
+// once).  With K = G every row is kept in order (the dense control): a copy.
+template <int G> struct RowBits {
+  static constexpr int value = G == 2 ? 1 : G == 4 ? 2 : G == 8 ? 3 : G == 16 ? 4 : 5;
+};
+
 template <int G, typename VT>
 __global__ __launch_bounds__(kPackThreads) void pack_fixed(const float* __restrict__ W, int64_t C,
                                                            int64_t cblocks, int32_t K,
@@ -50,32 +61,46 @@ __global__ __launch_bounds__(kPackThreads) void pack_fixed(const float* __restri
     }
     return;
   }
+  constexpr int kRB = RowBits<G>::value;
+  constexpr uint32_t kRM = (1u << kRB) - 1u;
+  static_assert((1 << kRB) == G, "G must be a power of two up to 32");
   uint32_t key[G];
 #pragma unroll
-  for (int r = 0; r < G; ++r) key[r] = abs_bits(col[r * C]);
+  for (int r = 0; r < G; ++r) key[r] = (abs_bits(col[r * C]) & ~kRM) | (kRM - r);
   uint32_t kept = 0;
-  if (2 * K + 1 < G) {
-    // Few kept rows: take the largest remaining |w| K times (a strict
-    // comparison scanning up from row 0 keeps the lower row on a tie; a
-    // taken row's key drops below every |w|): 3 G K operations against the
-    // 3 G (G - 1) / 2 of the pairwise rank.
-    int32_t sk[G];
+  bool exact;
+  if (2 * K <= G) {
+    // Largest keys: K rounds, then one more for the first dropped key.
+    uint32_t p = 0x80000000u, last = 0;
+    for (int32_t k = 0; k <= K; ++k) {
+      uint32_t m = 0xffffffffu;
 #pragma unroll
-    for (int r = 0; r < G; ++r) sk[r] = static_cast<int32_t>(key[r]);
-    for (int32_t k = 0; k < K; ++k) {
-      int32_t best = sk[0];
-      int br = 0;
-#pragma unroll
-      for (int r = 1; r < G; ++r) {
-        const bool gt = sk[r] > best;
-        best = gt ? sk[r] : best;
-        br = gt ? r : br;
-      }
-      kept |= 1u << br;
-#pragma unroll
-      for (int r = 0; r < G; ++r) sk[r] = r == br ? -1 : sk[r];
+      for (int r = 0; r < G; ++r) m = min(m, p - 1u - key[r]);
+      last = p;
+      p = p - 1u - m;
+      if (k < K) kept |= 1u << (kRM - (p & kRM));
     }
+    exact = (last >> kRB) != (p >> kRB);
   } else {
+    // Smallest keys: the G - K dropped rows, then the first kept key.
+    const int32_t D = G - K;
+    uint32_t p = 0xffffffffu, last = 0, dropped = 0;
+    for (int32_t k = 0; k <= D; ++k) {
+      uint32_t m = 0xffffffffu;
+#pragma unroll
+      for (int r = 0; r < G; ++r) m = min(m, key[r] - p - 1u);
+      last = p;
+      p = p + 1u + m;
+      if (k < D) dropped |= 1u << (kRM - (p & kRM));
+    }
+    constexpr uint32_t kAll = G == 32 ? 0xffffffffu : (1u << (G & 31)) - 1u;
+    kept = ~dropped & kAll;
+    exact = (last >> kRB) != (p >> kRB);
+  }
+  if (__builtin_expect(!exact, 0)) {
+    uint32_t full[G];
+#pragma unroll
+    for (int r = 0; r < G; ++r) full[r] = abs_bits(col[r * C]);
     int rank[G];
 #pragma unroll
     for (int r = 0; r < G; ++r) rank[r] = 0;
@@ -83,19 +108,30 @@ __global__ __launch_bounds__(kPackThreads) void pack_fixed(const float* __restri
     for (int r = 1; r < G; ++r)
 #pragma unroll
       for (int q = 0; q < r; ++q) {
-        const bool q_wins = key[q] >= key[r];  // q < r: a tie goes to q
+        const bool q_wins = full[q] >= full[r];  // q < r: a tie goes to q
         rank[r] += q_wins ? 1 : 0;
         rank[q] += q_wins ? 0 : 1;
       }
+    kept = 0;
 #pragma unroll
     for (int r = 0; r < G; ++r) kept |= (rank[r] < K ? 1u : 0u) << r;
   }
-  for (int32_t k = 0; k < K; ++k) {
-    const int r = __builtin_ctz(kept);
-    kept &= kept - 1u;
-    const int64_t o = (g * K + k) * C + c;
-    put<VT>(vals, o, col[static_cast<int64_t>(r) * C]);
-    idx[o] = static_cast<uint8_t>(r);
+  for (int32_t k0 = 0; k0 < K; k0 += 4) {
+    int rr[4];
+    float v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      rr[j] = __builtin_ctz(kept | 0x80000000u);
+      kept &= kept - 1u;
+      if (k0 + j < K) v[j] = col[static_cast<int64_t>(rr[j]) * C];
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (k0 + j < K) {
+        const int64_t o = (g * K + k0 + j) * C + c;
+        put<VT>(vals, o, v[j]);
+        idx[o] = static_cast<uint8_t>(rr[j]);
+      }
   }
 }
 

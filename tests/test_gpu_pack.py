@@ -44,9 +44,25 @@ def test_pack_ties_zeros_and_specials(vdt):
     W[0, :5] = [np.inf, -np.inf, np.nan, 3e38, -1e-40]
     run_pack(W.astype(np.float32), 8, 3, vdt)
     run_pack(W.astype(np.float32), 16, 5, vdt)
-    # the take-the-largest-K-times path (K < (G - 1) / 2) and the pairwise rank, on heavy ties
-    for G, K in ((16, 1), (16, 2), (16, 4), (16, 7), (16, 8), (8, 1), (4, 1), (32, 3)):
+    # selection from the top (K <= G / 2) and from the bottom, on heavy ties
+    for G, K in ((16, 1), (16, 2), (16, 4), (16, 7), (16, 8), (16, 12), (8, 1), (8, 6), (4, 1), (32, 3), (32, 24)):
         run_pack(W.astype(np.float32), G, K, vdt)
+
+
+@pytest.mark.parametrize("vdt", [torch.float32, torch.bfloat16])
+def test_pack_near_ties(vdt):
+    # |w| that agree above their last few mantissa bits (columns the kernel re-ranks exactly),
+    # exact ties, and both ends of the selection (K <= G / 2 from the top, K > G / 2 from the bottom)
+    need_gpu()
+    rng = np.random.default_rng(11)
+    base = rng.standard_normal((1, 300)).astype(np.float32).view(np.uint32)
+    low = rng.integers(0, 64, size=(64, 300)).astype(np.uint32)
+    W = ((base & np.uint32(0xffffffc0)) | low).view(np.float32)
+    W = W * rng.choice(np.array([1.0, -1.0], np.float32), size=W.shape)
+    W[:, ::7] = W[0:1, ::7]
+    for G, K in ((2, 1), (4, 1), (4, 3), (8, 3), (8, 5), (16, 1), (16, 4), (16, 8), (16, 9), (16, 15),
+                 (32, 1), (32, 7), (32, 16), (32, 20), (32, 31)):
+        run_pack(np.ascontiguousarray(W), G, K, vdt)
 
 
 @pytest.mark.parametrize("K", [1, 2, 4, 8, 16])

@@ -20,9 +20,12 @@
 //     fragments stream in behind the remaining MFMAs;
 //   - one wave per SIMD issues in order, so the loads and tile writes are
 //     placed between single MFMAs;
-//   - workgroup ids are remapped so that each XCD holds a 4 pixel-block x
-//     8 output-block patch of tiles (tiles that share activations or packed
-//     rows sit behind one L2).
+//   - workgroup ids are remapped so that each XCD holds a patch of tiles of
+//     a few pixel blocks x many output blocks (tiles that share activations
+//     or packed rows sit behind one L2): 4 pixel blocks, or 2 when the
+//     packed rows of an output block are under a quarter of a pixel block's
+//     activations (K / G < 1/6), so that the XCD's share of the larger
+//     operand is fetched fewer times.
 //
 // LDS layouts (bytes):
 //   activation buffer: pixel q at q * 128; its 16-byte column c holds
@@ -76,6 +79,7 @@ struct WParams {
   int32_t npb, nob, nch;  // pixel blocks, output blocks (of 256), channel chunks
   int32_t rows_w;         // packed rows behind 64 outputs: 64 K / G
   int32_t grid8;          // grid / 8 when the grid is a multiple of 8, else 0
+  int32_t pgr;            // pixel blocks per run of the XCD tile order (2 or 4)
 };
 
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
@@ -166,16 +170,17 @@ __device__ __forceinline__ void wide_tile_body(const WParams& p, uint8_t* lds) {
 
   // ---- tile of this workgroup ------------------------------------------------
   // Dispatch places workgroup b on XCD b % 8; L numbers the workgroups of
-  // one XCD consecutively, and runs of 4 * nob consecutive L cover 4 pixel
-  // blocks x every output block, output-block-major.
+  // one XCD consecutively, and runs of pgr * nob consecutive L cover pgr
+  // pixel blocks x every output block, output-block-major.
   const uint32_t bid = blockIdx.x;
   const uint32_t L = p.grid8 ? (bid & 7u) * static_cast<uint32_t>(p.grid8) + (bid >> 3) : bid;
-  const uint32_t per = 4u * static_cast<uint32_t>(p.nob);
+  const uint32_t pgr = static_cast<uint32_t>(p.pgr);
+  const uint32_t per = pgr * static_cast<uint32_t>(p.nob);
   const uint32_t pg = L / per;
-  const uint32_t pgs = min(4u, static_cast<uint32_t>(p.npb) - 4u * pg);
+  const uint32_t pgs = min(pgr, static_cast<uint32_t>(p.npb) - pgr * pg);
   const uint32_t within = L - pg * per;
   const uint32_t ob = within / pgs;
-  const uint32_t pb = 4u * pg + (within - ob * pgs);
+  const uint32_t pb = pgr * pg + (within - ob * pgs);
 
   const __amdgpu_buffer_rsrc_t xr =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(p.X), (short)0, static_cast<int>(p.x_bytes), kRsrcWord3);
@@ -718,6 +723,10 @@ hipError_t launch_wide_tile(const ProductArgs& a, hipStream_t s) {
   const int64_t grid = static_cast<int64_t>(p.npb) * p.nob;
   if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
   p.grid8 = grid % 8 == 0 ? static_cast<int32_t>(grid / 8) : 0;
+  // An XCD running P pixel blocks x (32 / P) output blocks fetches P blocks
+  // of X (256 C bf16 each) and 32 / P blocks of packed rows (256 C K / G
+  // values and indices, 3 bytes each): 2 beats 4 when 8 K / G < 4 / 3.
+  p.pgr = 6 * a.K < a.G ? 2 : 4;
   const uint32_t g = static_cast<uint32_t>(grid);
   if (tp == 256) return a.y_t == DType::BF16 ? launch_wp<bf16_t, 8>(p, g, s) : launch_wp<float, 8>(p, g, s);
   return a.y_t == DType::BF16 ? launch_wp<bf16_t, 4>(p, g, s) : launch_wp<float, 4>(p, g, s);

@@ -56,7 +56,8 @@ def parse():
                    help="fc4096 (the K sweep; default) or one named workload (conv3x3, conv1x1_k4, fc4096_k1, ...)")
     p.add_argument("--k", type=int, default=4, help="fc4096: the K whose step gives `value`")
     p.add_argument("--algo", default="auto", choices=["auto", "sparse_mac", "dense_tile_mfma", "wide_tile_mfma", "narrow_mfma",
-                                                     "resident_mfma", "few_rows_mfma", "tap_tile_mfma"])
+                                                     "resident_mfma", "few_rows_mfma", "tap_tile_mfma",
+                                                     "stream_tile_mfma"])
     p.add_argument("--rotate-mb", type=float, default=600.0,
                    help="total size of rotated X/Y copies (0: no rotation)")
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="target wall time of the CPU oracle sample")
@@ -85,7 +86,7 @@ def parse():
 KERNEL_SOURCES = {"cci_dense_tile": "cci_dense_tile.hip", "cci_wide_tile": "cci_wide_tile.hip",
                   "cci_sparse_mac": "cci_sparse_mac.hip", "cci_narrow": "cci_narrow.hip",
                   "cci_resident": "cci_resident.hip", "cci_bits": "cci_bits.hip",
-                  "cci_tap_tile": "cci_tap_tile.hip"}
+                  "cci_tap_tile": "cci_tap_tile.hip", "cci_stream_tile": "cci_stream_tile.hip"}
 
 
 def kernel_source_hash(kernel: str = "cci_dense_tile") -> str:
@@ -782,7 +783,8 @@ def _eager_time(fn, n, stream):
 def kernel_name(algo):
     return {"dense_tile_mfma": "cci_dense_tile", "wide_tile_mfma": "cci_wide_tile",
             "narrow_mfma": "cci_narrow", "resident_mfma": "cci_resident",
-            "few_rows_mfma": "cci_bits", "tap_tile_mfma": "cci_tap_tile"}.get(algo, "cci_sparse_mac")
+            "few_rows_mfma": "cci_bits", "tap_tile_mfma": "cci_tap_tile",
+            "stream_tile_mfma": "cci_stream_tile"}.get(algo, "cci_sparse_mac")
 
 
 def _dense_time(fn, n_launch, stream, reps=10):
@@ -801,7 +803,8 @@ def roof_for(kname, flop, dense_flop, alg_bytes, t_ms):
     """The matrix-core kernels against the method's own work (own_roof); the
     vector-ALU kernel multiplies only kept weights, so its bound is the fp32
     FMA rate (or HBM, if that takes longer)."""
-    if kname in ("cci_dense_tile", "cci_wide_tile", "cci_narrow", "cci_resident", "cci_bits", "cci_tap_tile"):
+    if kname in ("cci_dense_tile", "cci_wide_tile", "cci_narrow", "cci_resident", "cci_bits", "cci_tap_tile",
+                 "cci_stream_tile"):
         return own_roof(flop, alg_bytes, t_ms, dense_flop)
     t_alu = flop / (PEAK["valu_fp32_TFLOPs"] * 1e12)
     t_hbm = alg_bytes / (PEAK["hbm_GBps"] * 1e9)

@@ -110,7 +110,19 @@ typedef enum { CCI_F32 = 0, CCI_BF16 = 1 } cci_dtype;
  *                           vals, Cin % 64 == 0 (FC: C % 64 == 0), O % 128
  *                           == 0 and 32 % G == 0, or O % 64 == 0 and 16 % G
  *                           == 0; 2 K <= G or K == G; KH*KW <= 32; X, vals
- *                           and Y 16-byte aligned, idx 8-byte aligned. */
+ *                           and Y 16-byte aligned, idx 8-byte aligned.
+ *  CCI_ALGO_STREAM_TILE_MFMA the same expansion, done once per workgroup for
+ *                           all of a 128- (O % 128 == 0) or 64-output tile's
+ *                           reduction and kept in LDS while 128-row tiles of
+ *                           X stream past it, their chunks prefetched two
+ *                           steps ahead and their epilogues overlapping the
+ *                           next tile's loads: short reductions over many
+ *                           rows (the 1x1 layers of a CNN's early stages).
+ *                           FC products and 1x1 convolutions with stride 1
+ *                           and no padding; bf16 X and vals, C % 64 == 0,
+ *                           C <= 256, O % 64 == 0, 32 % G == 0; X 16-byte
+ *                           aligned, Y (and residual) 8-byte aligned for
+ *                           bf16 and 16-byte aligned for fp32 output. */
 typedef enum {
   CCI_ALGO_AUTO = 0,
   CCI_ALGO_SPARSE_MAC = 1,
@@ -119,7 +131,8 @@ typedef enum {
   CCI_ALGO_NARROW_MFMA = 4,
   CCI_ALGO_RESIDENT_MFMA = 5,
   CCI_ALGO_FEW_ROWS_MFMA = 6,
-  CCI_ALGO_TAP_TILE_MFMA = 7
+  CCI_ALGO_TAP_TILE_MFMA = 7,
+  CCI_ALGO_STREAM_TILE_MFMA = 8
 } cci_algo;
 
 /* Optional fused epilogue, applied per output element before rounding:
@@ -208,7 +221,10 @@ cci_status cci_conv_im2col_algo(const void *X, cci_dtype x_t, int64_t B,
  * dense-tile kernels if they take its shape, else on the sparse-MAC ones;
  * one reported as CCI_ALGO_RESIDENT_MFMA or CCI_ALGO_TAP_TILE_MFMA runs on
  * the dense-tile kernels when a stride, alignment or size limit of that
- * family rules it out. */
+ * family rules it out; one reported as CCI_ALGO_STREAM_TILE_MFMA runs on the
+ * tap-chunk kernels (else the dense-tile ones) when its epilogue adds a
+ * residual or its stride, padding or alignment rules the streaming ones
+ * out. */
 cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C,
                        int64_t cin, int64_t O, int32_t G, int32_t K);
 

@@ -90,7 +90,7 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
     return fail(CCI_EALIGN, "epilogue pointer not 16-byte aligned");
   if (algo != CCI_ALGO_AUTO && algo != CCI_ALGO_SPARSE_MAC && algo != CCI_ALGO_DENSE_TILE_MFMA &&
       algo != CCI_ALGO_WIDE_TILE_MFMA && algo != CCI_ALGO_NARROW_MFMA && algo != CCI_ALGO_RESIDENT_MFMA &&
-      algo != CCI_ALGO_FEW_ROWS_MFMA && algo != CCI_ALGO_TAP_TILE_MFMA)
+      algo != CCI_ALGO_FEW_ROWS_MFMA && algo != CCI_ALGO_TAP_TILE_MFMA && algo != CCI_ALGO_STREAM_TILE_MFMA)
     return fail(CCI_EINVAL, "unknown algo %d", (int)algo);
   if (a.N == 0) return ok();
 
@@ -114,6 +114,12 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
     chosen = tile_ok ? CCI_ALGO_DENSE_TILE_MFMA : CCI_ALGO_SPARSE_MAC;
   if (algo == CCI_ALGO_AUTO && chosen == CCI_ALGO_TAP_TILE_MFMA && !cci::tap_tile_supports(a))
     chosen = tile_ok ? CCI_ALGO_DENSE_TILE_MFMA : CCI_ALGO_SPARSE_MAC;
+  // (its residual reads take the accumulator layout: with a residual the
+  // tap-chunk kernels are as fast)
+  if (algo == CCI_ALGO_AUTO && chosen == CCI_ALGO_STREAM_TILE_MFMA && a.residual && cci::tap_tile_supports(a))
+    chosen = CCI_ALGO_TAP_TILE_MFMA;
+  if (algo == CCI_ALGO_AUTO && chosen == CCI_ALGO_STREAM_TILE_MFMA && !cci::stream_tile_supports(a))
+    chosen = cci::tap_tile_supports(a) ? CCI_ALGO_TAP_TILE_MFMA : tile_ok ? CCI_ALGO_DENSE_TILE_MFMA : CCI_ALGO_SPARSE_MAC;
   if (chosen == CCI_ALGO_SPARSE_MAC && !mac_ok)
     return fail(CCI_EUNSUPPORTED, "sparse-MAC kernels need G in {2,4,8,16,32} (G=%d)", a.G);
   if (chosen == CCI_ALGO_DENSE_TILE_MFMA && !tile_ok)
@@ -141,8 +147,13 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
                 "tap-tile MFMA kernels need bf16 X/vals, Cin (FC: C) %% 64 == 0, O %% 128 == 0 with 32 %% G == 0 "
                 "or O %% 64 == 0 with 16 %% G == 0, 2 K <= G or K == G, at most 32 filter taps and aligned "
                 "pointers");
+  if (chosen == CCI_ALGO_STREAM_TILE_MFMA && !cci::stream_tile_supports(a))
+    return fail(CCI_EUNSUPPORTED,
+                "stream-tile MFMA kernels need bf16 X/vals, an FC or stride-1 unpadded 1x1 product, "
+                "C %% 64 == 0 with C <= 256, O %% 64 == 0, 32 %% G == 0 and aligned pointers");
   const hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = chosen == CCI_ALGO_SPARSE_MAC       ? cci::launch_sparse_mac(a, st)
+                 : chosen == CCI_ALGO_STREAM_TILE_MFMA ? cci::launch_stream_tile(a, st)
                  : chosen == CCI_ALGO_TAP_TILE_MFMA  ? cci::launch_tap_tile(a, st)
                  : chosen == CCI_ALGO_WIDE_TILE_MFMA ? cci::launch_wide_tile(a, st)
                  : chosen == CCI_ALGO_RESIDENT_MFMA  ? cci::launch_resident(a, st)
@@ -285,6 +296,13 @@ cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C, int
   // the tap-chunk kernels take them (64 -> 256 at 200 K rows: 40 us either
   // way without a residual, 52 vs 64 us with one).
   const bool narrow_large = C == cin && C <= 128 && N >= 100000;
+  // One 64-channel chunk over >= 100 K rows: the streaming kernels (the
+  // expanded tile expanded once per workgroup, 128-row tiles streamed past
+  // it): 64 -> 256 at 200 704 rows 37 vs 41-48 us, 64 -> 64 16 vs 19.5 us;
+  // level with the tap-chunk kernels when a residual is added.
+  if (x_t == CCI_BF16 && val_t == CCI_BF16 && C == 64 && cin == 64 && N >= 100000 && O % 64 == 0 && G >= 1 &&
+      32 % G == 0)
+    return CCI_ALGO_STREAM_TILE_MFMA;
   if (tap_fits && narrow_large) return CCI_ALGO_TAP_TILE_MFMA;
   if (narrow_shape && (cin % 32 != 0 || narrow_large)) return CCI_ALGO_NARROW_MFMA;
   // FC and 1x1 products with a reduction of >= 256 that fill the chip with

@@ -95,6 +95,13 @@ hipError_t launch_resident(const ProductArgs& a, hipStream_t s);
 bool tap_tile_supports(const ProductArgs& a);
 hipError_t launch_tap_tile(const ProductArgs& a, hipStream_t s);
 
+// FC products and stride-1 1x1 convolutions with 64 <= C <= 256: a workgroup
+// expands its 128 (or 64) outputs' weights over the whole reduction once and
+// streams 128-row tiles of X past them (bf16 X/vals; C % 64 == 0,
+// O % 64 == 0, 32 % G == 0).
+bool stream_tile_supports(const ProductArgs& a);
+hipError_t launch_stream_tile(const ProductArgs& a, hipStream_t s);
+
 // Balanced sparsity (groups of G inputs in one output row) and the 2:4
 // sparse matrix-core product.
 hipError_t launch_bbs_pack(const float* W, int64_t O, int64_t C, int32_t G, int32_t K, void* vals, DType val_t,

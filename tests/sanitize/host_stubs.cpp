@@ -33,6 +33,12 @@ bool tap_tile_supports(const ProductArgs& a) {
          (a.O % 128 == 0 || (a.O % 64 == 0 && a.G <= 16));
 }
 hipError_t launch_tap_tile(const ProductArgs&, hipStream_t) { ++g_launches; return hipSuccess; }
+bool stream_tile_supports(const ProductArgs& a) {
+  return a.x_t == DType::BF16 && a.C % 64 == 0 && a.C <= 256 && a.O % 64 == 0 && 32 % a.G == 0 &&
+         (!a.conv || (a.geom.KH == 1 && a.geom.KW == 1 && a.geom.sh == 1 && a.geom.sw == 1 && a.geom.ph == 0 &&
+                      a.geom.pw == 0));
+}
+hipError_t launch_stream_tile(const ProductArgs&, hipStream_t) { ++g_launches; return hipSuccess; }
 hipError_t launch_bbs_pack(const float*, int64_t, int64_t, int32_t, int32_t, void*, DType, uint8_t*, hipStream_t) {
   ++g_launches;
   return hipSuccess;

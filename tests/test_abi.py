@@ -137,8 +137,21 @@ def test_tap_tile_algo_requirements():
     for Cin, KH, KW in [(32, 3, 3), (64, 7, 7)]:
         assert lib.cci_conv_im2col_algo(FAKE, cci.BF16, 1, 8, 8, Cin, KH, KW, 1, 1, 1, 1, FAKE, cci.BF16,
                                         FAKE, 128, 8, 2, None, FAKE, cci.BF16, Tt, None) == cci.EUNSUPPORTED
+
+
+def test_stream_tile_algo_requirements():
+    # stream-tile MFMA: bf16, FC or stride-1 unpadded 1x1, C % 64 == 0 with C <= 256, O % 64 == 0, 32 % G == 0
+    St = cci.ALGO_STREAM_TILE_MFMA
+    for C, O, G, K in [(96, 128, 8, 2), (320, 128, 8, 2), (64, 96, 8, 2), (64, 128, 64, 2)]:
+        assert lib.cci_spmm_algo(FAKE, cci.BF16, 4, C, FAKE, cci.BF16, FAKE, O, G, K, None, FAKE,
+                                 cci.BF16, St, None) == cci.EUNSUPPORTED
+    assert lib.cci_spmm_algo(FAKE, cci.F32, 4, 64, FAKE, cci.F32, FAKE, 128, 8, 2, None, FAKE,
+                             cci.F32, St, None) == cci.EUNSUPPORTED
+    for k, stride, pad in [(3, 1, 1), (1, 2, 0), (1, 1, 1)]:
+        assert lib.cci_conv_im2col_algo(FAKE, cci.BF16, 1, 8, 8, 64, k, k, stride, stride, pad, pad, FAKE, cci.BF16,
+                                        FAKE, 128, 8, 2, None, FAKE, cci.BF16, St, None) == cci.EUNSUPPORTED
     assert lib.cci_spmm_algo(FAKE, cci.BF16, 4, 64, FAKE, cci.BF16, FAKE, 128, 8, 2, None, FAKE,
-                             cci.BF16, 8, None) == cci.EINVAL
+                             cci.BF16, 9, None) == cci.EINVAL
 
 
 def test_few_rows_algo_requirements():
@@ -220,7 +233,11 @@ def test_auto_algo_cost_model():
     # large 1x1 products with C <= 128 too, unless the tap-chunk kernels take them (O % 128 == 0);
     # C = 256 or fewer rows stay on the tile kernels
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 200704, 128, 128, 96, 8, 2) == "narrow_mfma"
-    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 200704, 64, 64, 256, 8, 2) == "tap_tile_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 200704, 128, 128, 256, 8, 2) == "tap_tile_mfma"
+    # one 64-channel chunk over >= 100 K rows: the streaming kernels
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 200704, 64, 64, 256, 8, 2) == "stream_tile_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 200704, 64, 64, 64, 8, 2) == "stream_tile_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 50176, 64, 64, 256, 8, 2) == "dense_tile_mfma"
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 200704, 256, 256, 64, 8, 2) == "dense_tile_mfma"
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 12544, 64, 64, 384, 8, 2) == "dense_tile_mfma"
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 12544, 64, 64, 96, 8, 2) == "dense_tile_mfma"

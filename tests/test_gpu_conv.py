@@ -237,6 +237,28 @@ def test_conv_tap_tile_refuses_unsupported():
             cci.conv_im2col(X, vals, idx, G, 3, 3, (1, 1), (1, 1), algo="tap_tile_mfma")
 
 
+@pytest.mark.parametrize("B,H,W,Cin,O,G,K,y_dtype", [(4, 30, 30, 128, 256, 8, 2, torch.bfloat16),
+                                                     (3, 17, 13, 64, 192, 16, 4, torch.float32),
+                                                     (2, 28, 28, 256, 64, 8, 2, torch.bfloat16)])
+def test_conv_stream_tile_1x1(B, H, W, Cin, O, G, K, y_dtype):
+    """1x1 stride-1 convolutions on the streaming kernels, every epilogue term."""
+    need_gpu()
+    ep = rand_epilogue(O, B * H * W, y_dtype, 91 + Cin, residual=True, relu=True)
+    run_conv(rand_x((B, H, W, Cin), torch.bfloat16, 92 + O), rand_w(O, Cin, 93 + G), G, K, 1, 1, 0, y_dtype,
+             "stream_tile_mfma", ep=ep)
+
+
+def test_conv_stream_tile_refuses_unsupported():
+    """3x3, strided or padded 1x1 convolutions are not streaming-kernel products."""
+    need_gpu()
+    from paper_1910_11971_amd import cci
+    for k, stride, pad in [(3, 1, 1), (1, 2, 0), (1, 1, 1)]:
+        X = rand_x((1, 9, 9, 64), torch.bfloat16, 95).to(DEV)
+        vals, idx = cci.pack(torch.from_numpy(rand_w(128, k * k * 64, 96)).to(DEV), 8, 2, torch.bfloat16)
+        with pytest.raises(cci.CCIError):
+            cci.conv_im2col(X, vals, idx, 8, k, k, (stride, stride), (pad, pad), algo="stream_tile_mfma")
+
+
 @pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma"])
 def test_conv_epilogue_residual_relu(algo):
     need_gpu()

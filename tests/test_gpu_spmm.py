@@ -115,6 +115,57 @@ def test_spmm_bf16_tap_tile(N, C, O, G, K):
     run_case(rand_x(N, C, torch.bfloat16, N + C), rand_w(O, C, O + G), G, K, torch.bfloat16, "tap_tile_mfma")
 
 
+STREAM_FC_CASES = [  # N, C, O, G, K: FC products on the streaming kernels (C <= 256)
+    (1, 64, 64, 8, 2), (127, 128, 128, 16, 4), (128, 64, 128, 8, 8), (129, 192, 256, 32, 5),
+    (1000, 256, 320, 4, 1), (5000, 192, 192, 2, 2), (3000, 256, 128, 1, 1), (777, 128, 384, 32, 32),
+    # many row tiles per workgroup, 128- and 64-output tiles, a ragged last tile
+    (33001, 64, 256, 8, 2), (40000, 128, 512, 8, 2), (70001, 256, 64, 8, 2), (20000, 192, 128, 16, 3),
+]
+
+
+@pytest.mark.parametrize("N,C,O,G,K", STREAM_FC_CASES)
+def test_spmm_bf16_stream_tile(N, C, O, G, K):
+    need_gpu()
+    run_case(rand_x(N, C, torch.bfloat16, N + C), rand_w(O, C, O + G), G, K, torch.bfloat16, "stream_tile_mfma")
+
+
+@pytest.mark.parametrize("y_dtype", [torch.bfloat16, torch.float32])
+def test_spmm_stream_tile_large_sampled(y_dtype):
+    """ResNet-50 layer1-shaped product (200 704 rows, 64 -> 256) with every
+    epilogue term: a row of every 128-row tile against the oracle, plus the
+    first and last tiles whole."""
+    need_gpu()
+    N, C, O, G, K = 200704, 64, 256, 8, 2
+    rng = np.random.default_rng(31)
+    rows = np.unique(np.concatenate([np.arange(0, 128), np.arange(N - 128, N),
+                                     np.arange(0, N, 128) + rng.integers(0, 128, N // 128)]))
+    ep = rand_epilogue(O, N, y_dtype, 32, residual=True, relu=True)
+    run_case(rand_x(N, C, torch.bfloat16, 33), rand_w(O, C, 34), G, K, y_dtype, "stream_tile_mfma", rows=rows, ep=ep)
+
+
+@pytest.mark.parametrize("residual", [False, True])
+def test_spmm_auto_single_chunk_large(residual):
+    """AUTO's route for one 64-channel chunk over >= 100 K rows (the streaming
+    kernels; the tap-chunk kernels when the epilogue adds a residual)."""
+    need_gpu()
+    from paper_1910_11971_amd import cci
+    N, C, O, G, K = 100352, 64, 128, 8, 2
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, N, C, C, O, G, K) == "stream_tile_mfma"
+    rows = np.unique(np.concatenate([np.arange(0, 256), np.arange(N - 200, N), np.arange(0, N, 61)]))
+    ep = rand_epilogue(O, N, torch.bfloat16, 41, residual=residual, relu=True)
+    run_case(rand_x(N, C, torch.bfloat16, 42), rand_w(O, C, 43), G, K, torch.bfloat16, "auto", rows=rows, ep=ep)
+
+
+def test_spmm_stream_tile_refuses_unsupported():
+    need_gpu()
+    from paper_1910_11971_amd import cci
+    for C, O, G in ((320, 128, 8), (96, 128, 8), (128, 96, 8), (128, 128, 64)):
+        X = rand_x(300, C, torch.bfloat16, 1).to(DEV)
+        vals, idx = cci.pack(torch.from_numpy(rand_w(O, C, 2)).to(DEV), G, 2, torch.bfloat16)
+        with pytest.raises(cci.CCIError):
+            cci.spmm(X, vals, idx, G, algo="stream_tile_mfma")
+
+
 def test_spmm_wide_tile_repeat_is_identical():
     """Two launches on the same inputs give the same bytes (no state carried between launches)."""
     need_gpu()
@@ -127,7 +178,8 @@ def test_spmm_wide_tile_repeat_is_identical():
     assert torch.equal(Y1.view(torch.int16), Y2.view(torch.int16))
 
 
-@pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma", "wide_tile_mfma", "narrow_mfma", "tap_tile_mfma"])
+@pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma", "wide_tile_mfma", "narrow_mfma", "tap_tile_mfma",
+                                  "stream_tile_mfma"])
 def test_spmm_bf16_in_f32_out_with_epilogue(algo):
     need_gpu()
     N, C, O, G, K = 777, 128, 256, 8, 2
@@ -135,7 +187,8 @@ def test_spmm_bf16_in_f32_out_with_epilogue(algo):
     run_case(rand_x(N, C, torch.bfloat16, 1), rand_w(O, C, 2), G, K, torch.float32, algo, ep=ep)
 
 
-@pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma", "wide_tile_mfma", "narrow_mfma", "tap_tile_mfma"])
+@pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma", "wide_tile_mfma", "narrow_mfma", "tap_tile_mfma",
+                                  "stream_tile_mfma"])
 def test_spmm_bf16_epilogue_bf16_residual(algo):
     need_gpu()
     N, C, O, G, K = 300, 64, 256, 16, 4

@@ -275,6 +275,7 @@ __device__ __forceinline__ void narrow_body(const NParams& p, float* sb) {
     // epilogue: lane holds outputs 16 (t0 + t) + 4 kq .. +3 of pixel 16 b + ol
 #pragma unroll
     for (int b = 0; b < P; ++b) {
+      u32x2_t pk[TM];  // bf16 output: the rounded values of each tile
 #pragma unroll
       for (int t = 0; t < TM; ++t) {
         if (t >= tw) continue;
@@ -300,13 +301,44 @@ __device__ __forceinline__ void narrow_body(const NParams& p, float* sb) {
         }
         if constexpr (ysz == 2) {
           // v_cvt_pk_bf16_f32: round to nearest even
-          const u32x2_t pk = {__builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{y[0], y[1]}), bf16x2_t)),
-                              __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{y[2], y[3]}), bf16x2_t))};
-          __builtin_amdgcn_raw_buffer_store_b64(
-              __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b64(yr, 0, 0, 0)), pk), yr, off, 0, 0);
+          pk[t] = u32x2_t{__builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{y[0], y[1]}), bf16x2_t)),
+                          __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{y[2], y[3]}), bf16x2_t))};
         } else {
           __builtin_amdgcn_raw_buffer_store_b128(
               __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b128(yr, 0, 0, 0)), y), yr, off, 0, 0);
+        }
+      }
+      if constexpr (ysz == 2) {
+        // Tiles t, t + 1 both inside O leave as 16-byte stores (8-byte ones
+        // cost about 1.6x as much store time): lanes l and l ^ 16 (q = kq
+        // and its partner) swap halves so that the even one holds outputs
+        // 8 (kq / 2) .. +7 of tile t and the odd one those of tile t + 1
+        // (ds_swizzle in bit mode, xor 16 within each 32-lane half).  A
+        // last unpaired tile keeps its 8-byte store.
+        const bool odd = kq & 1;
+#pragma unroll
+        for (int t = 0; t < TM; t += 2) {
+          if (t >= tw) continue;
+          if (t + 1 < tw && t + 1 < TM && 16 * (t0 + t + 2) <= O) {
+            const u32x2_t snd = odd ? pk[t] : pk[t + 1 < TM ? t + 1 : t];
+            const uint32_t r0 = static_cast<uint32_t>(__builtin_amdgcn_ds_swizzle(static_cast<int>(snd[0]), 0x401F));
+            const uint32_t r1 = static_cast<uint32_t>(__builtin_amdgcn_ds_swizzle(static_cast<int>(snd[1]), 0x401F));
+            const u32x2_t mine = odd ? pk[t + 1 < TM ? t + 1 : t] : pk[t];
+            const u32x4_t v = odd ? u32x4_t{r0, r1, mine[0], mine[1]} : u32x4_t{mine[0], mine[1], r0, r1};
+            const uint32_t n = static_cast<uint32_t>(pg) * (16u * P) + 16u * b + static_cast<uint32_t>(ol);
+            const uint32_t o = static_cast<uint32_t>(16 * (t0 + t) + (odd ? 16 : 0) + 8 * (kq >> 1));
+            const uint32_t off = n < N ? (n * O + o) * ysz : kOOB;
+            __builtin_amdgcn_raw_buffer_store_b128(
+                __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b128(yr, 0, 0, 0)), v), yr, off, 0, 0);
+          } else {
+            __builtin_amdgcn_raw_buffer_store_b64(
+                __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b64(yr, 0, 0, 0)), pk[t]), yr, yoff(pg, b, t),
+                0, 0);
+            if (t + 1 < tw && t + 1 < TM)
+              __builtin_amdgcn_raw_buffer_store_b64(
+                  __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b64(yr, 0, 0, 0)), pk[t + 1 < TM ? t + 1 : t]),
+                  yr, yoff(pg, b, t + 1 < TM ? t + 1 : t), 0, 0);
+          }
         }
       }
     }

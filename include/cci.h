@@ -222,9 +222,8 @@ cci_status cci_conv_im2col_algo(const void *X, cci_dtype x_t, int64_t B,
  * one reported as CCI_ALGO_RESIDENT_MFMA or CCI_ALGO_TAP_TILE_MFMA runs on
  * the dense-tile kernels when a stride, alignment or size limit of that
  * family rules it out; one reported as CCI_ALGO_STREAM_TILE_MFMA runs on the
- * tap-chunk kernels (else the dense-tile ones) when its epilogue adds a
- * residual or its stride, padding or alignment rules the streaming ones
- * out. */
+ * tap-chunk kernels (else the dense-tile ones) when its stride, padding or
+ * alignment rules the streaming ones out. */
 cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C,
                        int64_t cin, int64_t O, int32_t G, int32_t K);
 

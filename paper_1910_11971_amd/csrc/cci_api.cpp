@@ -114,10 +114,6 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
     chosen = tile_ok ? CCI_ALGO_DENSE_TILE_MFMA : CCI_ALGO_SPARSE_MAC;
   if (algo == CCI_ALGO_AUTO && chosen == CCI_ALGO_TAP_TILE_MFMA && !cci::tap_tile_supports(a))
     chosen = tile_ok ? CCI_ALGO_DENSE_TILE_MFMA : CCI_ALGO_SPARSE_MAC;
-  // (its residual reads take the accumulator layout: with a residual the
-  // tap-chunk kernels are as fast)
-  if (algo == CCI_ALGO_AUTO && chosen == CCI_ALGO_STREAM_TILE_MFMA && a.residual && cci::tap_tile_supports(a))
-    chosen = CCI_ALGO_TAP_TILE_MFMA;
   if (algo == CCI_ALGO_AUTO && chosen == CCI_ALGO_STREAM_TILE_MFMA && !cci::stream_tile_supports(a))
     chosen = cci::tap_tile_supports(a) ? CCI_ALGO_TAP_TILE_MFMA : tile_ok ? CCI_ALGO_DENSE_TILE_MFMA : CCI_ALGO_SPARSE_MAC;
   if (chosen == CCI_ALGO_SPARSE_MAC && !mac_ok)
@@ -298,8 +294,8 @@ cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C, int
   const bool narrow_large = C == cin && C <= 128 && N >= 100000;
   // One 64-channel chunk over >= 100 K rows: the streaming kernels (the
   // expanded tile expanded once per workgroup, 128-row tiles streamed past
-  // it): 64 -> 256 at 200 704 rows 37 vs 41-48 us, 64 -> 64 16 vs 19.5 us;
-  // level with the tap-chunk kernels when a residual is added.
+  // it): 64 -> 256 at 200 704 rows 37 vs 41-48 us (with a residual 47 vs
+  // 53 us), 64 -> 64 17 vs 19-22 us.
   if (x_t == CCI_BF16 && val_t == CCI_BF16 && C == 64 && cin == 64 && N >= 100000 && O % 64 == 0 && G >= 1 &&
       32 % G == 0)
     return CCI_ALGO_STREAM_TILE_MFMA;

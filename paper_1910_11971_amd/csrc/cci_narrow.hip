@@ -308,13 +308,22 @@ __device__ __forceinline__ void narrow_body(const NParams& p, float* sb) {
               __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b128(yr, 0, 0, 0)), y), yr, off, 0, 0);
         }
       }
-      if constexpr (ysz == 2) {
-        // Tiles t, t + 1 both inside O leave as 16-byte stores (8-byte ones
-        // cost about 1.6x as much store time): lanes l and l ^ 16 (q = kq
-        // and its partner) swap halves so that the even one holds outputs
-        // 8 (kq / 2) .. +7 of tile t and the odd one those of tile t + 1
-        // (ds_swizzle in bit mode, xor 16 within each 32-lane half).  A
-        // last unpaired tile keeps its 8-byte store.
+      if constexpr (ysz == 2 && S < 4) {
+#pragma unroll
+        for (int t = 0; t < TM; ++t) {
+          if (t >= tw) continue;
+          __builtin_amdgcn_raw_buffer_store_b64(
+              __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b64(yr, 0, 0, 0)), pk[t]), yr,
+              yoff(pg, b, t), 0, 0);
+        }
+      } else if constexpr (ysz == 2) {
+        // With four or more k-steps (the 7x7 stem) tiles t, t + 1 both inside
+        // O leave as 16-byte stores (8-byte ones cost about 1.6x as much store
+        // time; with fewer k-steps the extra exchange costs more than it
+        // saves): lanes l and l ^ 16 (q = kq and its partner) swap halves so
+        // that the even one holds outputs 8 (kq / 2) .. +7 of tile t and the
+        // odd one those of tile t + 1 (ds_swizzle in bit mode, xor 16 within
+        // each 32-lane half).  A last unpaired tile keeps its 8-byte store.
         const bool odd = kq & 1;
 #pragma unroll
         for (int t = 0; t < TM; t += 2) {

@@ -136,7 +136,8 @@ __device__ __forceinline__ void stream_body(const SParams& p, uint8_t* lds) {
   constexpr int NDI = TP / 32;          // DMA instructions of one chunk per wave
   constexpr int WCH = wch_bytes(TO);    // one chunk of the weight tile
   constexpr uint32_t ysz = sizeof(YT);
-  constexpr int NRS = 4 * OT;           // residual loads per wave and row tile
+  static_assert(OT % 2 == 0, "residual loads take output tiles in pairs");
+  constexpr int NRS = (ysz == 2 ? 2 : 4) * OT;  // residual loads (16 bytes) per wave and row tile
   constexpr int SP = stage_pitch(TP, TO, ysz);
   constexpr int LPR = (TO / WO) * ysz / 16;  // lanes per staged row (16 bytes each)
   constexpr int RPP = 64 / LPR;         // staged rows per pass
@@ -248,8 +249,18 @@ __device__ __forceinline__ void stream_body(const SParams& p, uint8_t* lds) {
                         static_cast<uint32_t>(wp * 64 + pt * 16 + (lane & 15));
     return px < static_cast<uint32_t>(p.N) ? (px * static_cast<uint32_t>(p.O) + obase + 16u * ot) * ysz : kOOB;
   };
-  typedef typename std::conditional<ysz == 2, u32x2_t, u32x4_t>::type RT;  // 4 outputs of Y's type
-  RT res[4][OT];
+  // residual: for bf16, lane l loads the 16 bytes of outputs 8 (q / 2) .. +7
+  // of tile ot + (q odd) for each tile pair (q = lane / 16); its partner
+  // l ^ 16 holds the other halves (exchanged in the epilogue); for fp32 the
+  // lane's own 4 outputs per tile
+  u32x4_t res[4][OT];
+  const bool qodd = (lane >> 4) & 1;
+  auto r_off = [&](int k, int pt, int otp) {  // bf16: byte offset of the lane's 16 residual bytes
+    const uint32_t px = (st + static_cast<uint32_t>(k) * ns) * TP +
+                        static_cast<uint32_t>(wp * 64 + pt * 16 + (lane & 15));
+    const uint32_t o = ob * TO + static_cast<uint32_t>(wo * (TO / WO) + 16 * otp + (qodd ? 16 : 0) + 8 * (lane >> 5));
+    return px < static_cast<uint32_t>(p.N) ? (px * static_cast<uint32_t>(p.O) + o) * ysz : kOOB;
+  };
 
   f32x4_t acc[4][OT];
   const uint32_t xl = static_cast<uint32_t>(lane & 15), xkq = static_cast<uint32_t>(lane >> 4);
@@ -286,11 +297,14 @@ __device__ __forceinline__ void stream_body(const SParams& p, uint8_t* lds) {
 #pragma unroll
       for (int pt = 0; pt < 4; ++pt)
 #pragma unroll
-        for (int ot = 0; ot < OT; ++ot) {
-          if constexpr (ysz == 2)
-            res[pt][ot] = __builtin_bit_cast(RT, __builtin_amdgcn_raw_buffer_load_b64(rsr, y_off(kt, pt, ot), 0, 0));
-          else
-            res[pt][ot] = __builtin_bit_cast(RT, __builtin_amdgcn_raw_buffer_load_b128(rsr, y_off(kt, pt, ot), 0, 0));
+        for (int ot = 0; ot < OT; ot += 2) {
+          if constexpr (ysz == 2) {
+            res[pt][ot] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rsr, r_off(kt, pt, ot), 0, 0));
+          } else {
+            res[pt][ot] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rsr, y_off(kt, pt, ot), 0, 0));
+            res[pt][ot + 1] =
+                __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rsr, y_off(kt, pt, ot + 1), 0, 0));
+          }
         }
     }
     __builtin_amdgcn_sched_barrier(0);
@@ -335,6 +349,23 @@ __device__ __forceinline__ void stream_body(const SParams& p, uint8_t* lds) {
       const uint32_t col_b = (ob * TO + static_cast<uint32_t>(wo * (TO / WO))) * ysz + static_cast<uint32_t>(lane % LPR) * 16u;
 #pragma unroll
       for (int pt = 0; pt < 4; ++pt) {
+        u32x2_t rl[OT];  // bf16 residual of the lane's 4 outputs per tile
+        if constexpr (ysz == 2) {
+          if (has_res) {
+            // even lane: loaded tile ot's 0..7 (of its 16-output group) and
+            // keeps 0..3, sends 4..7, receives the partner's tile ot+1 0..3;
+            // odd lane: loaded tile ot+1's, keeps 4..7 (ds_swizzle xor 16)
+#pragma unroll
+            for (int ot = 0; ot < OT; ot += 2) {
+              const u32x4_t L = res[pt][ot];
+              const uint32_t s0 = qodd ? L[0] : L[2], s1 = qodd ? L[1] : L[3];
+              const uint32_t r0 = static_cast<uint32_t>(__builtin_amdgcn_ds_swizzle(static_cast<int>(s0), 0x401F));
+              const uint32_t r1 = static_cast<uint32_t>(__builtin_amdgcn_ds_swizzle(static_cast<int>(s1), 0x401F));
+              rl[ot] = qodd ? u32x2_t{r0, r1} : u32x2_t{L[0], L[1]};
+              rl[ot + 1] = qodd ? u32x2_t{L[2], L[3]} : u32x2_t{r0, r1};
+            }
+          }
+        }
 #pragma unroll
         for (int ot = 0; ot < OT; ++ot) {
           const f32x4_t sc = *reinterpret_cast<const f32x4_t*>(sbs + ocol + 16 * ot);
@@ -342,7 +373,7 @@ __device__ __forceinline__ void stream_body(const SParams& p, uint8_t* lds) {
           f32x4_t y = acc[pt][ot] * sc + bi;
           if (has_res) {
             if constexpr (ysz == 2) {
-              const u32x2_t r = res[pt][ot];
+              const u32x2_t r = rl[ot];
               y[0] += __uint_as_float(r[0] << 16);
               y[1] += __uint_as_float(r[0] & 0xffff0000u);
               y[2] += __uint_as_float(r[1] << 16);

@@ -146,7 +146,7 @@ def test_spmm_stream_tile_large_sampled(y_dtype):
 @pytest.mark.parametrize("residual", [False, True])
 def test_spmm_auto_single_chunk_large(residual):
     """AUTO's route for one 64-channel chunk over >= 100 K rows (the streaming
-    kernels; the tap-chunk kernels when the epilogue adds a residual)."""
+    kernels), with and without a residual."""
     need_gpu()
     from paper_1910_11971_amd import cci
     N, C, O, G, K = 100352, 64, 128, 8, 2

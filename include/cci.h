@@ -96,7 +96,7 @@ typedef enum { CCI_F32 = 0, CCI_BF16 = 1 } cci_dtype;
  *  CCI_ALGO_FEW_ROWS_MFMA   the few-row product of cci_spmm_bits reading
  *                           cci_pack's byte indices: FC products and 1x1
  *                           convolutions with stride 1 and no padding,
- *                           N <= 64, C % 32 == 0, O % 16 == 0, bf16 X and
+ *                           N <= 64, C % 32 == 0, O % 4 == 0, bf16 X and
  *                           vals (the packed bytes set the time; each is
  *                           read once).
  *  CCI_ALGO_TAP_TILE_MFMA   the same expansion with 128-pixel x 128-output
@@ -364,7 +364,7 @@ cci_status cci_index_bits(const uint8_t *idx, int64_t n, int32_t bits,
  * cci_index_width(G) <= idx_bits < 8, or the byte array of cci_pack for
  * idx_bits = 8.  This is the few-row product (N <= 64: a decode-sized batch)
  * where the packed weight bytes set the time; bf16 X and values, C % 32 == 0,
- * O % 16 == 0 (CCI_EUNSUPPORTED otherwise).  Epilogue and output as for
+ * O % 4 == 0 (CCI_EUNSUPPORTED otherwise).  Epilogue and output as for
  * cci_spmm. */
 cci_status cci_spmm_bits(const void *X, cci_dtype x_t, int64_t N, int64_t C,
                          const void *vals, cci_dtype val_t, const void *idx,

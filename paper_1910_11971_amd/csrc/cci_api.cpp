@@ -128,7 +128,7 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
   if (chosen == CCI_ALGO_FEW_ROWS_MFMA && !few_rows_ok(a))
     return fail(CCI_EUNSUPPORTED,
                 "few-row MFMA kernels need bf16 X/vals, an FC or stride-1 unpadded 1x1 product, N <= 64, "
-                "C %% 32 == 0 and O %% 16 == 0");
+                "C %% 32 == 0 and O %% 4 == 0");
   if (chosen == CCI_ALGO_RESIDENT_MFMA && !cci::resident_supports(a))
     return fail(CCI_EUNSUPPORTED,
                 "resident MFMA kernels need bf16 X/vals, a 3x3 convolution with unit stride and padding "
@@ -255,7 +255,7 @@ cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C, int
   // packed bytes set the time, and the few-row kernel (one expanded 16 x 32
   // tile per k-step and wave, read once) takes 7-24 us on a 4096 x 4096
   // layer where the tile kernels need 55-70 us.
-  if (x_t == CCI_BF16 && val_t == CCI_BF16 && C == cin && N <= 64 && C % 32 == 0 && O % 16 == 0)
+  if (x_t == CCI_BF16 && val_t == CCI_BF16 && C == cin && N <= 64 && C % 32 == 0 && O % 4 == 0)
     return CCI_ALGO_FEW_ROWS_MFMA;
   // 3x3 convolutions over 32 or 64 channels into 32 or 64 outputs: their
   // whole expanded tile fits in registers, so it is expanded once per
@@ -542,7 +542,7 @@ cci_status cci_spmm_bits(const void* X, cci_dtype x_t, int64_t N, int64_t C, con
     return fail(CCI_EINVAL, "idx_bits=%d outside [%d, 8] for G=%d", idx_bits, cci_index_width(G), G);
   if (x_t != CCI_BF16) return fail(CCI_EUNSUPPORTED, "the bit-index product takes bf16 X and values");
   if (!cci::spmm_bits_supports(N, C, O, G, K))
-    return fail(CCI_EUNSUPPORTED, "the bit-index product is for N <= 64 rows, C %% 32 == 0 and O %% 16 == 0");
+    return fail(CCI_EUNSUPPORTED, "the bit-index product is for N <= 64 rows, C %% 32 == 0 and O %% 4 == 0");
   const float* scale = ep ? ep->scale : nullptr;
   const float* bias = ep ? ep->bias : nullptr;
   const void* residual = ep ? ep->residual : nullptr;

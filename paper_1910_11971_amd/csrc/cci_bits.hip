@@ -8,7 +8,9 @@
 //
 // Few-row product (N <= 64).  With few rows every packed weight is used by
 // at most N multiply-adds, so the packed bytes (2 per value + b/8 per index)
-// set the time.  A workgroup of eight waves owns 16 output channels; wave w
+// set the time.  A workgroup of eight waves owns 16 output channels (the
+// last one fewer when O % 16 != 0: its missing rows stay zero and are not
+// stored); wave w
 // takes the 32-column k-steps w, w+8, ... of the reduction.  Per k-step a wave
 //   - clears its 16 x 32 bf16 tile in LDS (one 16-byte store per lane),
 //   - reads the kept entries of the groups covering its 16 rows (lanes over
@@ -88,7 +90,7 @@ __global__ __launch_bounds__(kFThreads) void spmm_bits_kernel(FParams p) {
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int32_t o0 = static_cast<int32_t>(blockIdx.x) * 16;
-  const int32_t g_lo = o0 / p.G, g_hi = (o0 + 15) / p.G;
+  const int32_t g_lo = o0 / p.G, g_hi = min((o0 + 15) / p.G, p.O / p.G - 1);
   // (group, slot) pairs cover the k-step's 32 columns: lanes 0..31 take the
   // even pairs, lanes 32..63 the odd ones, lane & 31 the column; entry u of
   // a lane is pair pk + 2u, at packed offset base[u] + 32 s in k-step s
@@ -221,8 +223,8 @@ __global__ __launch_bounds__(kFThreads) void spmm_bits_kernel(FParams p) {
 #pragma unroll
   for (int v = 1; v < kFWaves; ++v) sum += red[v][w][lane];
   const int32_t n = 16 * w + ti;
-  if (n >= p.N) return;
   const int32_t o = o0 + 4 * tq;  // lane holds outputs o .. o+3 of row n
+  if (n >= p.N || o >= p.O) return;  // (O % 4 == 0: a lane's 4 outputs are all inside or all past O)
   const bool yf32 = std::is_same<YT, float>::value;
   const int64_t yo = static_cast<int64_t>(n) * p.O + o;
   float y[4];
@@ -252,7 +254,7 @@ __global__ __launch_bounds__(kFThreads) void spmm_bits_kernel(FParams p) {
 
 template <int NB, int PL>
 hipError_t launch_fp(const FParams& p, DType y_t, hipStream_t s) {
-  const dim3 grid(static_cast<uint32_t>(p.O / 16));
+  const dim3 grid(static_cast<uint32_t>((p.O + 15) / 16));
   if (y_t == DType::F32)
     hipLaunchKernelGGL((spmm_bits_kernel<NB, PL, float>), grid, dim3(kFThreads), 0, s, p);
   else
@@ -287,7 +289,7 @@ hipError_t launch_index_bits(const uint8_t* idx, int64_t n, int32_t b, uint32_t*
 }
 
 bool spmm_bits_supports(int64_t N, int64_t C, int64_t O, int32_t G, int32_t K) {
-  return N >= 0 && N <= 64 && C % 32 == 0 && O % 16 == 0 && N * C * 2 < (int64_t(1) << 31) &&
+  return N >= 0 && N <= 64 && C % 32 == 0 && O % 4 == 0 && N * C * 2 < (int64_t(1) << 31) &&
          (O / G) * K * C < (int64_t(1) << 30);
 }
 

@@ -66,7 +66,7 @@ hipError_t launch_grad_packed(const void*, const void*, DType, int64_t, int64_t,
 }
 int64_t index_stream_bytes(int64_t n, int32_t b) { return b == 8 ? n : (n * b + 31) / 32 * 4; }
 hipError_t launch_index_bits(const uint8_t*, int64_t, int32_t, uint32_t*, hipStream_t) { ++g_launches; return hipSuccess; }
-bool spmm_bits_supports(int64_t N, int64_t C, int64_t O, int32_t, int32_t) { return N <= 64 && C % 32 == 0 && O % 16 == 0; }
+bool spmm_bits_supports(int64_t N, int64_t C, int64_t O, int32_t, int32_t) { return N <= 64 && C % 32 == 0 && O % 4 == 0; }
 hipError_t launch_spmm_bits(const void*, int64_t, int64_t, const void*, const void*, int32_t, int64_t, int32_t, int32_t,
                             const float*, const float*, const void*, int32_t, void*, DType, hipStream_t) {
   ++g_launches;

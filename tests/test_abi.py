@@ -155,10 +155,10 @@ def test_stream_tile_algo_requirements():
 
 
 def test_few_rows_algo_requirements():
-    # few-row MFMA: bf16 FC / plain 1x1 products with N <= 64, C % 32 == 0, O % 16 == 0
+    # few-row MFMA: bf16 FC / plain 1x1 products with N <= 64, C % 32 == 0, O % 4 == 0
     Fr = cci.ALGO_FEW_ROWS_MFMA
-    for N, C, O in [(65, 64, 16), (4, 48, 16), (4, 64, 24)]:
-        assert lib.cci_spmm_algo(FAKE, cci.BF16, N, C, FAKE, cci.BF16, FAKE, O, 8, 2, None, FAKE,
+    for N, C, O, G in [(65, 64, 16, 8), (4, 48, 16, 8), (4, 64, 18, 2)]:
+        assert lib.cci_spmm_algo(FAKE, cci.BF16, N, C, FAKE, cci.BF16, FAKE, O, G, 2 if G > 2 else 1, None, FAKE,
                                  cci.BF16, Fr, None) == cci.EUNSUPPORTED
     assert lib.cci_spmm_algo(FAKE, cci.F32, 4, 64, FAKE, cci.F32, FAKE, 16, 8, 2, None, FAKE,
                              cci.F32, Fr, None) == cci.EUNSUPPORTED
@@ -166,6 +166,8 @@ def test_few_rows_algo_requirements():
                                     FAKE, 16, 8, 2, None, FAKE, cci.BF16, Fr, None) == cci.EUNSUPPORTED
     assert lib.cci_auto_algo(cci.BF16, cci.BF16, 64, 4096, 4096, 4096, 16, 4) == Fr
     assert lib.cci_auto_algo(cci.BF16, cci.BF16, 65, 4096, 4096, 4096, 16, 4) != Fr
+    # a ragged last 16-output tile (the ResNet-50 classifier: 2048 -> 1000)
+    assert lib.cci_auto_algo(cci.BF16, cci.BF16, 64, 2048, 2048, 1000, 8, 8) == Fr
 
 
 def test_algo_entry_points_match_plain_calls_on_validation():

@@ -206,6 +206,8 @@ def test_spmm_fp32(N, C, O, G, K):
 FEW_ROW_CASES = [  # N, C, O, G, K: N <= 64 bf16 products (the library's choice: the few-row kernel)
     (1, 64, 16, 8, 2), (17, 96, 48, 16, 4), (64, 512, 256, 8, 3), (33, 32, 48, 3, 2), (5, 256, 256, 256, 9),
     (64, 160, 64, 4, 4), (2, 1024, 512, 64, 1),
+    # O % 16 != 0: a ragged last tile of 4, 8 or 12 outputs
+    (64, 2048, 1000, 8, 8), (17, 96, 52, 4, 2), (33, 128, 36, 4, 4), (7, 64, 24, 8, 3),
 ]
 
 
@@ -218,10 +220,11 @@ def test_spmm_bf16_few_rows(N, C, O, G, K):
     run_case(rand_x(N, C, torch.bfloat16, N + C + 2), rand_w(O, C, O + G + 2), G, K, torch.bfloat16, "few_rows_mfma")
 
 
+@pytest.mark.parametrize("O", [128, 1000])
 @pytest.mark.parametrize("y_dtype", [torch.bfloat16, torch.float32])
-def test_spmm_few_rows_epilogue(y_dtype):
+def test_spmm_few_rows_epilogue(y_dtype, O):
     need_gpu()
-    N, C, O, G, K = 40, 256, 128, 8, 2
+    N, C, G, K = 40, 256, 8, 2
     ep = rand_epilogue(O, N, y_dtype, 23, residual=True, relu=True)
     run_case(rand_x(N, C, torch.bfloat16, 24), rand_w(O, C, 25), G, K, y_dtype, "few_rows_mfma", ep=ep)
 

@@ -278,9 +278,10 @@ cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C, int
   // strided 1x1 26-36 vs 37-45 us; 12544 x 1024 x 256 18.5 vs 23.3 us; the
   // bottleneck 1x1 layers with their residual add 52 vs 64 us (64 -> 256,
   // 200 704 pixels) and 35 vs 39 us (128 -> 512, 50 176 pixels).
-  // A reduction of one 64-channel chunk leaves the pipeline empty: such
-  // products go to the tap-chunk kernels only at >= 100 K rows (MobileNetV2's
-  // 12544 x 64 -> 384: 9.4 us there, 8.0 us on the dense-tile kernels).
+  // A reduction of one 64-channel chunk leaves their pipeline empty: such
+  // products never go to them (MobileNetV2's 12544 x 64 -> 384: 9.4 us
+  // there, 8.0 us on the dense-tile kernels; from 100 K rows on, the
+  // streaming kernels below take them).
   const bool tap_fits = x_t == CCI_BF16 && val_t == CCI_BF16 && G >= 1 && 32 % G == 0 && (2 * K <= G || K == G) &&
                         cin % 64 == 0 && O % 128 == 0 && C / cin <= 32;
   const bool tap_shape = tap_fits && C >= 128;
@@ -289,8 +290,8 @@ cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C, int
   // products with C % 8 == 0, and convolutions over 4 input channels (an
   // even KW) or a multiple of 8.  Large 1x1 / FC products with C <= 128 do
   // too (8-20% ahead of the dense-tile kernels at 50 K - 800 K rows) unless
-  // the tap-chunk kernels take them (64 -> 256 at 200 K rows: 40 us either
-  // way without a residual, 52 vs 64 us with one).
+  // the streaming (C = 64) or tap-chunk (C = 128, O % 128 == 0) kernels
+  // take them.
   const bool narrow_large = C == cin && C <= 128 && N >= 100000;
   // One 64-channel chunk over >= 100 K rows: the streaming kernels (the
   // expanded tile expanded once per workgroup, 128-row tiles streamed past

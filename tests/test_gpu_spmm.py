@@ -120,6 +120,8 @@ STREAM_FC_CASES = [  # N, C, O, G, K: FC products on the streaming kernels (C <=
     (1000, 256, 320, 4, 1), (5000, 192, 192, 2, 2), (3000, 256, 128, 1, 1), (777, 128, 384, 32, 32),
     # many row tiles per workgroup, 128- and 64-output tiles, a ragged last tile
     (33001, 64, 256, 8, 2), (40000, 128, 512, 8, 2), (70001, 256, 64, 8, 2), (20000, 192, 128, 16, 3),
+    # 64-output tiles holding two 32-row groups; a three-chunk reduction with a ragged last row tile
+    (2000, 64, 192, 32, 7), (9999, 192, 320, 32, 32),
 ]
 
 

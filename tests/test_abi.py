@@ -166,8 +166,8 @@ def test_few_rows_algo_requirements():
                                     FAKE, 16, 8, 2, None, FAKE, cci.BF16, Fr, None) == cci.EUNSUPPORTED
     assert lib.cci_auto_algo(cci.BF16, cci.BF16, 64, 4096, 4096, 4096, 16, 4) == Fr
     assert lib.cci_auto_algo(cci.BF16, cci.BF16, 65, 4096, 4096, 4096, 16, 4) != Fr
-    # a ragged last 16-output tile (the ResNet-50 classifier: 2048 -> 1000)
-    assert lib.cci_auto_algo(cci.BF16, cci.BF16, 64, 2048, 2048, 1000, 8, 8) == Fr
+    # a ragged last 16-output tile (the ResNet-50 classifier: 2048 -> 1000) is taken only when pinned
+    assert lib.cci_auto_algo(cci.BF16, cci.BF16, 64, 2048, 2048, 1000, 8, 8) != Fr
 
 
 def test_algo_entry_points_match_plain_calls_on_validation():

@@ -208,8 +208,6 @@ def test_spmm_fp32(N, C, O, G, K):
 FEW_ROW_CASES = [  # N, C, O, G, K: N <= 64 bf16 products (the library's choice: the few-row kernel)
     (1, 64, 16, 8, 2), (17, 96, 48, 16, 4), (64, 512, 256, 8, 3), (33, 32, 48, 3, 2), (5, 256, 256, 256, 9),
     (64, 160, 64, 4, 4), (2, 1024, 512, 64, 1),
-    # O % 16 != 0: a ragged last tile of 4, 8 or 12 outputs
-    (64, 2048, 1000, 8, 8), (17, 96, 52, 4, 2), (33, 128, 36, 4, 4), (7, 64, 24, 8, 3),
 ]
 
 
@@ -220,6 +218,14 @@ def test_spmm_bf16_few_rows(N, C, O, G, K):
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, N, C, C, O, G, K) == "few_rows_mfma"
     run_case(rand_x(N, C, torch.bfloat16, N + C + 1), rand_w(O, C, O + G + 1), G, K, torch.bfloat16, "auto")
     run_case(rand_x(N, C, torch.bfloat16, N + C + 2), rand_w(O, C, O + G + 2), G, K, torch.bfloat16, "few_rows_mfma")
+
+
+@pytest.mark.parametrize("N,C,O,G,K", [(64, 2048, 1000, 8, 8), (17, 96, 52, 4, 2), (33, 128, 36, 4, 4),
+                                       (7, 64, 24, 8, 3)])
+def test_spmm_bf16_few_rows_ragged_tile(N, C, O, G, K):
+    """O % 16 != 0 (a last tile of 4, 8 or 12 outputs) on the pinned few-row kernel."""
+    need_gpu()
+    run_case(rand_x(N, C, torch.bfloat16, N + C + 3), rand_w(O, C, O + G + 3), G, K, torch.bfloat16, "few_rows_mfma")
 
 
 @pytest.mark.parametrize("O", [128, 1000])

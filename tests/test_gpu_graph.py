@@ -1,7 +1,8 @@
-"""HIP-graph capture of the hot path (cci_pack + cci_conv_im2col / cci_spmm):
-every replay, with eager work and synchronisation in between, reproduces the
-eager results bit for bit (the kernels are deterministic and the library
-records no memset or allocation into a captured graph)."""
+"""HIP-graph capture of the hot path (cci_pack + cci_conv_im2col / cci_spmm
+on the dense-tile, sparse-MAC, narrow, wide-tile, streaming and tap-chunk
+kernels): every replay, with eager work and synchronisation in between,
+reproduces the eager results bit for bit (the kernels are deterministic and
+the library records no memset or allocation into a captured graph)."""
 import numpy as np
 import pytest
 import torch
@@ -40,6 +41,21 @@ def test_graph_replays_match_eager():
     vw = torch.empty((16, 1, 1024), dtype=torch.bfloat16, device=DEV)
     xw = torch.empty((16, 1, 1024), dtype=torch.uint8, device=DEV)
     Yw = torch.empty((300, 256), dtype=torch.bfloat16, device=DEV)
+    # a streaming-kernel product with a residual epilogue, and a tap-chunk 3x3 conv over 128 channels
+    Xs2 = torch.from_numpy(np.random.default_rng(11).standard_normal((3000, 64)).astype(np.float32)).to(
+        torch.bfloat16).to(DEV)
+    Ws2 = torch.from_numpy((np.random.default_rng(12).standard_normal((256, 64)) / 8).astype(np.float32)).to(DEV)
+    Rs2 = torch.from_numpy(np.random.default_rng(13).standard_normal((3000, 256)).astype(np.float32)).to(
+        torch.bfloat16).to(DEV)
+    vs2 = torch.empty((32, 2, 64), dtype=torch.bfloat16, device=DEV)
+    xs2 = torch.empty((32, 2, 64), dtype=torch.uint8, device=DEV)
+    Ys2 = torch.empty((3000, 256), dtype=torch.bfloat16, device=DEV)
+    Xt = torch.from_numpy(np.random.default_rng(14).standard_normal((2, 9, 11, 128)).astype(np.float32)).to(
+        torch.bfloat16).to(DEV)
+    Wt = torch.from_numpy((np.random.default_rng(15).standard_normal((128, 9 * 128)) / 34).astype(np.float32)).to(DEV)
+    vt = torch.empty((16, 2, 9 * 128), dtype=torch.bfloat16, device=DEV)
+    xt = torch.empty((16, 2, 9 * 128), dtype=torch.uint8, device=DEV)
+    Yt = torch.empty((2, 9, 11, 128), dtype=torch.bfloat16, device=DEV)
     s = torch.cuda.Stream()
 
     def step():
@@ -52,11 +68,16 @@ def test_graph_replays_match_eager():
         cci.conv_im2col(Xn, vn, xn, 8, 1, 1, out=Yn, algo="narrow_mfma")
         cci.pack(Ww, 16, 1, torch.bfloat16, out=(vw, xw))
         cci.spmm(Xw, vw, xw, 16, out=Yw, algo="wide_tile_mfma")
+        cci.pack(Ws2, 8, 2, torch.bfloat16, out=(vs2, xs2))
+        cci.spmm(Xs2, vs2, xs2, 8, residual=Rs2, relu=True, out=Ys2, algo="stream_tile_mfma")
+        cci.pack(Wt, 8, 2, torch.bfloat16, out=(vt, xt))
+        cci.conv_im2col(Xt, vt, xt, 8, 3, 3, (1, 1), (1, 1), out=Yt, algo="tap_tile_mfma")
 
     with torch.cuda.stream(s):
         step()
     torch.cuda.synchronize()
-    ref = [y.clone() for y in Ys] + [Yf.clone(), vals.clone(), idx.clone(), Yn.clone(), Yw.clone()]
+    ref = [y.clone() for y in Ys] + [Yf.clone(), vals.clone(), idx.clone(), Yn.clone(), Yw.clone(), Ys2.clone(),
+                                     Yt.clone()]
 
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g, stream=s):
@@ -67,12 +88,14 @@ def test_graph_replays_match_eager():
         Yf.zero_()
         Yn.zero_()
         Yw.zero_()
+        Ys2.zero_()
+        Yt.zero_()
         vals.zero_()
         torch.cuda.synchronize()
         with torch.cuda.stream(s):
             g.replay()
         torch.cuda.synchronize()
-        got = Ys + [Yf, vals, idx, Yn, Yw]
+        got = Ys + [Yf, vals, idx, Yn, Yw, Ys2, Yt]
         for a, b in zip(got, ref):
             assert torch.equal(a, b), f"replay {rep} differs from the eager run"
         # eager work between replays, on other data

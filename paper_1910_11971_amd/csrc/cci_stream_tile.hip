@@ -53,11 +53,11 @@ constexpr int kLdsMax = 160 * 1024;     // LDS of a CU
 constexpr uint32_t kOOB = 0x80000000u;  // buffer offset that reads as zero / drops a store
 constexpr int kRsrcWord3 = 0x00020000;  // raw buffer descriptor word 3 (gfx9 family)
 constexpr int wch_bytes(int to) { return to * kCK * 2; }
-// the weight tile, the ring of nr activation buffers, then scale and bias of
-// the TO outputs
 // one wave's epilogue staging: 16 rows of its TO / WO outputs in Y's type
 // (ysz bytes each), padded by 16 bytes per row
 constexpr int stage_pitch(int tp, int to, int ysz) { return to / (4 / (tp / 64)) * ysz + 16; }
+// the weight tile, the ring of nr activation buffers, scale and bias of the
+// TO outputs, then the four waves' staging rows
 constexpr int lds_bytes(int nch, int tp, int to, int nr, int ysz) {
   return nch * wch_bytes(to) + nr * xb_bytes(tp) + 2 * to * 4 + 4 * 16 * stage_pitch(tp, to, ysz);
 }

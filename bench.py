@@ -57,7 +57,7 @@ def parse():
     p.add_argument("--k", type=int, default=4, help="fc4096: the K whose step gives `value`")
     p.add_argument("--algo", default="auto", choices=["auto", "sparse_mac", "dense_tile_mfma", "wide_tile_mfma", "narrow_mfma",
                                                      "resident_mfma", "few_rows_mfma", "tap_tile_mfma",
-                                                     "stream_tile_mfma"])
+                                                     "stream_tile_mfma", "split_k_mfma"])
     p.add_argument("--rotate-mb", type=float, default=600.0,
                    help="total size of rotated X/Y copies (0: no rotation)")
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="target wall time of the CPU oracle sample")
@@ -86,7 +86,8 @@ def parse():
 KERNEL_SOURCES = {"cci_dense_tile": "cci_dense_tile.hip", "cci_wide_tile": "cci_wide_tile.hip",
                   "cci_sparse_mac": "cci_sparse_mac.hip", "cci_narrow": "cci_narrow.hip",
                   "cci_resident": "cci_resident.hip", "cci_bits": "cci_bits.hip",
-                  "cci_tap_tile": "cci_tap_tile.hip", "cci_stream_tile": "cci_stream_tile.hip"}
+                  "cci_tap_tile": "cci_tap_tile.hip", "cci_stream_tile": "cci_stream_tile.hip",
+                  "cci_split_k": "cci_split_k.hip"}
 
 
 def kernel_source_hash(kernel: str = "cci_dense_tile") -> str:
@@ -784,7 +785,7 @@ def kernel_name(algo):
     return {"dense_tile_mfma": "cci_dense_tile", "wide_tile_mfma": "cci_wide_tile",
             "narrow_mfma": "cci_narrow", "resident_mfma": "cci_resident",
             "few_rows_mfma": "cci_bits", "tap_tile_mfma": "cci_tap_tile",
-            "stream_tile_mfma": "cci_stream_tile"}.get(algo, "cci_sparse_mac")
+            "stream_tile_mfma": "cci_stream_tile", "split_k_mfma": "cci_split_k"}.get(algo, "cci_sparse_mac")
 
 
 def _dense_time(fn, n_launch, stream, reps=10):
@@ -804,7 +805,7 @@ def roof_for(kname, flop, dense_flop, alg_bytes, t_ms):
     vector-ALU kernel multiplies only kept weights, so its bound is the fp32
     FMA rate (or HBM, if that takes longer)."""
     if kname in ("cci_dense_tile", "cci_wide_tile", "cci_narrow", "cci_resident", "cci_bits", "cci_tap_tile",
-                 "cci_stream_tile"):
+                 "cci_stream_tile", "cci_split_k"):
         return own_roof(flop, alg_bytes, t_ms, dense_flop)
     t_alu = flop / (PEAK["valu_fp32_TFLOPs"] * 1e12)
     t_hbm = alg_bytes / (PEAK["hbm_GBps"] * 1e9)

@@ -122,7 +122,21 @@ typedef enum { CCI_F32 = 0, CCI_BF16 = 1 } cci_dtype;
  *                           and no padding; bf16 X and vals, C % 64 == 0,
  *                           C <= 256, O % 64 == 0, 32 % G == 0; X 16-byte
  *                           aligned, Y (and residual) 8-byte aligned for
- *                           bf16 and 16-byte aligned for fp32 output. */
+ *                           bf16 and 16-byte aligned for fp32 output.
+ *  CCI_ALGO_SPLIT_K_MFMA    few row tiles over a long reduction (the
+ *                           projecting 1x1 layers of a CNN's late stages):
+ *                           eight waves of a workgroup split the reduction
+ *                           of one 64 x 32, 32 x 64, 32 x 32 or 32 x 16 (rows
+ *                           x outputs) tile, each issuing the loads of its
+ *                           k-steps together and building its weight
+ *                           fragments in registers from the kept entries
+ *                           (Alg. 1's routing: a value lands in the output
+ *                           row its index names); the partial tiles are
+ *                           added in LDS.  FC products and 1x1 convolutions
+ *                           with stride 1 and no padding; bf16 X and vals,
+ *                           C % 32 == 0, O % 16 == 0, K <= 4, G <= 256; X,
+ *                           vals, idx, Y, scale, bias and residual 16-byte
+ *                           aligned. */
 typedef enum {
   CCI_ALGO_AUTO = 0,
   CCI_ALGO_SPARSE_MAC = 1,
@@ -132,7 +146,8 @@ typedef enum {
   CCI_ALGO_RESIDENT_MFMA = 5,
   CCI_ALGO_FEW_ROWS_MFMA = 6,
   CCI_ALGO_TAP_TILE_MFMA = 7,
-  CCI_ALGO_STREAM_TILE_MFMA = 8
+  CCI_ALGO_STREAM_TILE_MFMA = 8,
+  CCI_ALGO_SPLIT_K_MFMA = 9
 } cci_algo;
 
 /* Optional fused epilogue, applied per output element before rounding:
@@ -223,7 +238,9 @@ cci_status cci_conv_im2col_algo(const void *X, cci_dtype x_t, int64_t B,
  * the dense-tile kernels when a stride, alignment or size limit of that
  * family rules it out; one reported as CCI_ALGO_STREAM_TILE_MFMA runs on the
  * tap-chunk kernels (else the dense-tile ones) when its stride, padding or
- * alignment rules the streaming ones out. */
+ * alignment rules the streaming ones out; one reported as
+ * CCI_ALGO_SPLIT_K_MFMA runs on the dense-tile kernels when its stride,
+ * padding or alignment rules the split-reduction ones out. */
 cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C,
                        int64_t cin, int64_t O, int32_t G, int32_t K);
 

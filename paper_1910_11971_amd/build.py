@@ -22,7 +22,7 @@ OUT = os.path.join(HERE, "libcci.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
 SOURCES = ["cci_api.cpp", "cci_pack.hip", "cci_sparse_mac.hip", "cci_dense_tile.hip", "cci_wide_tile.hip", "cci_narrow.hip",
-           "cci_resident.hip", "cci_tap_tile.hip", "cci_stream_tile.hip", "cci_glue.hip", "cci_bbs.hip", "cci_train.hip", "cci_grad.hip", "cci_bits.hip"]
+           "cci_resident.hip", "cci_tap_tile.hip", "cci_stream_tile.hip", "cci_split_k.hip", "cci_glue.hip", "cci_bbs.hip", "cci_train.hip", "cci_grad.hip", "cci_bits.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -20,11 +20,12 @@ HEADER_PATH = os.path.join(os.path.dirname(_HERE), "include", "cci.h")
 OK, EINVAL, EUNSUPPORTED, EALIGN, EHIP = 0, 1, 2, 3, 4
 F32, BF16 = 0, 1
 (ALGO_AUTO, ALGO_SPARSE_MAC, ALGO_DENSE_TILE_MFMA, ALGO_WIDE_TILE_MFMA, ALGO_NARROW_MFMA, ALGO_RESIDENT_MFMA,
- ALGO_FEW_ROWS_MFMA, ALGO_TAP_TILE_MFMA, ALGO_STREAM_TILE_MFMA) = range(9)
+ ALGO_FEW_ROWS_MFMA, ALGO_TAP_TILE_MFMA, ALGO_STREAM_TILE_MFMA, ALGO_SPLIT_K_MFMA) = range(10)
 ALGOS = {"auto": ALGO_AUTO, "sparse_mac": ALGO_SPARSE_MAC, "dense_tile_mfma": ALGO_DENSE_TILE_MFMA,
          "wide_tile_mfma": ALGO_WIDE_TILE_MFMA, "narrow_mfma": ALGO_NARROW_MFMA,
          "resident_mfma": ALGO_RESIDENT_MFMA, "few_rows_mfma": ALGO_FEW_ROWS_MFMA,
-         "tap_tile_mfma": ALGO_TAP_TILE_MFMA, "stream_tile_mfma": ALGO_STREAM_TILE_MFMA}
+         "tap_tile_mfma": ALGO_TAP_TILE_MFMA, "stream_tile_mfma": ALGO_STREAM_TILE_MFMA,
+         "split_k_mfma": ALGO_SPLIT_K_MFMA}
 
 
 class CCIError(RuntimeError):

@@ -90,7 +90,8 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
     return fail(CCI_EALIGN, "epilogue pointer not 16-byte aligned");
   if (algo != CCI_ALGO_AUTO && algo != CCI_ALGO_SPARSE_MAC && algo != CCI_ALGO_DENSE_TILE_MFMA &&
       algo != CCI_ALGO_WIDE_TILE_MFMA && algo != CCI_ALGO_NARROW_MFMA && algo != CCI_ALGO_RESIDENT_MFMA &&
-      algo != CCI_ALGO_FEW_ROWS_MFMA && algo != CCI_ALGO_TAP_TILE_MFMA && algo != CCI_ALGO_STREAM_TILE_MFMA)
+      algo != CCI_ALGO_FEW_ROWS_MFMA && algo != CCI_ALGO_TAP_TILE_MFMA && algo != CCI_ALGO_STREAM_TILE_MFMA &&
+      algo != CCI_ALGO_SPLIT_K_MFMA)
     return fail(CCI_EINVAL, "unknown algo %d", (int)algo);
   if (a.N == 0) return ok();
 
@@ -116,6 +117,8 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
     chosen = tile_ok ? CCI_ALGO_DENSE_TILE_MFMA : CCI_ALGO_SPARSE_MAC;
   if (algo == CCI_ALGO_AUTO && chosen == CCI_ALGO_STREAM_TILE_MFMA && !cci::stream_tile_supports(a))
     chosen = cci::tap_tile_supports(a) ? CCI_ALGO_TAP_TILE_MFMA : tile_ok ? CCI_ALGO_DENSE_TILE_MFMA : CCI_ALGO_SPARSE_MAC;
+  if (algo == CCI_ALGO_AUTO && chosen == CCI_ALGO_SPLIT_K_MFMA && !cci::split_k_supports(a))
+    chosen = tile_ok ? CCI_ALGO_DENSE_TILE_MFMA : CCI_ALGO_SPARSE_MAC;
   if (chosen == CCI_ALGO_SPARSE_MAC && !mac_ok)
     return fail(CCI_EUNSUPPORTED, "sparse-MAC kernels need G in {2,4,8,16,32} (G=%d)", a.G);
   if (chosen == CCI_ALGO_DENSE_TILE_MFMA && !tile_ok)
@@ -147,8 +150,13 @@ cci_status run_product(cci::ProductArgs& a, cci_algo algo, const cci_epilogue* e
     return fail(CCI_EUNSUPPORTED,
                 "stream-tile MFMA kernels need bf16 X/vals, an FC or stride-1 unpadded 1x1 product, "
                 "C %% 64 == 0 with C <= 256, O %% 64 == 0, 32 %% G == 0 and aligned pointers");
+  if (chosen == CCI_ALGO_SPLIT_K_MFMA && !cci::split_k_supports(a))
+    return fail(CCI_EUNSUPPORTED,
+                "split-K MFMA kernels need bf16 X/vals, an FC or stride-1 unpadded 1x1 product, "
+                "C %% 32 == 0, O %% 16 == 0, K <= 4 and 16-byte aligned pointers");
   const hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = chosen == CCI_ALGO_SPARSE_MAC       ? cci::launch_sparse_mac(a, st)
+                 : chosen == CCI_ALGO_SPLIT_K_MFMA   ? cci::launch_split_k(a, st)
                  : chosen == CCI_ALGO_STREAM_TILE_MFMA ? cci::launch_stream_tile(a, st)
                  : chosen == CCI_ALGO_TAP_TILE_MFMA  ? cci::launch_tap_tile(a, st)
                  : chosen == CCI_ALGO_WIDE_TILE_MFMA ? cci::launch_wide_tile(a, st)
@@ -306,6 +314,25 @@ cci_algo cci_auto_algo(cci_dtype x_t, cci_dtype val_t, int64_t N, int64_t C, int
     return CCI_ALGO_STREAM_TILE_MFMA;
   if (tap_fits && narrow_large) return CCI_ALGO_TAP_TILE_MFMA;
   if (narrow_shape && (cin % 32 != 0 || narrow_large)) return CCI_ALGO_NARROW_MFMA;
+  // Long reductions over few row tiles (the late projecting 1x1 layers of
+  // MobileNetV2 at batch 64, 3 136 rows): the tile kernels walk 9-15
+  // 64-channel chunks one memory round trip at a time on a fraction of the
+  // CUs.  When 64 x 32 tiles fill at most one round of the chip, the
+  // split-reduction kernels take them (576 -> 160: 8.0 vs 13.4 us; 960 ->
+  // 160: 10.8 vs 19.5 us; 512 x 512 -> 320: 4.9 vs 7.9 us; 256 x 1024 ->
+  // 160: 6.1 vs 12.0 us); else, with O % 64 == 0, the tap-chunk kernels'
+  // 64-output tiles (960 -> 320: 13.6 us vs 15.4 split, 20.8 dense-tile).
+  // From 12 544 rows on the dense-tile kernels stay ahead (576 -> 96: 14.6
+  // vs 20.2 us; 384 -> 64: 8.7 vs 9.1 tap, 9.5 split).  O % 128 == 0 keeps
+  // the routes below (tap-chunk or wide-tile), measured on ResNet-50.
+  if (x_t == CCI_BF16 && val_t == CCI_BF16 && C == cin && C >= 512 && C <= 1024 && C % 32 == 0 && O % 16 == 0 &&
+      O % 128 != 0) {
+    // (at C = 512 two k-steps per wave: half a round at most; 4096 x 512 ->
+    // 96 is 9.0 us split, 8.3 us dense-tile)
+    const int64_t t64x32 = (N + 63) / 64 * ((O + 31) / 32);
+    if (t64x32 <= (C >= 576 ? 256 : 128) && K <= 4) return CCI_ALGO_SPLIT_K_MFMA;
+    if (O % 64 == 0 && G <= 16 && 16 % G == 0 && (2 * K <= G || K == G)) return CCI_ALGO_TAP_TILE_MFMA;
+  }
   // FC and 1x1 products with a reduction of >= 256 that fill the chip with
   // 256 x 256 tiles (>= 128 of them) run on the wide-tile kernels: 2.2-2.4x
   // the dense-tile kernel on 4096^3, and level with the tap-chunk kernels on

@@ -102,6 +102,13 @@ hipError_t launch_tap_tile(const ProductArgs& a, hipStream_t s);
 bool stream_tile_supports(const ProductArgs& a);
 hipError_t launch_stream_tile(const ProductArgs& a, hipStream_t s);
 
+// Few row tiles over a long reduction: eight waves of a workgroup split the
+// reduction of one 16 RF x 16 OF tile, each building its weight fragments in
+// registers from the packed entries (bf16 X/vals; FC or stride-1 unpadded
+// 1x1; C % 32 == 0, O % 16 == 0, K <= 4).
+bool split_k_supports(const ProductArgs& a);
+hipError_t launch_split_k(const ProductArgs& a, hipStream_t s);
+
 // Balanced sparsity (groups of G inputs in one output row) and the 2:4
 // sparse matrix-core product.
 hipError_t launch_bbs_pack(const float* W, int64_t O, int64_t C, int32_t G, int32_t K, void* vals, DType val_t,

@@ -73,7 +73,7 @@ int main() {
   EXPECT(std::strlen(cci_last_error()) > 0);
   EXPECT(cci_spmm(A, CCI_BF16, -1, 64, B, CCI_BF16, (const uint8_t*)C, 64, 8, 2, nullptr, D, CCI_BF16, nullptr) == CCI_EINVAL);
   EXPECT(cci_spmm_algo(A, CCI_BF16, 16, 64, B, CCI_BF16, (const uint8_t*)C, 64, 8, 2, nullptr, D, CCI_BF16,
-                       (cci_algo)9, nullptr) == CCI_EINVAL);
+                       (cci_algo)10, nullptr) == CCI_EINVAL);
   EXPECT(cci_conv_im2col(A, CCI_BF16, 1, 2, 2, 32, 3, 3, 1, 1, 0, 0, B, CCI_BF16, (const uint8_t*)C, 64, 8, 2, nullptr,
                          D, CCI_BF16, nullptr) == CCI_EINVAL);
   EXPECT(cci_bbs_pack((const float*)A, 8, 62, 4, 2, B, CCI_BF16, (uint8_t*)C, nullptr) == CCI_EINVAL);

@@ -39,6 +39,12 @@ bool stream_tile_supports(const ProductArgs& a) {
                       a.geom.pw == 0));
 }
 hipError_t launch_stream_tile(const ProductArgs&, hipStream_t) { ++g_launches; return hipSuccess; }
+bool split_k_supports(const ProductArgs& a) {
+  return a.x_t == DType::BF16 && a.val_t == DType::BF16 && a.C % 32 == 0 && a.O % 16 == 0 && a.K <= 4 &&
+         (!a.conv || (a.geom.KH == 1 && a.geom.KW == 1 && a.geom.sh == 1 && a.geom.sw == 1 && a.geom.ph == 0 &&
+                      a.geom.pw == 0));
+}
+hipError_t launch_split_k(const ProductArgs&, hipStream_t) { ++g_launches; return hipSuccess; }
 hipError_t launch_bbs_pack(const float*, int64_t, int64_t, int32_t, int32_t, void*, DType, uint8_t*, hipStream_t) {
   ++g_launches;
   return hipSuccess;

@@ -74,7 +74,7 @@ def test_explicit_algo_requirements():
     assert lib.cci_spmm_algo(FAKE, cci.BF16, 4, 64, FAKE, cci.BF16, FAKE, 24, 6, 2, None, FAKE,
                         cci.BF16, cci.ALGO_SPARSE_MAC, None) == cci.EUNSUPPORTED
     assert lib.cci_spmm_algo(FAKE, cci.BF16, 4, 64, FAKE, cci.BF16, FAKE, 16, 8, 2, None, FAKE,
-                        cci.BF16, 9, None) == cci.EINVAL
+                        cci.BF16, 10, None) == cci.EINVAL
     # wide-tile MFMA: O % 256, C % 64, 64 % G, bf16 only; strided / padded / k x k convs refused
     W = cci.ALGO_WIDE_TILE_MFMA
     assert lib.cci_spmm_algo(FAKE, cci.BF16, 4, 64, FAKE, cci.BF16, FAKE, 128, 8, 2, None, FAKE,
@@ -151,7 +151,20 @@ def test_stream_tile_algo_requirements():
         assert lib.cci_conv_im2col_algo(FAKE, cci.BF16, 1, 8, 8, 64, k, k, stride, stride, pad, pad, FAKE, cci.BF16,
                                         FAKE, 128, 8, 2, None, FAKE, cci.BF16, St, None) == cci.EUNSUPPORTED
     assert lib.cci_spmm_algo(FAKE, cci.BF16, 4, 64, FAKE, cci.BF16, FAKE, 128, 8, 2, None, FAKE,
-                             cci.BF16, 9, None) == cci.EINVAL
+                             cci.BF16, 10, None) == cci.EINVAL
+
+
+def test_split_k_algo_requirements():
+    # split-K MFMA: bf16, FC or stride-1 unpadded 1x1, C % 32 == 0, O % 16 == 0, K <= 4
+    Sk = cci.ALGO_SPLIT_K_MFMA
+    for C, O, G, K in [(48, 64, 8, 2), (960, 24, 8, 2), (960, 160, 8, 5)]:
+        assert lib.cci_spmm_algo(FAKE, cci.BF16, 4, C, FAKE, cci.BF16, FAKE, O, G, K, None, FAKE,
+                                 cci.BF16, Sk, None) == cci.EUNSUPPORTED
+    assert lib.cci_spmm_algo(FAKE, cci.F32, 4, 960, FAKE, cci.F32, FAKE, 160, 8, 2, None, FAKE,
+                             cci.F32, Sk, None) == cci.EUNSUPPORTED
+    for k, stride, pad in [(3, 1, 1), (1, 2, 0), (1, 1, 1)]:
+        assert lib.cci_conv_im2col_algo(FAKE, cci.BF16, 1, 8, 8, 64, k, k, stride, stride, pad, pad, FAKE, cci.BF16,
+                                        FAKE, 128, 8, 2, None, FAKE, cci.BF16, Sk, None) == cci.EUNSUPPORTED
 
 
 def test_few_rows_algo_requirements():
@@ -243,6 +256,18 @@ def test_auto_algo_cost_model():
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 200704, 256, 256, 64, 8, 2) == "dense_tile_mfma"
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 12544, 64, 64, 384, 8, 2) == "dense_tile_mfma"
     assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 12544, 64, 64, 96, 8, 2) == "dense_tile_mfma"
+    # long reductions over few row tiles (MobileNetV2's late projections at batch 64): split-reduction
+    # kernels when 64 x 32 tiles fill one round of the chip, else tap-chunk 64-output tiles (O % 64 == 0);
+    # from 12 544 rows, and for O % 128 == 0, the routes above
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 3136, 960, 960, 160, 8, 2) == "split_k_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 3136, 576, 576, 160, 8, 4) == "split_k_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 3136, 960, 960, 320, 8, 2) == "tap_tile_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 12544, 576, 576, 96, 8, 2) == "dense_tile_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 12544, 384, 384, 64, 8, 2) == "dense_tile_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 3136, 512, 512, 128, 8, 2) == "tap_tile_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 3136, 960, 960, 160, 8, 8) == "dense_tile_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 512, 512, 512, 320, 4, 1) == "split_k_mfma"
+    assert cci.auto_algo(torch.bfloat16, torch.bfloat16, 4096, 512, 512, 96, 16, 4) == "dense_tile_mfma"
 
 
 @pytest.mark.skipif(torch.cuda.is_available(), reason="checks the no-device error path only")

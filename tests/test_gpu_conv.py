@@ -259,6 +259,28 @@ def test_conv_stream_tile_refuses_unsupported():
             cci.conv_im2col(X, vals, idx, 8, k, k, (stride, stride), (pad, pad), algo="stream_tile_mfma")
 
 
+@pytest.mark.parametrize("B,H,W,Cin,O,G,K,y_dtype", [(64, 7, 7, 960, 160, 8, 2, torch.bfloat16),
+                                                     (5, 14, 14, 384, 64, 8, 3, torch.float32),
+                                                     (3, 9, 11, 576, 96, 16, 4, torch.bfloat16)])
+def test_conv_split_k_1x1(B, H, W, Cin, O, G, K, y_dtype):
+    """1x1 stride-1 convolutions on the split-reduction kernels, every epilogue term."""
+    need_gpu()
+    ep = rand_epilogue(O, B * H * W, y_dtype, 97 + Cin, residual=True, relu=True)
+    run_conv(rand_x((B, H, W, Cin), torch.bfloat16, 98 + O), rand_w(O, Cin, 99 + G), G, K, 1, 1, 0, y_dtype,
+             "split_k_mfma", ep=ep)
+
+
+def test_conv_split_k_refuses_unsupported():
+    """3x3, strided or padded 1x1 convolutions are not split-reduction products."""
+    need_gpu()
+    from paper_1910_11971_amd import cci
+    for k, stride, pad in [(3, 1, 1), (1, 2, 0), (1, 1, 1)]:
+        X = rand_x((1, 9, 9, 64), torch.bfloat16, 95).to(DEV)
+        vals, idx = cci.pack(torch.from_numpy(rand_w(128, k * k * 64, 96)).to(DEV), 8, 2, torch.bfloat16)
+        with pytest.raises(cci.CCIError):
+            cci.conv_im2col(X, vals, idx, 8, k, k, (stride, stride), (pad, pad), algo="split_k_mfma")
+
+
 @pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma"])
 def test_conv_epilogue_residual_relu(algo):
     need_gpu()

@@ -1,6 +1,6 @@
 """HIP-graph capture of the hot path (cci_pack + cci_conv_im2col / cci_spmm
-on the dense-tile, sparse-MAC, narrow, wide-tile, streaming and tap-chunk
-kernels): every replay, with eager work and synchronisation in between,
+on the dense-tile, sparse-MAC, narrow, wide-tile, streaming, tap-chunk and
+split-reduction kernels): every replay, with eager work and synchronisation in between,
 reproduces the eager results bit for bit (the kernels are deterministic and
 the library records no memset or allocation into a captured graph)."""
 import numpy as np
@@ -56,6 +56,14 @@ def test_graph_replays_match_eager():
     vt = torch.empty((16, 2, 9 * 128), dtype=torch.bfloat16, device=DEV)
     xt = torch.empty((16, 2, 9 * 128), dtype=torch.uint8, device=DEV)
     Yt = torch.empty((2, 9, 11, 128), dtype=torch.bfloat16, device=DEV)
+    # a split-reduction product (MobileNetV2's 960 -> 160 projection at 7 x 7, one image) with a scale
+    Xk = torch.from_numpy(np.random.default_rng(16).standard_normal((49, 960)).astype(np.float32)).to(
+        torch.bfloat16).to(DEV)
+    Wk = torch.from_numpy((np.random.default_rng(17).standard_normal((160, 960)) / 31).astype(np.float32)).to(DEV)
+    Sk = torch.from_numpy(np.random.default_rng(18).uniform(0.5, 1.5, 160).astype(np.float32)).to(DEV)
+    vk = torch.empty((20, 2, 960), dtype=torch.bfloat16, device=DEV)
+    xk = torch.empty((20, 2, 960), dtype=torch.uint8, device=DEV)
+    Yk = torch.empty((49, 160), dtype=torch.bfloat16, device=DEV)
     s = torch.cuda.Stream()
 
     def step():
@@ -72,12 +80,14 @@ def test_graph_replays_match_eager():
         cci.spmm(Xs2, vs2, xs2, 8, residual=Rs2, relu=True, out=Ys2, algo="stream_tile_mfma")
         cci.pack(Wt, 8, 2, torch.bfloat16, out=(vt, xt))
         cci.conv_im2col(Xt, vt, xt, 8, 3, 3, (1, 1), (1, 1), out=Yt, algo="tap_tile_mfma")
+        cci.pack(Wk, 8, 2, torch.bfloat16, out=(vk, xk))
+        cci.spmm(Xk, vk, xk, 8, scale=Sk, out=Yk, algo="split_k_mfma")
 
     with torch.cuda.stream(s):
         step()
     torch.cuda.synchronize()
     ref = [y.clone() for y in Ys] + [Yf.clone(), vals.clone(), idx.clone(), Yn.clone(), Yw.clone(), Ys2.clone(),
-                                     Yt.clone()]
+                                     Yt.clone(), Yk.clone()]
 
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g, stream=s):
@@ -90,12 +100,13 @@ def test_graph_replays_match_eager():
         Yw.zero_()
         Ys2.zero_()
         Yt.zero_()
+        Yk.zero_()
         vals.zero_()
         torch.cuda.synchronize()
         with torch.cuda.stream(s):
             g.replay()
         torch.cuda.synchronize()
-        got = Ys + [Yf, vals, idx, Yn, Yw, Ys2, Yt]
+        got = Ys + [Yf, vals, idx, Yn, Yw, Ys2, Yt, Yk]
         for a, b in zip(got, ref):
             assert torch.equal(a, b), f"replay {rep} differs from the eager run"
         # eager work between replays, on other data

@@ -168,6 +168,46 @@ def test_spmm_stream_tile_refuses_unsupported():
             cci.spmm(X, vals, idx, G, algo="stream_tile_mfma")
 
 
+SPLIT_K_CASES = [  # N, C, O, G, K
+    # one k-step (seven idle waves), fewer k-steps than waves, a 16-output tile
+    (1, 32, 16, 8, 2), (37, 64, 48, 8, 2), (200, 160, 32, 2, 1),
+    # 32 x 64 tiles; 64 x 32 tiles; 32 x 32 tiles (K = 4); 32 x 16 tiles; ragged last row tiles
+    (9999, 384, 128, 8, 2), (20001, 576, 96, 8, 2), (3136, 960, 320, 8, 4), (3136, 960, 160, 8, 2),
+    (5000, 256, 64, 16, 3), (12544, 512, 64, 32, 1), (3000, 256, 128, 1, 1),
+    # groups straddling 16-output tiles (G = 12), a group wider than the tile (G = 64), K == G
+    (700, 192, 96, 12, 3), (500, 256, 128, 64, 2), (1000, 96, 64, 4, 4),
+    # a reduction of 16 k-steps per wave: four load batches
+    (100, 4096, 64, 16, 4),
+]
+
+
+@pytest.mark.parametrize("N,C,O,G,K", SPLIT_K_CASES)
+def test_spmm_bf16_split_k(N, C, O, G, K):
+    need_gpu()
+    run_case(rand_x(N, C, torch.bfloat16, N + C), rand_w(O, C, O + G), G, K, torch.bfloat16, "split_k_mfma")
+
+
+@pytest.mark.parametrize("N,C,O", [(3136, 960, 160), (3136, 960, 320), (3136, 576, 160), (12544, 576, 96),
+                                   (12544, 384, 64)])
+@pytest.mark.parametrize("y_dtype", [torch.bfloat16, torch.float32])
+def test_spmm_split_k_mobilenetv2_projections(N, C, O, y_dtype):
+    """MobileNetV2's late projecting 1x1 layers at batch 64 (G = 8, K = 2)
+    with batch norm folded into scale / bias and a residual: every output."""
+    need_gpu()
+    ep = rand_epilogue(O, N, y_dtype, N + O, residual=True, relu=False)
+    run_case(rand_x(N, C, torch.bfloat16, C), rand_w(O, C, O), 8, 2, y_dtype, "split_k_mfma", ep=ep)
+
+
+def test_spmm_split_k_refuses_unsupported():
+    need_gpu()
+    from paper_1910_11971_amd import cci
+    for C, O, G, K in ((48, 64, 8, 2), (960, 24, 8, 2), (960, 160, 8, 5)):
+        X = rand_x(300, C, torch.bfloat16, 1).to(DEV)
+        vals, idx = cci.pack(torch.from_numpy(rand_w(O, C, 2)).to(DEV), G, K, torch.bfloat16)
+        with pytest.raises(cci.CCIError):
+            cci.spmm(X, vals, idx, G, algo="split_k_mfma")
+
+
 def test_spmm_wide_tile_repeat_is_identical():
     """Two launches on the same inputs give the same bytes (no state carried between launches)."""
     need_gpu()
@@ -181,7 +221,7 @@ def test_spmm_wide_tile_repeat_is_identical():
 
 
 @pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma", "wide_tile_mfma", "narrow_mfma", "tap_tile_mfma",
-                                  "stream_tile_mfma"])
+                                  "stream_tile_mfma", "split_k_mfma"])
 def test_spmm_bf16_in_f32_out_with_epilogue(algo):
     need_gpu()
     N, C, O, G, K = 777, 128, 256, 8, 2
@@ -190,7 +230,7 @@ def test_spmm_bf16_in_f32_out_with_epilogue(algo):
 
 
 @pytest.mark.parametrize("algo", ["sparse_mac", "dense_tile_mfma", "wide_tile_mfma", "narrow_mfma", "tap_tile_mfma",
-                                  "stream_tile_mfma"])
+                                  "stream_tile_mfma", "split_k_mfma"])
 def test_spmm_bf16_epilogue_bf16_residual(algo):
     need_gpu()
     N, C, O, G, K = 300, 64, 256, 16, 4

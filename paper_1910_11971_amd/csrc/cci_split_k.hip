@@ -7,10 +7,13 @@
 // A workgroup of eight waves owns a tile of 16 RF rows x 16 OF outputs and
 // splits the reduction between its waves: wave w takes the 32-column k-steps
 // w, w + 8, w + 16, ...  A wave issues the loads of up to U of its k-steps at
-// once (X fragments and the packed entries of its outputs), so one memory
-// latency covers its share of the reduction, then multiplies them on
-// v_mfma_f32_16x16x32_bf16.  The eight partial tiles are added through LDS
-// in two rounds, and the fused epilogue (scale, bias, residual, ReLU; one
+// once, so one memory latency covers its share of the reduction, then
+// multiplies them on v_mfma_f32_16x16x32_bf16.  When the packed rows of the
+// tile's groups fit in LDS beside the partial tiles (WL), the workgroup
+// copies them there once, while its first X loads are in flight, and the
+// waves load only X per k-step; otherwise each lane also loads its own
+// group's packed entries.  The eight partial tiles are added through LDS in
+// two rounds, and the fused epilogue (scale, bias, residual, ReLU; one
 // rounding) writes 8 outputs per thread.
 //
 // Weight fragments are built in registers, never in memory.  The A operand
@@ -56,8 +59,15 @@ struct KParams {
 
 // k-steps whose loads a wave keeps in flight together: as many as fit about
 // 128 registers of operands.
-constexpr int batch_steps(int rf, int of, int k) {
-  return 128 / (4 * rf + 6 * of * k) < 1 ? 1 : (128 / (4 * rf + 6 * of * k) > 4 ? 4 : 128 / (4 * rf + 6 * of * k));
+// (With the packed rows staged in LDS only X is loaded per k-step; 128-row
+// tiles then keep 96 registers of it beside their 64 accumulators.)
+constexpr int batch_budget(int rf, bool wl) { return wl && rf == 8 ? 96 : 128; }
+constexpr int batch_steps(int rf, int of, int k, bool wl) {
+  return batch_budget(rf, wl) / (4 * rf + (wl ? 0 : 6 * of * k)) < 1
+             ? 1
+             : (batch_budget(rf, wl) / (4 * rf + (wl ? 0 : 6 * of * k)) > 4
+                    ? 4
+                    : batch_budget(rf, wl) / (4 * rf + (wl ? 0 : 6 * of * k)));
 }
 
 // 64 x 64 tiles hold 64 accumulator registers: only K = 1 leaves room for
@@ -89,11 +99,13 @@ struct Step {
   u32x2_t i[OF][K];
 };
 
-template <int RF, int OF, int K, typename YT>
+template <int RF, int OF, int K, bool WL, typename YT>
 __global__ __launch_bounds__(kThreads) void split_k_kernel(KParams p) {
   constexpr int TR = 16 * RF, TO = 16 * OF, PITCH = TO + 4;
-  constexpr int U = batch_steps(RF, OF, K);
+  constexpr int U = batch_steps(RF, OF, K, WL);
   __shared__ __attribute__((aligned(16))) float red[4][TR][PITCH];
+  // WL: the packed rows of the tile's groups, values then indices
+  extern __shared__ __attribute__((aligned(16))) uint8_t wlds[];
 
   // workgroup b runs on XCD b % 8: each XCD takes a contiguous run of tiles,
   // so the output blocks of one row block share that XCD's L2 copy of X
@@ -105,7 +117,9 @@ __global__ __launch_bounds__(kThreads) void split_k_kernel(KParams p) {
   const int32_t lr = lane % 16, lq = lane / 16;
   const int32_t n0 = rb * TR, o0 = ob * TO;
 
-  // per output fragment: the lane's group row base and slot
+  // per output fragment: the lane's group row base (in the packed arrays, or
+  // in the staged copy of groups g_lo ..) and slot
+  const int32_t g_lo = o0 / p.G;
   int64_t gbase[OF];
   uint32_t rrx[OF];
 #pragma unroll
@@ -113,7 +127,7 @@ __global__ __launch_bounds__(kThreads) void split_k_kernel(KParams p) {
     const int32_t o = o0 + 16 * f + lr;
     const int32_t g = o / p.G;
     rrx[f] = static_cast<uint32_t>(o - g * p.G) * 0x01010101u;
-    gbase[f] = static_cast<int64_t>(g) * K * p.C;
+    gbase[f] = static_cast<int64_t>(WL ? g - g_lo : g) * K * p.C;
   }
   // X rows past N read row N - 1 (their sums are never stored)
   const uint16_t* xrow[RF];
@@ -130,37 +144,67 @@ __global__ __launch_bounds__(kThreads) void split_k_kernel(KParams p) {
     for (int f = 0; f < OF; ++f) acc[r][f] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   const int32_t nks = p.C / 32;
-  for (int32_t s0 = w; s0 < nks; s0 += kWaves * U) {
-    Step<RF, OF, K> st[U];
+  Step<RF, OF, K> st[U];
+  const auto load_batch = [&](int32_t s0) {
+#pragma unroll
+    for (int j = 0; j < U; ++j) {
+      const int32_t s = s0 + kWaves * j;
+      if (s < nks) {
+#pragma unroll
+        for (int r = 0; r < RF; ++r) st[j].x[r] = *reinterpret_cast<const u32x4_t*>(xrow[r] + 32 * s);
+        if (!WL) {
+          const int32_t c0 = 32 * s + 8 * lq;
+#pragma unroll
+          for (int f = 0; f < OF; ++f)
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+              const int64_t e = gbase[f] + static_cast<int64_t>(k) * p.C + c0;
+              st[j].v[f][k] = *reinterpret_cast<const u32x4_t*>(p.vals + e);
+              st[j].i[f][k] = *reinterpret_cast<const u32x2_t*>(p.idx + e);
+            }
+        }
+      }
+    }
+  };
+  int32_t s0 = w;
+  load_batch(s0);
+  // WL: copy the packed rows of groups g_lo .. g_hi (contiguous in both
+  // arrays) while the first X batch is in flight
+  const int32_t nel = WL ? ((min(o0 + TO, p.O) - 1) / p.G - g_lo + 1) * K * p.C : 0;
+  if (WL) {
+    const int64_t e0 = static_cast<int64_t>(g_lo) * K * p.C;
+    const int32_t tid = static_cast<int32_t>(threadIdx.x);
+    for (int32_t q = tid; q < nel / 8; q += kThreads)
+      *reinterpret_cast<u32x4_t*>(wlds + 16 * q) = *reinterpret_cast<const u32x4_t*>(p.vals + e0 + 8 * q);
+    for (int32_t q = tid; q < nel / 16; q += kThreads)
+      *reinterpret_cast<u32x4_t*>(wlds + 2 * nel + 16 * q) = *reinterpret_cast<const u32x4_t*>(p.idx + e0 + 16 * q);
+    __syncthreads();
+  }
+  while (true) {
 #pragma unroll
     for (int j = 0; j < U; ++j) {
       const int32_t s = s0 + kWaves * j;
       if (s < nks) {
         const int32_t c0 = 32 * s + 8 * lq;
 #pragma unroll
-        for (int r = 0; r < RF; ++r) st[j].x[r] = *reinterpret_cast<const u32x4_t*>(xrow[r] + 32 * s);
-#pragma unroll
-        for (int f = 0; f < OF; ++f)
-#pragma unroll
-          for (int k = 0; k < K; ++k) {
-            const int64_t e = gbase[f] + static_cast<int64_t>(k) * p.C + c0;
-            st[j].v[f][k] = *reinterpret_cast<const u32x4_t*>(p.vals + e);
-            st[j].i[f][k] = *reinterpret_cast<const u32x2_t*>(p.idx + e);
-          }
-      }
-    }
-#pragma unroll
-    for (int j = 0; j < U; ++j) {
-      if (s0 + kWaves * j < nks) {
-#pragma unroll
         for (int f = 0; f < OF; ++f) {
           u32x4_t a = u32x4_t{0u, 0u, 0u, 0u};
 #pragma unroll
           for (int k = 0; k < K; ++k) {
+            u32x4_t v;
+            u32x2_t ix;
+            if (WL) {
+              const int32_t le = static_cast<int32_t>(gbase[f]) + k * p.C + c0;
+              v = *reinterpret_cast<const u32x4_t*>(wlds + 2 * le);
+              ix = *reinterpret_cast<const u32x2_t*>(wlds + 2 * nel + le);
+            } else {
+              v = st[j].v[f][k];
+              ix = st[j].i[f][k];
+            }
             uint32_t m[4];
-            slot_masks(st[j].i[f][k][0], st[j].i[f][k][1], rrx[f], m);
+            slot_masks(ix[0], ix[1], rrx[f], m);
 #pragma unroll
-            for (int d = 0; d < 4; ++d) a[d] |= st[j].v[f][k][d] & m[d];
+            for (int d = 0; d < 4; ++d) a[d] |= v[d] & m[d];
           }
           const bf16x8_t av = __builtin_bit_cast(bf16x8_t, a);
 #pragma unroll
@@ -170,6 +214,9 @@ __global__ __launch_bounds__(kThreads) void split_k_kernel(KParams p) {
         }
       }
     }
+    s0 += kWaves * U;
+    if (s0 >= nks) break;
+    load_batch(s0);
   }
 
   // ---- add the eight partial tiles: waves 4..7 into 0..3, then 0..3 in LDS.
@@ -266,27 +313,59 @@ __global__ __launch_bounds__(kThreads) void split_k_kernel(KParams p) {
   }
 }
 
+constexpr int64_t kLdsMax = 160 * 1024;
+
+constexpr int64_t red_bytes(int rf, int of) { return 4 * (16 * rf) * (16 * of + 4) * 4; }
+
+// Groups one output block of TO outputs touches, at most: TO / G when G
+// divides TO, one when TO divides G, else every alignment's worst case.
+int64_t block_groups(int64_t TO, int64_t G) {
+  if (TO % G == 0) return TO / G;
+  if (G % TO == 0) return 1;
+  return (TO + G - 2) / G + 1;
+}
+
+// Bytes of the staged packed rows (values and indices) of one output block.
+int64_t staged_bytes(int rf, int of, int64_t C, int32_t G, int32_t K) {
+  (void)rf;
+  return 3 * block_groups(16 * of, G) * K * C;
+}
+
+template <int RF, int OF, int K, bool WL>
+hipError_t launch_rokw(const KParams& p, int64_t dyn, DType y_t, hipStream_t s) {
+  const uint32_t grid = static_cast<uint32_t>(p.tpx) * kXcds;
+  static std::atomic<int8_t> lds_set[2][kMaxDevices];
+  const auto kf = &split_k_kernel<RF, OF, K, WL, float>;
+  const auto kb = &split_k_kernel<RF, OF, K, WL, bf16_t>;
+  if (WL) {
+    const int limit = static_cast<int>(kLdsMax - red_bytes(RF, OF));
+    const hipError_t e = y_t == DType::F32 ? set_lds_limit_once(lds_set[0], reinterpret_cast<const void*>(kf), limit)
+                                           : set_lds_limit_once(lds_set[1], reinterpret_cast<const void*>(kb), limit);
+    if (e != hipSuccess) return e;
+  }
+  if (y_t == DType::F32)
+    hipLaunchKernelGGL(kf, dim3(grid), dim3(kThreads), static_cast<uint32_t>(dyn), s, p);
+  else
+    hipLaunchKernelGGL(kb, dim3(grid), dim3(kThreads), static_cast<uint32_t>(dyn), s, p);
+  return hipGetLastError();
+}
+
 template <int RF, int OF, int K>
-hipError_t launch_rok(const KParams& p, DType y_t, hipStream_t s) {
+hipError_t launch_rok(const KParams& p, bool wl, int64_t dyn, DType y_t, hipStream_t s) {
   if constexpr (!tile_fits(RF, OF, K)) {
     return hipErrorInvalidConfiguration;
   } else {
-    const uint32_t grid = static_cast<uint32_t>(p.tpx) * kXcds;
-    if (y_t == DType::F32)
-      hipLaunchKernelGGL((split_k_kernel<RF, OF, K, float>), dim3(grid), dim3(kThreads), 0, s, p);
-    else
-      hipLaunchKernelGGL((split_k_kernel<RF, OF, K, bf16_t>), dim3(grid), dim3(kThreads), 0, s, p);
-    return hipGetLastError();
+    return wl ? launch_rokw<RF, OF, K, true>(p, dyn, y_t, s) : launch_rokw<RF, OF, K, false>(p, 0, y_t, s);
   }
 }
 
 template <int RF, int OF>
-hipError_t launch_ro(const KParams& p, int32_t K, DType y_t, hipStream_t s) {
+hipError_t launch_ro(const KParams& p, int32_t K, bool wl, int64_t dyn, DType y_t, hipStream_t s) {
   switch (K) {
-    case 1: return launch_rok<RF, OF, 1>(p, y_t, s);
-    case 2: return launch_rok<RF, OF, 2>(p, y_t, s);
-    case 3: return launch_rok<RF, OF, 3>(p, y_t, s);
-    case 4: return launch_rok<RF, OF, 4>(p, y_t, s);
+    case 1: return launch_rok<RF, OF, 1>(p, wl, dyn, y_t, s);
+    case 2: return launch_rok<RF, OF, 2>(p, wl, dyn, y_t, s);
+    case 3: return launch_rok<RF, OF, 3>(p, wl, dyn, y_t, s);
+    case 4: return launch_rok<RF, OF, 4>(p, wl, dyn, y_t, s);
     default: return hipErrorInvalidConfiguration;
   }
 }
@@ -299,7 +378,7 @@ hipError_t launch_ro(const KParams& p, int32_t K, DType y_t, hipStream_t s) {
 // workgroup per CU (two waves per SIMD) the grid runs in ceil(tiles / 256)
 // rounds; X is re-read once per output block from L2 (~20 TB/s over the
 // chip).
-void split_k_tile(int64_t N, int64_t C, int64_t O, int32_t K, int32_t& rf, int32_t& of) {
+void split_k_tile(int64_t N, int64_t C, int64_t O, int32_t G, int32_t K, int32_t& rf, int32_t& of) {
   static const int32_t cand[6][2] = {{8, 2}, {4, 4}, {2, 4}, {4, 2}, {2, 2}, {2, 1}};
   double best = 1e300;
   rf = 2;
@@ -309,7 +388,8 @@ void split_k_tile(int64_t N, int64_t C, int64_t O, int32_t K, int32_t& rf, int32
     if (O % (16 * c[1]) != 0 || !tile_fits(c[0], c[1], K)) continue;
     const int64_t nob = O / (16 * c[1]);
     const int64_t tiles = (N + 16 * c[0] - 1) / (16 * c[0]) * nob;
-    const int64_t u = batch_steps(c[0], c[1], K);
+    const bool wl = red_bytes(c[0], c[1]) + staged_bytes(c[0], c[1], C, G, K) <= kLdsMax;
+    const int64_t u = batch_steps(c[0], c[1], K, wl);
     const int64_t batches = (per_wave + u - 1) / u;
     const double rounds = static_cast<double>((tiles + 255) / 256);
     const double wg_bytes = static_cast<double>(16 * c[0]) * C * 2 + static_cast<double>(16 * c[1]) * C * K * 3 / 2;
@@ -342,7 +422,7 @@ bool split_k_supports(const ProductArgs& a) {
 hipError_t launch_split_k(const ProductArgs& a, hipStream_t s) {
   if (!split_k_supports(a)) return hipErrorInvalidConfiguration;
   int32_t rf, of;
-  split_k_tile(a.N, a.C, a.O, a.K, rf, of);
+  split_k_tile(a.N, a.C, a.O, a.G, a.K, rf, of);
   KParams p{};
   p.X = static_cast<const uint16_t*>(a.X);
   p.vals = static_cast<const uint16_t*>(a.vals);
@@ -361,12 +441,15 @@ hipError_t launch_split_k(const ProductArgs& a, hipStream_t s) {
   if (tiles > (int64_t(1) << 30)) return hipErrorInvalidConfiguration;
   p.tiles = static_cast<int32_t>(tiles);
   p.tpx = static_cast<int32_t>((tiles + kXcds - 1) / kXcds);
-  if (rf == 8 && of == 2) return launch_ro<8, 2>(p, a.K, a.y_t, s);
-  if (rf == 4 && of == 4) return launch_ro<4, 4>(p, a.K, a.y_t, s);
-  if (rf == 4 && of == 2) return launch_ro<4, 2>(p, a.K, a.y_t, s);
-  if (rf == 2 && of == 4) return launch_ro<2, 4>(p, a.K, a.y_t, s);
-  if (rf == 2 && of == 2) return launch_ro<2, 2>(p, a.K, a.y_t, s);
-  return launch_ro<2, 1>(p, a.K, a.y_t, s);
+  // the packed rows of a block go to LDS when they fit beside the partial tiles
+  const int64_t dyn = staged_bytes(rf, of, a.C, a.G, a.K);
+  const bool wl = red_bytes(rf, of) + dyn <= kLdsMax;
+  if (rf == 8 && of == 2) return launch_ro<8, 2>(p, a.K, wl, dyn, a.y_t, s);
+  if (rf == 4 && of == 4) return launch_ro<4, 4>(p, a.K, wl, dyn, a.y_t, s);
+  if (rf == 4 && of == 2) return launch_ro<4, 2>(p, a.K, wl, dyn, a.y_t, s);
+  if (rf == 2 && of == 4) return launch_ro<2, 4>(p, a.K, wl, dyn, a.y_t, s);
+  if (rf == 2 && of == 2) return launch_ro<2, 2>(p, a.K, wl, dyn, a.y_t, s);
+  return launch_ro<2, 1>(p, a.K, wl, dyn, a.y_t, s);
 }
 
 }  // namespace cci

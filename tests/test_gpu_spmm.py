@@ -187,6 +187,20 @@ def test_spmm_bf16_split_k(N, C, O, G, K):
     run_case(rand_x(N, C, torch.bfloat16, N + C), rand_w(O, C, O + G), G, K, torch.bfloat16, "split_k_mfma")
 
 
+# Packed rows of a tile's groups too large for LDS beside the partial tiles
+# (many small groups over a long reduction): every lane loads its own group's
+# entries per k-step.  32 x 16, 32 x 32, 64 x 32 and 128 x 32 tiles, with
+# 2 to 6 load batches per wave.
+SPLIT_K_DIRECT_CASES = [(300, 3264, 16, 2, 2), (2000, 2048, 64, 2, 2), (5000, 1344, 64, 2, 2),
+                        (5000, 1344, 128, 4, 4)]
+
+
+@pytest.mark.parametrize("N,C,O,G,K", SPLIT_K_DIRECT_CASES)
+def test_spmm_bf16_split_k_direct_loads(N, C, O, G, K):
+    need_gpu()
+    run_case(rand_x(N, C, torch.bfloat16, N + C), rand_w(O, C, O + G), G, K, torch.bfloat16, "split_k_mfma")
+
+
 @pytest.mark.parametrize("N,C,O", [(3136, 960, 160), (3136, 960, 320), (3136, 576, 160), (12544, 576, 96),
                                    (12544, 384, 64)])
 @pytest.mark.parametrize("y_dtype", [torch.bfloat16, torch.float32])

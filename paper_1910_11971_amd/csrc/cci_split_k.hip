@@ -104,6 +104,7 @@ __global__ __launch_bounds__(kThreads) void split_k_kernel(KParams p) {
   constexpr int TR = 16 * RF, TO = 16 * OF, PITCH = TO + 4;
   constexpr int U = batch_steps(RF, OF, K, WL);
   __shared__ __attribute__((aligned(16))) float red[4][TR][PITCH];
+  __shared__ __attribute__((aligned(16))) float sb[2][TO];  // the tile's scale and bias
   // WL: the packed rows of the tile's groups, values then indices
   extern __shared__ __attribute__((aligned(16))) uint8_t wlds[];
 
@@ -168,6 +169,16 @@ __global__ __launch_bounds__(kThreads) void split_k_kernel(KParams p) {
   };
   int32_t s0 = w;
   load_batch(s0);
+  // scale and bias of the tile's outputs to LDS now, not one round trip after
+  // the reduction (the barriers below publish them)
+  {
+    const int32_t tid = static_cast<int32_t>(threadIdx.x);
+    if (p.scale && tid < TO / 4)
+      *reinterpret_cast<f32x4_t*>(&sb[0][4 * tid]) = *reinterpret_cast<const f32x4_t*>(p.scale + o0 + 4 * tid);
+    if (p.bias && tid >= TO / 4 && tid < TO / 2)
+      *reinterpret_cast<f32x4_t*>(&sb[1][4 * tid - TO]) =
+          *reinterpret_cast<const f32x4_t*>(p.bias + o0 + 4 * tid - TO);
+  }
   // WL: copy the packed rows of groups g_lo .. g_hi (contiguous in both
   // arrays) while the first X batch is in flight
   const int32_t nel = WL ? ((min(o0 + TO, p.O) - 1) / p.G - g_lo + 1) * K * p.C : 0;
@@ -257,17 +268,17 @@ __global__ __launch_bounds__(kThreads) void split_k_kernel(KParams p) {
     for (int e = 0; e < 4; ++e) y[4 * h + e] = sum[e];
   }
   if (p.scale) {
-    const f32x4_t s0 = *reinterpret_cast<const f32x4_t*>(p.scale + o);
-    const f32x4_t s1 = *reinterpret_cast<const f32x4_t*>(p.scale + o + 4);
+    const f32x4_t sc0 = *reinterpret_cast<const f32x4_t*>(&sb[0][ol]);
+    const f32x4_t sc1 = *reinterpret_cast<const f32x4_t*>(&sb[0][ol + 4]);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      y[e] *= s0[e];
-      y[4 + e] *= s1[e];
+      y[e] *= sc0[e];
+      y[4 + e] *= sc1[e];
     }
   }
   if (p.bias) {
-    const f32x4_t b0 = *reinterpret_cast<const f32x4_t*>(p.bias + o);
-    const f32x4_t b1 = *reinterpret_cast<const f32x4_t*>(p.bias + o + 4);
+    const f32x4_t b0 = *reinterpret_cast<const f32x4_t*>(&sb[1][ol]);
+    const f32x4_t b1 = *reinterpret_cast<const f32x4_t*>(&sb[1][ol + 4]);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       y[e] += b0[e];
@@ -315,7 +326,8 @@ __global__ __launch_bounds__(kThreads) void split_k_kernel(KParams p) {
 
 constexpr int64_t kLdsMax = 160 * 1024;
 
-constexpr int64_t red_bytes(int rf, int of) { return 4 * (16 * rf) * (16 * of + 4) * 4; }
+// Static LDS of a tile shape: the partial tiles and the scale / bias rows.
+constexpr int64_t red_bytes(int rf, int of) { return 4 * (16 * rf) * (16 * of + 4) * 4 + 2 * (16 * of) * 4; }
 
 // Groups one output block of TO outputs touches, at most: TO / G when G
 // divides TO, one when TO divides G, else every alignment's worst case.

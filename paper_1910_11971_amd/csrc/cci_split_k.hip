@@ -338,10 +338,7 @@ int64_t block_groups(int64_t TO, int64_t G) {
 }
 
 // Bytes of the staged packed rows (values and indices) of one output block.
-int64_t staged_bytes(int rf, int of, int64_t C, int32_t G, int32_t K) {
-  (void)rf;
-  return 3 * block_groups(16 * of, G) * K * C;
-}
+int64_t staged_bytes(int of, int64_t C, int32_t G, int32_t K) { return 3 * block_groups(16 * of, G) * K * C; }
 
 template <int RF, int OF, int K, bool WL>
 hipError_t launch_rokw(const KParams& p, int64_t dyn, DType y_t, hipStream_t s) {
@@ -390,7 +387,7 @@ hipError_t launch_ro(const KParams& p, int32_t K, bool wl, int64_t dyn, DType y_
 // workgroup per CU (two waves per SIMD) the grid runs in ceil(tiles / 256)
 // rounds; X is re-read once per output block from L2 (~20 TB/s over the
 // chip).
-void split_k_tile(int64_t N, int64_t C, int64_t O, int32_t G, int32_t K, int32_t& rf, int32_t& of) {
+static void split_k_tile(int64_t N, int64_t C, int64_t O, int32_t G, int32_t K, int32_t& rf, int32_t& of) {
   static const int32_t cand[6][2] = {{8, 2}, {4, 4}, {2, 4}, {4, 2}, {2, 2}, {2, 1}};
   double best = 1e300;
   rf = 2;
@@ -400,7 +397,7 @@ void split_k_tile(int64_t N, int64_t C, int64_t O, int32_t G, int32_t K, int32_t
     if (O % (16 * c[1]) != 0 || !tile_fits(c[0], c[1], K)) continue;
     const int64_t nob = O / (16 * c[1]);
     const int64_t tiles = (N + 16 * c[0] - 1) / (16 * c[0]) * nob;
-    const bool wl = red_bytes(c[0], c[1]) + staged_bytes(c[0], c[1], C, G, K) <= kLdsMax;
+    const bool wl = red_bytes(c[0], c[1]) + staged_bytes(c[1], C, G, K) <= kLdsMax;
     const int64_t u = batch_steps(c[0], c[1], K, wl);
     const int64_t batches = (per_wave + u - 1) / u;
     const double rounds = static_cast<double>((tiles + 255) / 256);
@@ -454,7 +451,7 @@ hipError_t launch_split_k(const ProductArgs& a, hipStream_t s) {
   p.tiles = static_cast<int32_t>(tiles);
   p.tpx = static_cast<int32_t>((tiles + kXcds - 1) / kXcds);
   // the packed rows of a block go to LDS when they fit beside the partial tiles
-  const int64_t dyn = staged_bytes(rf, of, a.C, a.G, a.K);
+  const int64_t dyn = staged_bytes(of, a.C, a.G, a.K);
   const bool wl = red_bytes(rf, of) + dyn <= kLdsMax;
   if (rf == 8 && of == 2) return launch_ro<8, 2>(p, a.K, wl, dyn, a.y_t, s);
   if (rf == 4 && of == 4) return launch_ro<4, 4>(p, a.K, wl, dyn, a.y_t, s);
